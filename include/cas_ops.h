@@ -1,0 +1,85 @@
+/*
+ * cas_ops.h - kernel-level entry points of the CAS-Spec tree decoder library,
+ * on caller-owned DEVICE buffers.
+ *
+ * These expose single kernels of the forward of cas.h so that each can be
+ * checked against a CPU definition on identical inputs, and timed alone.
+ * All pointers are device pointers (except where noted) owned by the caller;
+ * `stream` is a hipStream_t (NULL = the null stream).  Every call is
+ * asynchronous on that stream and returns CAS_ERR_ARG / CAS_ERR_UNSUPPORTED
+ * for shapes it does not handle, CAS_ERR_DEVICE if the launch fails.
+ */
+#ifndef CAS_OPS_H
+#define CAS_OPS_H
+
+#include "cas.h"
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum { CAS_W_F32 = 0, CAS_W_BF16 = 1, CAS_W_I8 = 2 } cas_wtype;
+typedef enum {
+    CAS_EPI_STORE = 0,   /* out[t*ldo + n] = y (float32) */
+    CAS_EPI_RESID = 1,   /* out[t*ldo + n] += y (float32 residual stream) */
+    CAS_EPI_RAW_I32 = 2  /* out[t*ldo + n] = integer accumulator (int32; int8 only) */
+} cas_epi;
+
+/*
+ * Linear layer y[t][n] = sum_k X[t][k] W[n][k] for t < T, n < N (the weight
+ * streaming GEMM of every projection and the LM head).
+ *   W: [N][K] row-major, element type wtype (float32, bf16 bits, int8)
+ *   X: [T][K] row-major, same element type as W
+ *   xs, ws: for CAS_W_I8 the per-row activation scales [T] and per-output
+ *           channel weight scales [N]; y = (float(acc) * xs[t]) * ws[n]
+ *           (ignored for the other types; unused with CAS_EPI_RAW_I32)
+ * Limits: N multiple of 16, K multiple of 16, 1 <= T <= 128.
+ * Accumulation: fp32 (float32, bf16 inputs), exact int32 (int8 inputs).
+ */
+cas_status cas_op_gemm(int32_t wtype, const void* W, const void* X, int32_t N, int32_t K, int32_t T,
+                       const float* xs, const float* ws, int32_t epi, void* out, int32_t ldo,
+                       void* stream);
+
+/*
+ * Per-row symmetric int8 quantisation of activations (App. C, activation
+ * quantisation; one row per token): s[t] = max_k |x[t][k]| / 127 (fp32),
+ * q[t][k] = clamp(round-half-even(x[t][k] / s[t]), -127, 127); a zero row
+ * gives s = 0, q = 0.  x: [T][K] of type atype (CAS_W_F32 or CAS_W_BF16).
+ */
+cas_status cas_op_quant_rows(int32_t atype, const void* x, int32_t T, int32_t K,
+                             int8_t* q, float* s, void* stream);
+
+/* Per-output-channel int8 copy of W [N][K] (same rule, one row per output
+ * channel).  wtype: CAS_W_F32 or CAS_W_BF16. */
+cas_status cas_op_quant_weight(int32_t wtype, const void* W, int32_t N, int32_t K,
+                               int8_t* q, float* s, void* stream);
+
+/*
+ * Tree-masked attention of one layer (bf16 storage, fp32 softmax):
+ *   q:   [T][n_heads][head_dim] bf16 (after RoPE)
+ *   kc:  [n_kv_heads][ctx_cap][head_dim] bf16 key cache
+ *   vt:  [n_kv_heads][head_dim][ctx_cap] bf16 value cache, slot-contiguous
+ *   anc: [T][2] 64-bit ancestor-or-self masks over the round's nodes
+ *        (bit j = node j, whose slot is Lc + j)
+ *   out: [T][n_heads*head_dim] bf16
+ * Query row t sees slots [0, Lc) and the slots Lc + j of the nodes j set in
+ * anc[t]; n_tree nodes exist (Lc + n_tree <= ctx_cap, n_tree <= 128;
+ * ctx_cap a multiple of 32: key tiles of 32 slots are read whole).
+ * head_dim 64 or 128; T <= 128.  Uses `work` (device, at least
+ * cas_op_attention_work_bytes(...) bytes) for split partial results.
+ */
+cas_status cas_op_attention(const void* q, const void* kc, const void* vt, int32_t ctx_cap,
+                            int32_t Lc, int32_t n_tree, int32_t T, int32_t n_heads,
+                            int32_t n_kv_heads, int32_t head_dim, const uint64_t* anc,
+                            void* out, void* work, size_t work_bytes, void* stream);
+size_t cas_op_attention_work_bytes(int32_t Lc, int32_t n_tree, int32_t T, int32_t n_heads,
+                                   int32_t head_dim);
+
+/* Plain device copy kernel (16-byte vector loads and stores): the reference
+ * traffic for calibrating HBM byte counters.  bytes must be a multiple of 16. */
+cas_status cas_op_copy(void* dst, const void* src, size_t bytes, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* CAS_OPS_H */

@@ -1,0 +1,290 @@
+"""ctypes binding of libcas.so (include/cas.h, include/cas_ops.h).
+
+Argument marshalling only: every step of the decoder forward, acceptance and
+compaction runs in the library's HIP kernels.  The binding refuses to run
+without the built library; there is no fallback of any kind.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Dict, List, Optional, Sequence, Tuple
+
+import numpy as np
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libcas.so")
+_lib = None
+
+# status codes (cas_status)
+OK, ERR_ARG, ERR_TREE, ERR_CAPACITY, ERR_UNSUPPORTED, ERR_OOM, ERR_DEVICE, ERR_STATE = range(8)
+STATUS_NAMES = ["CAS_OK", "CAS_ERR_ARG", "CAS_ERR_TREE", "CAS_ERR_CAPACITY", "CAS_ERR_UNSUPPORTED",
+                "CAS_ERR_OOM", "CAS_ERR_DEVICE", "CAS_ERR_STATE"]
+F32, BF16 = 0, 1
+W_F32, W_BF16, W_I8 = 0, 1, 2
+EPI_STORE, EPI_RESID, EPI_RAW_I32 = 0, 1, 2
+TENSOR = {"embed": 0, "lm_head": 1, "final_norm": 2, "attn_norm": 3, "ffn_norm": 4, "wq": 5, "wk": 6,
+          "wv": 7, "wo": 8, "w_gate": 9, "w_up": 10, "w_down": 11}
+KCLASS = ["embed", "rmsnorm", "gemm_qkv", "attn", "attn_combine", "gemm_o", "gemm_gateup", "gemm_down",
+          "gemm_head", "quant", "accept", "compact"]
+
+# every symbol the two headers declare
+EXPORTS = ("cas_create", "cas_destroy", "cas_last_error", "cas_create_error", "cas_load_tensor", "cas_build_int8",
+           "cas_prefill", "cas_kv_load", "cas_kv_read", "cas_set_committed", "cas_committed_len", "cas_forward",
+           "cas_logits_device", "cas_accept_tree", "cas_kv_compact", "cas_tree_info", "cas_set_graphs",
+           "cas_profile", "cas_profile_read", "cas_sync", "cas_op_gemm", "cas_op_quant_rows",
+           "cas_op_quant_weight", "cas_op_attention", "cas_op_attention_work_bytes", "cas_op_copy")
+
+
+class CasError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        name = STATUS_NAMES[status] if 0 <= status < len(STATUS_NAMES) else str(status)
+        super().__init__(f"{name}: {msg}")
+        self.status = status
+
+
+class Config(ctypes.Structure):
+    _fields_ = [("n_layers", ctypes.c_int32), ("d_model", ctypes.c_int32), ("n_heads", ctypes.c_int32),
+                ("n_kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32), ("ffn_dim", ctypes.c_int32),
+                ("vocab", ctypes.c_int32), ("rope_theta", ctypes.c_float), ("rms_eps", ctypes.c_float),
+                ("dtype", ctypes.c_int32), ("max_ctx", ctypes.c_int32), ("max_tree", ctypes.c_int32)]
+
+
+def lib():
+    """Load libcas.so; raises if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is not built: run `python -c 'import __graft_entry__ as g; g.build()'`")
+        L = ctypes.CDLL(LIB_PATH)
+        P, I, Z = ctypes.c_void_p, ctypes.c_int32, ctypes.c_size_t
+        sig = {
+            "cas_create": ([P, ctypes.c_int, P, P], I),
+            "cas_destroy": ([P], None),
+            "cas_last_error": ([P], ctypes.c_char_p),
+            "cas_create_error": ([], ctypes.c_char_p),
+            "cas_load_tensor": ([P, I, I, P, Z], I),
+            "cas_build_int8": ([P], I),
+            "cas_prefill": ([P, P, I], I),
+            "cas_kv_load": ([P, I, P, P, I], I),
+            "cas_kv_read": ([P, I, P, P, I], I),
+            "cas_set_committed": ([P, I], I),
+            "cas_committed_len": ([P, P], I),
+            "cas_forward": ([P, P, P, I, I, P, I, P], I),
+            "cas_logits_device": ([P, P, P], I),
+            "cas_accept_tree": ([P, I, P, P, P], I),
+            "cas_kv_compact": ([P, P, I], I),
+            "cas_tree_info": ([P, I, P, P], I),
+            "cas_set_graphs": ([P, I], I),
+            "cas_profile": ([P, I], I),
+            "cas_profile_read": ([P, P, P, I], I),
+            "cas_sync": ([P], I),
+            "cas_op_gemm": ([I, P, P, I, I, I, P, P, I, P, I, P], I),
+            "cas_op_quant_rows": ([I, P, I, I, P, P, P], I),
+            "cas_op_quant_weight": ([I, P, I, I, P, P, P], I),
+            "cas_op_attention": ([P, P, P, I, I, I, I, I, I, I, P, P, P, Z, P], I),
+            "cas_op_attention_work_bytes": ([I, I, I, I, I], Z),
+            "cas_op_copy": ([P, P, Z, P], I),
+        }
+        for name, (args, res) in sig.items():
+            fn = getattr(L, name)
+            fn.argtypes = args
+            fn.restype = res
+        _lib = L
+    return _lib
+
+
+def _p(a: np.ndarray) -> int:
+    return a.ctypes.data
+
+
+def tree_info(parents: Sequence[int]) -> Tuple[np.ndarray, np.ndarray]:
+    """Depth and 128-bit ancestor-or-self masks ([n][2] uint64) as the library computes them."""
+    par = np.ascontiguousarray(parents, dtype=np.int32)
+    n = par.shape[0]
+    depth = np.zeros(n, dtype=np.int32)
+    anc = np.zeros((n, 2), dtype=np.uint64)
+    st = lib().cas_tree_info(_p(par), n, _p(depth), _p(anc))
+    if st:
+        raise CasError(st, "invalid parent list")
+    return depth, anc
+
+
+class Model:
+    """One decoder context (weights, KV cache, round state) on one GPU."""
+
+    def __init__(self, shape, max_ctx: int, max_tree: int = 128, device: int = 0, stream: Optional[int] = None):
+        self.shape = shape
+        self.bf16 = shape.dtype == "bf16"
+        cfg = Config(shape.n_layers, shape.d_model, shape.n_heads, shape.n_kv_heads, shape.head_dim, shape.ffn_dim,
+                     shape.vocab, float(shape.rope_theta), float(shape.rms_eps), BF16 if self.bf16 else F32,
+                     int(max_ctx), int(max_tree))
+        self.max_ctx, self.max_tree = int(max_ctx), int(max_tree)
+        h = ctypes.c_void_p()
+        st = lib().cas_create(ctypes.byref(cfg), int(device), stream, ctypes.byref(h))
+        if st:
+            raise CasError(st, lib().cas_create_error().decode())
+        self.h = h.value
+        self._acc = np.zeros(self.max_tree, dtype=np.int32)
+
+    def close(self) -> None:
+        if getattr(self, "h", None):
+            lib().cas_destroy(self.h)
+            self.h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def _chk(self, st: int) -> None:
+        if st:
+            raise CasError(st, lib().cas_last_error(self.h).decode())
+
+    # weights ------------------------------------------------------------------
+    def load_tensor(self, name: str, layer: int, arr: np.ndarray) -> None:
+        a = np.ascontiguousarray(arr)
+        self._chk(lib().cas_load_tensor(self.h, TENSOR[name], int(layer), _p(a), a.nbytes))
+
+    def load_weights(self, w: Dict, layers: Optional[Sequence[int]] = None) -> None:
+        self.load_tensor("embed", 0, w["embed"])
+        self.load_tensor("lm_head", 0, w["lm_head"])
+        self.load_tensor("final_norm", 0, np.asarray(w["final_norm"], dtype=np.float32))
+        for l, lw in enumerate(w["layers"]):
+            if lw is None or (layers is not None and l not in layers):
+                continue
+            for n in ("wq", "wk", "wv", "wo", "w_gate", "w_up", "w_down"):
+                self.load_tensor(n, l, lw[n])
+            self.load_tensor("attn_norm", l, np.asarray(lw["attn_norm"], dtype=np.float32))
+            self.load_tensor("ffn_norm", l, np.asarray(lw["ffn_norm"], dtype=np.float32))
+
+    def build_int8(self) -> None:
+        self._chk(lib().cas_build_int8(self.h))
+
+    # state ----------------------------------------------------------------------
+    @property
+    def committed(self) -> int:
+        n = ctypes.c_int32()
+        self._chk(lib().cas_committed_len(self.h, ctypes.byref(n)))
+        return n.value
+
+    def set_committed(self, n: int) -> None:
+        self._chk(lib().cas_set_committed(self.h, int(n)))
+
+    def kv_load(self, layer: int, k: np.ndarray, v: np.ndarray) -> None:
+        """Committed KV of one layer, [n_kv_heads][n][head_dim] in the storage type."""
+        k = np.ascontiguousarray(k)
+        v = np.ascontiguousarray(v)
+        self._chk(lib().cas_kv_load(self.h, int(layer), _p(k), _p(v), int(k.shape[1])))
+
+    def kv_read(self, layer: int, n: int) -> Tuple[np.ndarray, np.ndarray]:
+        """KV slots 0..n-1 of one layer as [n_kv_heads][n][head_dim] (bf16 bits or float32)."""
+        dt = np.uint16 if self.bf16 else np.float32
+        k = np.zeros((self.shape.n_kv_heads, n, self.shape.head_dim), dtype=dt)
+        v = np.zeros_like(k)
+        self._chk(lib().cas_kv_read(self.h, int(layer), _p(k), _p(v), int(n)))
+        return k, v
+
+    def prefill(self, tokens: Sequence[int]) -> None:
+        t = np.ascontiguousarray(tokens, dtype=np.int32)
+        self._chk(lib().cas_prefill(self.h, _p(t), t.shape[0]))
+
+    # the step -------------------------------------------------------------------
+    def forward(self, tokens: Sequence[int], parents: Sequence[int], node_offset: int = 0,
+                skip: Optional[Sequence[int]] = None, act_quant: bool = False,
+                logits: bool = True) -> Optional[np.ndarray]:
+        t = np.ascontiguousarray(tokens, dtype=np.int32)
+        p = np.ascontiguousarray(parents, dtype=np.int32)
+        n = t.shape[0]
+        if p.shape[0] != n:
+            raise ValueError("tokens and parents differ in length")
+        sk = None
+        if skip is not None:
+            sk = np.ascontiguousarray(skip, dtype=np.uint8)  # the library validates the values
+            if sk.shape[0] != self.shape.n_layers:
+                raise ValueError("skip mask length")
+        out = np.empty((n, self.shape.vocab), dtype=np.float32) if logits else None
+        self._chk(lib().cas_forward(self.h, _p(t), _p(p), n, int(node_offset), None if sk is None else _p(sk),
+                                    1 if act_quant else 0, None if out is None else _p(out)))
+        return out
+
+    def logits_device(self) -> Tuple[int, int]:
+        ptr = ctypes.c_void_p()
+        n = ctypes.c_int32()
+        self._chk(lib().cas_logits_device(self.h, ctypes.byref(ptr), ctypes.byref(n)))
+        return ptr.value, n.value
+
+    def accept(self) -> Tuple[List[int], int]:
+        n = ctypes.c_int32()
+        b = ctypes.c_int32()
+        self._chk(lib().cas_accept_tree(self.h, 1, _p(self._acc), ctypes.byref(n), ctypes.byref(b)))
+        return [int(x) for x in self._acc[: n.value]], int(b.value)
+
+    def compact(self, accepted: Sequence[int]) -> None:
+        a = np.ascontiguousarray(accepted, dtype=np.int32)
+        self._chk(lib().cas_kv_compact(self.h, _p(a), a.shape[0]))
+
+    def sync(self) -> None:
+        self._chk(lib().cas_sync(self.h))
+
+    def set_graphs(self, on: bool) -> None:
+        self._chk(lib().cas_set_graphs(self.h, 1 if on else 0))
+
+    def profile(self, on: bool) -> None:
+        self._chk(lib().cas_profile(self.h, 1 if on else 0))
+
+    def profile_read(self, reset: bool = True) -> Dict[str, Tuple[float, int]]:
+        ms = np.zeros(len(KCLASS), dtype=np.float64)
+        cnt = np.zeros(len(KCLASS), dtype=np.int32)
+        self._chk(lib().cas_profile_read(self.h, _p(ms), _p(cnt), 1 if reset else 0))
+        return {k: (float(ms[i]), int(cnt[i])) for i, k in enumerate(KCLASS)}
+
+
+# ----------------------------------------------------------------------------
+# kernel-level entry points on device tensors (torch tensors on a HIP device)
+# ----------------------------------------------------------------------------
+
+def _dp(t) -> Optional[int]:
+    return None if t is None else int(t.data_ptr())
+
+
+def _stream(stream) -> Optional[int]:
+    if stream is None:
+        import torch
+        return int(torch.cuda.current_stream().cuda_stream)
+    return int(stream)
+
+
+def _ochk(st: int, what: str) -> None:
+    if st:
+        raise CasError(st, what)
+
+
+def op_gemm(wtype: int, W, X, N: int, K: int, T: int, out, ldo: int, epi: int = EPI_STORE,
+            xs=None, ws=None, stream=None) -> None:
+    _ochk(lib().cas_op_gemm(wtype, _dp(W), _dp(X), N, K, T, _dp(xs), _dp(ws), epi, _dp(out), ldo, _stream(stream)),
+          "cas_op_gemm")
+
+
+def op_quant_rows(atype: int, x, T: int, K: int, q, s, stream=None) -> None:
+    _ochk(lib().cas_op_quant_rows(atype, _dp(x), T, K, _dp(q), _dp(s), _stream(stream)), "cas_op_quant_rows")
+
+
+def op_quant_weight(wtype: int, W, N: int, K: int, q, s, stream=None) -> None:
+    _ochk(lib().cas_op_quant_weight(wtype, _dp(W), N, K, _dp(q), _dp(s), _stream(stream)), "cas_op_quant_weight")
+
+
+def op_attention_work_bytes(Lc: int, n_tree: int, T: int, H: int, hd: int) -> int:
+    return int(lib().cas_op_attention_work_bytes(Lc, n_tree, T, H, hd))
+
+
+def op_attention(q, kc, vt, ctx_cap: int, Lc: int, n_tree: int, T: int, H: int, Hkv: int, hd: int, anc, out,
+                 work, stream=None) -> None:
+    _ochk(lib().cas_op_attention(_dp(q), _dp(kc), _dp(vt), ctx_cap, Lc, n_tree, T, H, Hkv, hd, _dp(anc), _dp(out),
+                                 _dp(work), int(work.numel() * work.element_size()), _stream(stream)),
+          "cas_op_attention")
+
+
+def op_copy(dst, src, nbytes: int, stream=None) -> None:
+    _ochk(lib().cas_op_copy(_dp(dst), _dp(src), nbytes, _stream(stream)), "cas_op_copy")

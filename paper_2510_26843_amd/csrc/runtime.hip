@@ -1,0 +1,1008 @@
+// Runtime behind the C ABI of include/cas.h and include/cas_ops.h: weight
+// store (device layouts for the fused epilogues), KV cache with committed and
+// tree-scratch regions, round bookkeeping, argument validation, launch
+// sequencing, HIP graph cache and per-kernel event timing.
+#include "cas.h"
+#include "cas_ops.h"
+#include "cas_internal.h"
+
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdio>
+#include <cstring>
+#include <map>
+#include <string>
+#include <vector>
+
+using namespace cas;
+
+namespace {
+
+constexpr int kStages = 8;          // pinned upload buffers in flight
+constexpr size_t kMaxGraphs = 64;   // captured forwards kept at once
+constexpr size_t kStageBytes = 4096;
+
+struct LayerW {
+    void* wqkv = nullptr;   // [qkv_rows][d]: q heads, k heads (rows pair-interleaved), v heads
+    void* wo = nullptr;     // [d][H*hd]
+    void* wgu = nullptr;    // [2*ffn][d]: rows gate 0, up 0, gate 1, up 1, ...
+    void* wd = nullptr;     // [d][ffn]
+    float* attn_norm = nullptr;
+    float* ffn_norm = nullptr;
+    int8_t* q8[4] = {nullptr, nullptr, nullptr, nullptr};  // int8 copies in the same row layouts
+    float* s8[4] = {nullptr, nullptr, nullptr, nullptr};
+    unsigned loaded = 0;    // bit per tensor kind
+};
+
+struct Stage {
+    unsigned char* host = nullptr;
+    hipEvent_t ev = nullptr;
+    bool pending = false;
+};
+
+struct ProfRec {
+    int cls;
+    hipEvent_t a, b;
+};
+
+}  // namespace
+
+struct cas_ctx {
+    cas_config cfg{};
+    int dev = 0;
+    hipStream_t stream = nullptr;
+    bool own_stream = false;
+    int et = ET_BF16;
+    size_t es = 2;
+    int qrows = 0, krows = 0, qkv_rows = 0, ctx_cap = 0;
+
+    void* embed = nullptr;
+    void* lm_head = nullptr;
+    float* final_norm = nullptr;
+    unsigned global_loaded = 0;
+    std::vector<LayerW> layers;
+    bool int8_ready = false;
+
+    void* kc = nullptr;  // [L][Hkv][ctx_cap][hd]
+    void* vt = nullptr;  // [L][Hkv][hd][ctx_cap]
+    float* rope_cos = nullptr;
+    float* rope_sin = nullptr;
+
+    int Lc = 0, n_nodes = 0, verified_n = 0, logits_rows = 0;
+    std::vector<int> parent, token;
+
+    int* d_rtok = nullptr;
+    int* d_rpar = nullptr;
+    StepParams* d_sp = nullptr;
+    int* d_row_pos = nullptr;
+    int* d_row_slot = nullptr;
+    uint64_t* d_row_anc = nullptr;
+    float* d_h = nullptr;
+    void* d_xn = nullptr;
+    int8_t* d_xq = nullptr;
+    float* d_xs = nullptr;
+    void* d_q = nullptr;
+    void* d_ao = nullptr;
+    void* d_sw = nullptr;
+    float* d_logits = nullptr;
+    float* d_part = nullptr;
+    size_t part_bytes = 0;
+    int* d_gbuf = nullptr;
+    int* d_result = nullptr;
+    int* d_acc = nullptr;
+    int* h_result = nullptr;  // pinned
+
+    Stage stage[kStages];
+    int stage_i = 0;
+
+    bool graphs = true;
+    std::map<std::string, hipGraphExec_t> gcache;
+
+    bool prof = false;
+    std::vector<ProfRec> prec;
+    std::vector<hipEvent_t> ev_pool;
+    double pms[CAS_K_COUNT] = {};
+    int pn[CAS_K_COUNT] = {};
+
+    std::vector<void*> allocs;
+    std::string err;
+};
+
+namespace {
+
+std::string g_create_err;
+
+cas_status fail(cas_ctx* c, cas_status st, const std::string& msg) {
+    if (c) c->err = msg;
+    return st;
+}
+
+cas_status hip_fail(cas_ctx* c, hipError_t e, const char* what) {
+    std::string m = std::string(what) + ": " + hipGetErrorString(e);
+    return fail(c, CAS_ERR_DEVICE, m);
+}
+
+#define HIPCHK(c, expr)                                        \
+    do {                                                       \
+        hipError_t _e = (expr);                                \
+        if (_e != hipSuccess) return hip_fail((c), _e, #expr); \
+    } while (0)
+
+template <typename T>
+hipError_t dalloc(cas_ctx* c, T** p, size_t bytes) {
+    void* q = nullptr;
+    hipError_t e = hipMalloc(&q, bytes ? bytes : 16);
+    if (e != hipSuccess) return e;
+    c->allocs.push_back(q);
+    *p = (T*)q;
+    return hipSuccess;
+}
+
+hipEvent_t take_event(cas_ctx* c) {
+    if (!c->ev_pool.empty()) {
+        hipEvent_t e = c->ev_pool.back();
+        c->ev_pool.pop_back();
+        return e;
+    }
+    hipEvent_t e = nullptr;
+    if (hipEventCreate(&e) != hipSuccess) return nullptr;
+    return e;
+}
+
+// Launch wrapper: with profiling on, bracket the launch with events.
+template <typename F>
+hipError_t timed(cas_ctx* c, int cls, F&& f) {
+    if (!c->prof) return f();
+    hipEvent_t a = take_event(c), b = take_event(c);
+    if (!a || !b) return hipErrorOutOfMemory;
+    hipError_t e = hipEventRecord(a, c->stream);
+    if (e != hipSuccess) return e;
+    e = f();
+    if (e != hipSuccess) return e;
+    e = hipEventRecord(b, c->stream);
+    if (e != hipSuccess) return e;
+    c->prec.push_back({cls, a, b});
+    return hipSuccess;
+}
+
+// Pinned upload buffer whose previous copy has completed.
+unsigned char* next_stage(cas_ctx* c, hipEvent_t* ev) {
+    Stage& s = c->stage[c->stage_i];
+    c->stage_i = (c->stage_i + 1) % kStages;
+    if (s.pending) {
+        if (hipEventSynchronize(s.ev) != hipSuccess) return nullptr;
+        s.pending = false;
+    }
+    *ev = s.ev;
+    s.pending = true;
+    return s.host;
+}
+
+size_t tensor_elems(const cas_ctx* c, int kind) {
+    const cas_config& f = c->cfg;
+    const size_t d = f.d_model, hd = f.head_dim;
+    switch (kind) {
+    case CAS_T_EMBED:
+    case CAS_T_LM_HEAD: return (size_t)f.vocab * d;
+    case CAS_T_FINAL_NORM:
+    case CAS_T_ATTN_NORM:
+    case CAS_T_FFN_NORM: return d;
+    case CAS_T_WQ: return (size_t)f.n_heads * hd * d;
+    case CAS_T_WK:
+    case CAS_T_WV: return (size_t)f.n_kv_heads * hd * d;
+    case CAS_T_WO: return d * f.n_heads * hd;
+    case CAS_T_W_GATE:
+    case CAS_T_W_UP:
+    case CAS_T_W_DOWN: return d * (size_t)f.ffn_dim;
+    }
+    return 0;
+}
+
+bool is_norm(int kind) { return kind == CAS_T_FINAL_NORM || kind == CAS_T_ATTN_NORM || kind == CAS_T_FFN_NORM; }
+bool is_global(int kind) { return kind == CAS_T_EMBED || kind == CAS_T_LM_HEAD || kind == CAS_T_FINAL_NORM; }
+constexpr unsigned kLayerMask = (1u << CAS_T_ATTN_NORM) | (1u << CAS_T_FFN_NORM) | (1u << CAS_T_WQ) |
+                                (1u << CAS_T_WK) | (1u << CAS_T_WV) | (1u << CAS_T_WO) | (1u << CAS_T_W_GATE) |
+                                (1u << CAS_T_W_UP) | (1u << CAS_T_W_DOWN);
+constexpr unsigned kGlobalMask = (1u << CAS_T_EMBED) | (1u << CAS_T_LM_HEAD) | (1u << CAS_T_FINAL_NORM);
+
+// Host copy of the tree checks shared by cas_tree_info and cas_forward.
+bool tree_depths(const int32_t* parent, int first, int n, const std::vector<int>& prior, std::vector<int>* depth,
+                 std::string* why) {
+    depth->assign(first + n, 0);
+    for (int j = 0; j < first; ++j) (*depth)[j] = 0;
+    // depths of prior nodes
+    for (int j = 0; j < first; ++j) {
+        const int p = prior[j];
+        (*depth)[j] = p < 0 ? 0 : (*depth)[p] + 1;
+    }
+    for (int i = 0; i < n; ++i) {
+        const int node = first + i, p = parent[i];
+        if (node == 0) {
+            if (p != -1) {
+                *why = "node 0 (the root) must have parent -1";
+                return false;
+            }
+            (*depth)[0] = 0;
+        } else {
+            if (p < 0 || p >= node) {
+                char b[128];
+                snprintf(b, sizeof b, "node %d has parent %d; parents must precede their children", node, p);
+                *why = b;
+                return false;
+            }
+            (*depth)[node] = (*depth)[p] + 1;
+        }
+    }
+    return true;
+}
+
+// The forward's launch sequence (captured into a graph, or launched directly).
+hipError_t enqueue_forward(cas_ctx* c, int T, const uint8_t* skip, int aq) {
+    const cas_config& f = c->cfg;
+    const int d = f.d_model, H = f.n_heads, Hkv = f.n_kv_heads, hd = f.head_dim, ffn = f.ffn_dim;
+    const int et = c->et;
+    hipStream_t s = c->stream;
+    hipError_t e;
+#define RUN(cls, call)                                        \
+    do {                                                      \
+        e = timed(c, (cls), [&]() -> hipError_t { return call; }); \
+        if (e != hipSuccess) return e;                        \
+    } while (0)
+
+    RUN(CAS_K_EMBED, launch_embed(et, c->embed, d, c->d_rtok, c->d_rpar, c->d_sp, T, c->d_h, c->d_row_pos,
+                                  c->d_row_slot, c->d_row_anc, s));
+    const size_t kv_layer = (size_t)Hkv * c->ctx_cap * hd * c->es;
+    AttnArgs at{};
+    at.q = c->d_q;
+    at.anc = c->d_row_anc;
+    at.sp = c->d_sp;
+    at.out = c->d_ao;
+    at.T = T;
+    at.H = H;
+    at.Hkv = Hkv;
+    at.hd = hd;
+    at.ctx_cap = c->ctx_cap;
+    // splits for the attention grid come from the host copy of the state
+    at.Lc_host = c->Lc;
+    at.n_tree_host = c->n_nodes;  // already the post-call node count
+    const int S = attention_splits(at.Lc_host + at.n_tree_host);
+    at.part_o = c->d_part;
+    at.part_ml = c->d_part + (size_t)S * H * T * hd;
+    const int wq = aq ? (int)ET_I8 : et;
+
+    for (int l = 0; l < f.n_layers; ++l) {
+        if (skip && skip[l]) continue;
+        LayerW& w = c->layers[l];
+        void* kc = (char*)c->kc + kv_layer * l;
+        void* vt = (char*)c->vt + kv_layer * l;
+        // --- attention block
+        RUN(CAS_K_RMSNORM, launch_rmsnorm(et, c->d_h, w.attn_norm, T, d, f.rms_eps, aq ? nullptr : c->d_xn,
+                                          aq ? c->d_xq : nullptr, c->d_xs, s));
+        GemmArgs g{};
+        g.T = T;
+        g.N = c->qkv_rows;
+        g.K = d;
+        g.W = aq ? (const void*)w.q8[0] : w.wqkv;
+        g.X = aq ? (const void*)c->d_xq : c->d_xn;
+        g.xs = c->d_xs;
+        g.ws = w.s8[0];
+        g.out = c->d_q;
+        g.rope_cos = c->rope_cos;
+        g.rope_sin = c->rope_sin;
+        g.row_pos = c->d_row_pos;
+        g.row_slot = c->d_row_slot;
+        g.kc = kc;
+        g.vt = vt;
+        g.H = H;
+        g.Hkv = Hkv;
+        g.hd = hd;
+        g.ctx_cap = c->ctx_cap;
+        RUN(CAS_K_GEMM_QKV, launch_gemm(wq, et, EPI_QKV, g, s));
+        at.kc = kc;
+        at.vt = vt;
+        RUN(CAS_K_ATTN, launch_attention(et, at, s));
+        if (et == ET_BF16) RUN(CAS_K_ATTN_COMBINE, launch_attention_combine(et, at, s));
+        if (aq) RUN(CAS_K_QUANT, launch_quant_rows(et, c->d_ao, T, H * hd, c->d_xq, c->d_xs, s));
+        GemmArgs go{};
+        go.T = T;
+        go.N = d;
+        go.K = H * hd;
+        go.W = aq ? (const void*)w.q8[1] : w.wo;
+        go.X = aq ? (const void*)c->d_xq : c->d_ao;
+        go.xs = c->d_xs;
+        go.ws = w.s8[1];
+        go.out = c->d_h;
+        go.ldo = d;
+        RUN(CAS_K_GEMM_O, launch_gemm(wq, et, EPI_RESID, go, s));
+        // --- FFN block
+        RUN(CAS_K_RMSNORM, launch_rmsnorm(et, c->d_h, w.ffn_norm, T, d, f.rms_eps, aq ? nullptr : c->d_xn,
+                                          aq ? c->d_xq : nullptr, c->d_xs, s));
+        GemmArgs gu{};
+        gu.T = T;
+        gu.N = 2 * ffn;
+        gu.K = d;
+        gu.W = aq ? (const void*)w.q8[2] : w.wgu;
+        gu.X = aq ? (const void*)c->d_xq : c->d_xn;
+        gu.xs = c->d_xs;
+        gu.ws = w.s8[2];
+        gu.out = c->d_sw;
+        gu.ldo = ffn;
+        RUN(CAS_K_GEMM_GATEUP, launch_gemm(wq, et, EPI_SWIGLU, gu, s));
+        if (aq) RUN(CAS_K_QUANT, launch_quant_rows(et, c->d_sw, T, ffn, c->d_xq, c->d_xs, s));
+        GemmArgs gd{};
+        gd.T = T;
+        gd.N = d;
+        gd.K = ffn;
+        gd.W = aq ? (const void*)w.q8[3] : w.wd;
+        gd.X = aq ? (const void*)c->d_xq : c->d_sw;
+        gd.xs = c->d_xs;
+        gd.ws = w.s8[3];
+        gd.out = c->d_h;
+        gd.ldo = d;
+        RUN(CAS_K_GEMM_DOWN, launch_gemm(wq, et, EPI_RESID, gd, s));
+    }
+    RUN(CAS_K_RMSNORM, launch_rmsnorm(et, c->d_h, c->final_norm, T, d, f.rms_eps, c->d_xn, nullptr, nullptr, s));
+    GemmArgs gh{};
+    gh.T = T;
+    gh.N = f.vocab;
+    gh.K = d;
+    gh.W = c->lm_head;
+    gh.X = c->d_xn;
+    gh.out = c->d_logits;
+    gh.ldo = f.vocab;
+    RUN(CAS_K_GEMM_HEAD, launch_gemm(et, et, EPI_STORE, gh, s));
+#undef RUN
+    return hipSuccess;
+}
+
+std::string graph_key(const cas_ctx* c, int T, const uint8_t* skip, int aq, int S) {
+    std::string k = std::to_string(T) + ":" + std::to_string(aq) + ":" + std::to_string(S) + ":";
+    for (int l = 0; l < c->cfg.n_layers; ++l) k.push_back(skip && skip[l] ? '1' : '0');
+    return k;
+}
+
+cas_status check_ready(cas_ctx* c, const uint8_t* skip) {
+    if ((c->global_loaded & kGlobalMask) != kGlobalMask) return fail(c, CAS_ERR_STATE, "embedding, LM head or final norm not loaded");
+    for (int l = 0; l < c->cfg.n_layers; ++l) {
+        if (skip && skip[l]) continue;
+        if ((c->layers[l].loaded & kLayerMask) != kLayerMask) {
+            return fail(c, CAS_ERR_STATE, "layer " + std::to_string(l) + " has tensors not loaded");
+        }
+    }
+    return CAS_OK;
+}
+
+cas_status do_forward(cas_ctx* c, const int32_t* tokens, const int32_t* parent, int n, int node_offset,
+                      const uint8_t* skip, int aq, float* logits_host, bool allow_graph = true) {
+    const cas_config& f = c->cfg;
+    if (!tokens || !parent) return fail(c, CAS_ERR_ARG, "tokens and tree_parent must not be NULL");
+    if (n < 1) return fail(c, CAS_ERR_ARG, "n must be >= 1");
+    if (node_offset < 0) return fail(c, CAS_ERR_ARG, "node_offset must be >= 0");
+    if (aq != 0 && aq != 1) return fail(c, CAS_ERR_ARG, "act_quant must be 0 or 1");
+    if (node_offset != 0 && node_offset != c->n_nodes)
+        return fail(c, CAS_ERR_TREE, "node_offset must be 0 (new round) or the round's node count " +
+                                         std::to_string(c->n_nodes));
+    if (node_offset + n > f.max_tree)
+        return fail(c, CAS_ERR_CAPACITY, "round would exceed max_tree = " + std::to_string(f.max_tree));
+    if (c->Lc + node_offset + n > f.max_ctx)
+        return fail(c, CAS_ERR_CAPACITY, "committed + tree slots would exceed max_ctx = " + std::to_string(f.max_ctx));
+    for (int i = 0; i < n; ++i)
+        if (tokens[i] < 0 || tokens[i] >= f.vocab)
+            return fail(c, CAS_ERR_ARG, "token " + std::to_string(tokens[i]) + " out of range");
+    bool any_skip = false;
+    if (skip) {
+        for (int l = 0; l < f.n_layers; ++l) {
+            if (skip[l] > 1) return fail(c, CAS_ERR_ARG, "skip_mask entries must be 0 or 1");
+            any_skip |= skip[l] != 0;
+        }
+    }
+    if (aq && !c->int8_ready) return fail(c, CAS_ERR_STATE, "act_quant needs cas_build_int8 first");
+    std::vector<int> depth;
+    std::string why;
+    if (!tree_depths(parent, node_offset, n, c->parent, &depth, &why)) return fail(c, CAS_ERR_TREE, why);
+    cas_status st = check_ready(c, skip);
+    if (st != CAS_OK) return st;
+
+    // upload tokens, parents and the step parameters through a pinned buffer
+    hipEvent_t ev = nullptr;
+    unsigned char* buf = next_stage(c, &ev);
+    if (!buf) return fail(c, CAS_ERR_DEVICE, "staging buffer wait failed");
+    StepParams sp{c->Lc, node_offset, node_offset + n, 0};
+    memcpy(buf, &sp, sizeof sp);
+    memcpy(buf + 16, tokens, sizeof(int32_t) * n);
+    memcpy(buf + 16 + 4 * 128, parent, sizeof(int32_t) * n);
+    HIPCHK(c, hipMemcpyAsync(c->d_sp, buf, sizeof sp, hipMemcpyHostToDevice, c->stream));
+    HIPCHK(c, hipMemcpyAsync(c->d_rtok + node_offset, buf + 16, 4 * (size_t)n, hipMemcpyHostToDevice, c->stream));
+    HIPCHK(c, hipMemcpyAsync(c->d_rpar + node_offset, buf + 16 + 4 * 128, 4 * (size_t)n, hipMemcpyHostToDevice,
+                             c->stream));
+    HIPCHK(c, hipEventRecord(ev, c->stream));
+
+    // round state (the launch sequence reads the post-call node count)
+    const int old_nodes = c->n_nodes;
+    c->n_nodes = node_offset + n;
+    const int S = attention_splits(c->Lc + c->n_nodes);
+    hipError_t e;
+    if (c->graphs && !c->prof && allow_graph) {
+        const std::string key = graph_key(c, n, skip, aq, S);
+        auto it = c->gcache.find(key);
+        if (it == c->gcache.end()) {
+            if (c->gcache.size() >= kMaxGraphs) {
+                HIPCHK(c, hipStreamSynchronize(c->stream));
+                for (auto& kv : c->gcache) (void)hipGraphExecDestroy(kv.second);
+                c->gcache.clear();
+            }
+            hipGraph_t gr = nullptr;
+            e = hipStreamBeginCapture(c->stream, hipStreamCaptureModeThreadLocal);
+            if (e == hipSuccess) {
+                hipError_t e2 = enqueue_forward(c, n, skip, aq);
+                e = hipStreamEndCapture(c->stream, &gr);
+                if (e2 != hipSuccess) e = e2;
+            }
+            hipGraphExec_t ex = nullptr;
+            if (e == hipSuccess) e = hipGraphInstantiate(&ex, gr, nullptr, nullptr, 0);
+            if (gr) (void)hipGraphDestroy(gr);
+            if (e != hipSuccess) {
+                c->n_nodes = old_nodes;
+                return hip_fail(c, e, "graph capture of the forward");
+            }
+            it = c->gcache.emplace(key, ex).first;
+        }
+        e = hipGraphLaunch(it->second, c->stream);
+    } else {
+        e = enqueue_forward(c, n, skip, aq);
+    }
+    if (e != hipSuccess) {
+        c->n_nodes = old_nodes;
+        return hip_fail(c, e, "forward launch");
+    }
+    for (int i = 0; i < n; ++i) {
+        c->parent[node_offset + i] = parent[i];
+        c->token[node_offset + i] = tokens[i];
+    }
+    c->verified_n = (node_offset == 0 && !any_skip && !aq) ? n : 0;
+    c->logits_rows = n;
+    if (logits_host) {
+        HIPCHK(c, hipMemcpyAsync(logits_host, c->d_logits, sizeof(float) * (size_t)n * f.vocab, hipMemcpyDeviceToHost,
+                                 c->stream));
+        HIPCHK(c, hipStreamSynchronize(c->stream));
+    }
+    return CAS_OK;
+}
+
+cas_status do_compact(cas_ctx* c, const int32_t* acc, int n_acc) {
+    if (!acc) return fail(c, CAS_ERR_ARG, "accepted must not be NULL");
+    if (c->verified_n == 0 || c->verified_n != c->n_nodes)
+        return fail(c, CAS_ERR_STATE, "cas_kv_compact needs a verify call covering the whole round");
+    if (n_acc < 1 || n_acc > c->n_nodes) return fail(c, CAS_ERR_ARG, "n_accepted out of range");
+    if (acc[0] != 0) return fail(c, CAS_ERR_TREE, "accepted path must start at the root (node 0)");
+    bool identity = true;
+    for (int j = 1; j < n_acc; ++j) {
+        if (acc[j] <= 0 || acc[j] >= c->n_nodes || c->parent[acc[j]] != acc[j - 1])
+            return fail(c, CAS_ERR_TREE, "accepted[" + std::to_string(j) + "] is not a child of accepted[" +
+                                             std::to_string(j - 1) + "]");
+        identity &= acc[j] == j;
+    }
+    if (!identity) {
+        hipEvent_t ev = nullptr;
+        unsigned char* buf = next_stage(c, &ev);
+        if (!buf) return fail(c, CAS_ERR_DEVICE, "staging buffer wait failed");
+        memcpy(buf, acc, sizeof(int32_t) * n_acc);
+        HIPCHK(c, hipMemcpyAsync(c->d_acc, buf, sizeof(int32_t) * n_acc, hipMemcpyHostToDevice, c->stream));
+        HIPCHK(c, hipEventRecord(ev, c->stream));
+        const cas_config& f = c->cfg;
+        hipError_t e = timed(c, CAS_K_COMPACT, [&]() -> hipError_t {
+            return launch_compact(c->et, c->kc, c->vt, f.n_layers, f.n_kv_heads, f.head_dim, c->ctx_cap, c->d_sp,
+                                  c->d_acc, n_acc, c->stream);
+        });
+        if (e != hipSuccess) return hip_fail(c, e, "kv compaction");
+    }
+    c->Lc += n_acc;
+    c->n_nodes = 0;
+    c->verified_n = 0;
+    return CAS_OK;
+}
+
+void free_ctx(cas_ctx* c) {
+    if (!c) return;
+    if (c->stream) (void)hipStreamSynchronize(c->stream);
+    for (auto& kv : c->gcache) (void)hipGraphExecDestroy(kv.second);
+    for (auto& r : c->prec) {
+        (void)hipEventDestroy(r.a);
+        (void)hipEventDestroy(r.b);
+    }
+    for (auto e : c->ev_pool) (void)hipEventDestroy(e);
+    for (auto& s : c->stage) {
+        if (s.ev) (void)hipEventDestroy(s.ev);
+        if (s.host) (void)hipHostFree(s.host);
+    }
+    if (c->h_result) (void)hipHostFree(c->h_result);
+    for (void* p : c->allocs) (void)hipFree(p);
+    if (c->own_stream && c->stream) (void)hipStreamDestroy(c->stream);
+    delete c;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* cas_create_error(void) { return g_create_err.c_str(); }
+
+const char* cas_last_error(const cas_ctx* c) { return c ? c->err.c_str() : "null context"; }
+
+cas_status cas_tree_info(const int32_t* parent, int32_t n, int32_t* depth, uint64_t* anc) {
+    if (!parent || n < 1 || n > 128) return CAS_ERR_ARG;
+    std::vector<int> dep;
+    std::string why;
+    std::vector<int> none;
+    if (!tree_depths(parent, 0, n, none, &dep, &why)) return CAS_ERR_TREE;
+    for (int i = 0; i < n; ++i) {
+        uint64_t a[2] = {0, 0};
+        for (int x = i; x >= 0; x = parent[x]) a[x >> 6] |= 1ull << (x & 63);
+        if (depth) depth[i] = dep[i];
+        if (anc) {
+            anc[2 * i] = a[0];
+            anc[2 * i + 1] = a[1];
+        }
+    }
+    return CAS_OK;
+}
+
+cas_status cas_create(const cas_config* cfg, int device, void* stream, cas_ctx** out) {
+    if (!out) return CAS_ERR_ARG;
+    *out = nullptr;
+    g_create_err.clear();
+    auto bad = [](cas_status s, const std::string& m) {
+        g_create_err = m;
+        return s;
+    };
+    if (!cfg) return bad(CAS_ERR_ARG, "cfg is NULL");
+    const cas_config f = *cfg;
+    if (f.n_layers < 1 || f.d_model < 16 || f.n_heads < 1 || f.n_kv_heads < 1 || f.vocab < 16 || f.ffn_dim < 16)
+        return bad(CAS_ERR_ARG, "non-positive dimension");
+    if (f.n_heads % f.n_kv_heads) return bad(CAS_ERR_ARG, "n_heads must be a multiple of n_kv_heads");
+    if (f.head_dim != 64 && f.head_dim != 128) return bad(CAS_ERR_UNSUPPORTED, "head_dim must be 64 or 128");
+    if (f.d_model % 16 || f.ffn_dim % 16 || f.vocab % 16)
+        return bad(CAS_ERR_UNSUPPORTED, "d_model, ffn_dim and vocab must be multiples of 16");
+    if (f.d_model > 8192 || f.ffn_dim > 65536) return bad(CAS_ERR_UNSUPPORTED, "d_model above 8192");
+    if (f.dtype != CAS_F32 && f.dtype != CAS_BF16) return bad(CAS_ERR_ARG, "dtype");
+    if (f.max_tree < 1 || f.max_tree > 128) return bad(CAS_ERR_UNSUPPORTED, "max_tree must be in [1, 128]");
+    if (f.max_ctx < f.max_tree) return bad(CAS_ERR_ARG, "max_ctx must be >= max_tree");
+    if (f.dtype == CAS_F32 && f.max_ctx > 4096 - 128) return bad(CAS_ERR_UNSUPPORTED, "fp32 models need max_ctx <= 3968");
+    if (!(f.rms_eps > 0.f) || !(f.rope_theta > 1.f)) return bad(CAS_ERR_ARG, "rms_eps / rope_theta");
+
+    hipError_t e = hipSetDevice(device);
+    if (e != hipSuccess) return bad(CAS_ERR_DEVICE, std::string("hipSetDevice: ") + hipGetErrorString(e));
+    cas_ctx* c = new cas_ctx();
+    c->cfg = f;
+    c->dev = device;
+    c->et = f.dtype == CAS_BF16 ? ET_BF16 : ET_F32;
+    c->es = f.dtype == CAS_BF16 ? 2 : 4;
+    c->qrows = f.n_heads * f.head_dim;
+    c->krows = f.n_kv_heads * f.head_dim;
+    c->qkv_rows = c->qrows + 2 * c->krows;
+    c->ctx_cap = ((f.max_ctx + 127) / 128) * 128;
+    c->layers.resize(f.n_layers);
+    c->parent.assign(f.max_tree, -1);
+    c->token.assign(f.max_tree, 0);
+    auto cleanup = [&](cas_status s, const std::string& m) {
+        free_ctx(c);
+        return bad(s, m);
+    };
+#define ALLOC(p, bytes)                                                              \
+    do {                                                                             \
+        if (dalloc(c, &(p), (bytes)) != hipSuccess)                                  \
+            return cleanup(CAS_ERR_OOM, std::string("hipMalloc failed for ") + #p); \
+    } while (0)
+    if (stream) {
+        c->stream = (hipStream_t)stream;
+    } else {
+        if (hipStreamCreate(&c->stream) != hipSuccess) return cleanup(CAS_ERR_DEVICE, "hipStreamCreate");
+        c->own_stream = true;
+    }
+    const size_t es = c->es, d = f.d_model, ffn = f.ffn_dim, T = f.max_tree;
+    ALLOC(c->embed, (size_t)f.vocab * d * es);
+    ALLOC(c->lm_head, (size_t)f.vocab * d * es);
+    ALLOC(c->final_norm, d * 4);
+    for (auto& w : c->layers) {
+        ALLOC(w.wqkv, (size_t)c->qkv_rows * d * es);
+        ALLOC(w.wo, d * c->qrows * es);
+        ALLOC(w.wgu, 2 * ffn * d * es);
+        ALLOC(w.wd, d * ffn * es);
+        ALLOC(w.attn_norm, d * 4);
+        ALLOC(w.ffn_norm, d * 4);
+    }
+    const size_t kv = (size_t)f.n_layers * f.n_kv_heads * c->ctx_cap * f.head_dim * es;
+    ALLOC(c->kc, kv);
+    ALLOC(c->vt, kv);
+    if (hipMemset(c->kc, 0, kv) != hipSuccess || hipMemset(c->vt, 0, kv) != hipSuccess)
+        return cleanup(CAS_ERR_DEVICE, "hipMemset of the KV cache");
+    const int half = f.head_dim / 2;
+    ALLOC(c->rope_cos, (size_t)c->ctx_cap * half * 4);
+    ALLOC(c->rope_sin, (size_t)c->ctx_cap * half * 4);
+    {
+        std::vector<float> cs((size_t)c->ctx_cap * half), sn((size_t)c->ctx_cap * half);
+        for (int p = 0; p < c->ctx_cap; ++p)
+            for (int i = 0; i < half; ++i) {
+                const double inv = std::pow((double)f.rope_theta, -2.0 * i / (double)f.head_dim);
+                const double ang = (double)p * inv;
+                cs[(size_t)p * half + i] = (float)std::cos(ang);
+                sn[(size_t)p * half + i] = (float)std::sin(ang);
+            }
+        if (hipMemcpy(c->rope_cos, cs.data(), cs.size() * 4, hipMemcpyHostToDevice) != hipSuccess ||
+            hipMemcpy(c->rope_sin, sn.data(), sn.size() * 4, hipMemcpyHostToDevice) != hipSuccess)
+            return cleanup(CAS_ERR_DEVICE, "RoPE table upload");
+    }
+    ALLOC(c->d_rtok, T * 4);
+    ALLOC(c->d_rpar, T * 4);
+    ALLOC(c->d_sp, sizeof(StepParams));
+    ALLOC(c->d_row_pos, T * 4);
+    ALLOC(c->d_row_slot, T * 4);
+    ALLOC(c->d_row_anc, T * 16);
+    ALLOC(c->d_h, T * d * 4);
+    const size_t wmax = std::max(std::max(d, ffn), (size_t)c->qrows);
+    ALLOC(c->d_xn, T * wmax * es);
+    ALLOC(c->d_xq, T * wmax);
+    ALLOC(c->d_xs, T * 4);
+    ALLOC(c->d_q, T * c->qrows * es);
+    ALLOC(c->d_ao, T * c->qrows * es);
+    ALLOC(c->d_sw, T * ffn * es);
+    ALLOC(c->d_logits, T * (size_t)f.vocab * 4);
+    c->part_bytes = attention_work_bytes(c->ctx_cap, (int)T, f.n_heads, f.head_dim);
+    ALLOC(c->d_part, c->part_bytes);
+    ALLOC(c->d_gbuf, T * 8);
+    ALLOC(c->d_result, (T + 4) * 4);
+    ALLOC(c->d_acc, (T + 1) * 4);
+    if (hipMemset(c->d_rtok, 0, T * 4) != hipSuccess || hipMemset(c->d_rpar, 0xff, T * 4) != hipSuccess)
+        return cleanup(CAS_ERR_DEVICE, "hipMemset of the round arrays");
+    if (hipHostMalloc((void**)&c->h_result, (T + 4) * 4, hipHostMallocDefault) != hipSuccess)
+        return cleanup(CAS_ERR_OOM, "hipHostMalloc");
+    for (auto& s : c->stage) {
+        if (hipHostMalloc((void**)&s.host, kStageBytes, hipHostMallocDefault) != hipSuccess)
+            return cleanup(CAS_ERR_OOM, "hipHostMalloc");
+        if (hipEventCreateWithFlags(&s.ev, hipEventDisableTiming) != hipSuccess)
+            return cleanup(CAS_ERR_DEVICE, "hipEventCreate");
+    }
+#undef ALLOC
+    if (hipDeviceSynchronize() != hipSuccess) return cleanup(CAS_ERR_DEVICE, "device sync after create");
+    *out = c;
+    return CAS_OK;
+}
+
+void cas_destroy(cas_ctx* c) { free_ctx(c); }
+
+cas_status cas_load_tensor(cas_ctx* c, int32_t kind, int32_t layer, const void* host, size_t bytes) {
+    if (!c) return CAS_ERR_ARG;
+    if (!host) return fail(c, CAS_ERR_ARG, "host pointer is NULL");
+    if (kind < CAS_T_EMBED || kind > CAS_T_W_DOWN) return fail(c, CAS_ERR_ARG, "unknown tensor kind");
+    const cas_config& f = c->cfg;
+    if (!is_global(kind) && (layer < 0 || layer >= f.n_layers)) return fail(c, CAS_ERR_ARG, "layer out of range");
+    const size_t el = is_norm(kind) ? 4 : c->es;
+    const size_t want = tensor_elems(c, kind) * el;
+    if (bytes != want)
+        return fail(c, CAS_ERR_ARG, "tensor size " + std::to_string(bytes) + " bytes, expected " + std::to_string(want));
+    const size_t d = f.d_model, hd = f.head_dim, es = c->es, row = d * es;
+    LayerW* w = is_global(kind) ? nullptr : &c->layers[layer];
+    auto cp = [&](void* dst) { return hipMemcpy(dst, host, bytes, hipMemcpyHostToDevice); };
+    hipError_t e = hipSuccess;
+    switch (kind) {
+    case CAS_T_EMBED: e = cp(c->embed); break;
+    case CAS_T_LM_HEAD: e = cp(c->lm_head); break;
+    case CAS_T_FINAL_NORM: e = cp(c->final_norm); break;
+    case CAS_T_ATTN_NORM: e = cp(w->attn_norm); break;
+    case CAS_T_FFN_NORM: e = cp(w->ffn_norm); break;
+    case CAS_T_WO: e = cp(w->wo); break;
+    case CAS_T_W_DOWN: e = cp(w->wd); break;
+    case CAS_T_WV: e = hipMemcpy((char*)w->wqkv + (size_t)(c->qrows + c->krows) * row, host, bytes,
+                                 hipMemcpyHostToDevice); break;
+    case CAS_T_WQ:
+    case CAS_T_WK: {
+        // rows of each head reordered so RoPE pairs (i, i + hd/2) are adjacent
+        const int heads = kind == CAS_T_WQ ? f.n_heads : f.n_kv_heads;
+        char* base = (char*)w->wqkv + (kind == CAS_T_WQ ? 0 : (size_t)c->qrows * row);
+        for (int h = 0; h < heads && e == hipSuccess; ++h) {
+            const char* src = (const char*)host + (size_t)h * hd * row;
+            char* dst = base + (size_t)h * hd * row;
+            e = hipMemcpy2D(dst, 2 * row, src, row, row, hd / 2, hipMemcpyHostToDevice);
+            if (e == hipSuccess)
+                e = hipMemcpy2D(dst + row, 2 * row, src + (hd / 2) * row, row, row, hd / 2, hipMemcpyHostToDevice);
+        }
+        break;
+    }
+    case CAS_T_W_GATE:
+    case CAS_T_W_UP: {
+        char* dst = (char*)w->wgu + (kind == CAS_T_W_UP ? row : 0);
+        e = hipMemcpy2D(dst, 2 * row, host, row, row, f.ffn_dim, hipMemcpyHostToDevice);
+        break;
+    }
+    }
+    if (e != hipSuccess) return hip_fail(c, e, "weight upload");
+    if (w) {
+        w->loaded |= 1u << kind;
+    } else {
+        c->global_loaded |= 1u << kind;
+    }
+    c->int8_ready = false;
+    return CAS_OK;
+}
+
+cas_status cas_build_int8(cas_ctx* c) {
+    if (!c) return CAS_ERR_ARG;
+    cas_status st = check_ready(c, nullptr);
+    if (st != CAS_OK) return st;
+    const cas_config& f = c->cfg;
+    const size_t d = f.d_model, ffn = f.ffn_dim;
+    for (auto& w : c->layers) {
+        const void* src[4] = {w.wqkv, w.wo, w.wgu, w.wd};
+        const size_t N[4] = {(size_t)c->qkv_rows, d, 2 * ffn, d};
+        const size_t K[4] = {d, (size_t)c->qrows, d, ffn};
+        for (int i = 0; i < 4; ++i) {
+            if (!w.q8[i]) {
+                if (dalloc(c, &w.q8[i], N[i] * K[i]) != hipSuccess || dalloc(c, &w.s8[i], N[i] * 4) != hipSuccess)
+                    return fail(c, CAS_ERR_OOM, "hipMalloc of the int8 weight copy");
+            }
+            hipError_t e = launch_quant_weight(c->et, src[i], (int)N[i], (int)K[i], w.q8[i], w.s8[i], c->stream);
+            if (e != hipSuccess) return hip_fail(c, e, "int8 weight quantisation");
+        }
+    }
+    HIPCHK(c, hipStreamSynchronize(c->stream));
+    c->int8_ready = true;
+    return CAS_OK;
+}
+
+cas_status cas_forward(cas_ctx* c, const int32_t* tokens, const int32_t* parent, int32_t n, int32_t node_offset,
+                       const uint8_t* skip, int32_t aq, float* logits_host) {
+    if (!c) return CAS_ERR_ARG;
+    return do_forward(c, tokens, parent, n, node_offset, skip, aq, logits_host);
+}
+
+cas_status cas_prefill(cas_ctx* c, const int32_t* tokens, int32_t n) {
+    if (!c) return CAS_ERR_ARG;
+    if (!tokens || n < 1) return fail(c, CAS_ERR_ARG, "prefill needs tokens and n >= 1");
+    if (c->Lc + n > c->cfg.max_ctx) return fail(c, CAS_ERR_CAPACITY, "prefill would exceed max_ctx");
+    for (int i = 0; i < n; ++i)
+        if (tokens[i] < 0 || tokens[i] >= c->cfg.vocab) return fail(c, CAS_ERR_ARG, "token out of range");
+    std::vector<int32_t> par(c->cfg.max_tree), acc(c->cfg.max_tree);
+    for (int i = 0; i < c->cfg.max_tree; ++i) {
+        par[i] = i - 1;
+        acc[i] = i;
+    }
+    int done = 0;
+    while (done < n) {
+        const int m = std::min(c->cfg.max_tree, n - done);
+        // one-off shapes: launched directly rather than captured
+        cas_status st = do_forward(c, tokens + done, par.data(), m, 0, nullptr, 0, nullptr, false);
+        if (st != CAS_OK) return st;
+        st = do_compact(c, acc.data(), m);
+        if (st != CAS_OK) return st;
+        done += m;
+    }
+    return CAS_OK;
+}
+
+cas_status cas_kv_load(cas_ctx* c, int32_t layer, const void* k, const void* v, int32_t n) {
+    if (!c) return CAS_ERR_ARG;
+    const cas_config& f = c->cfg;
+    if (!k || !v) return fail(c, CAS_ERR_ARG, "k and v must not be NULL");
+    if (layer < 0 || layer >= f.n_layers) return fail(c, CAS_ERR_ARG, "layer out of range");
+    if (n < 0 || n > f.max_ctx) return fail(c, CAS_ERR_CAPACITY, "n exceeds max_ctx");
+    if (n == 0) return CAS_OK;
+    const size_t es = c->es, hd = f.head_dim;
+    const size_t kv_layer = (size_t)f.n_kv_heads * c->ctx_cap * hd * es;
+    HIPCHK(c, hipStreamSynchronize(c->stream));
+    std::vector<unsigned char> tr((size_t)hd * n * es);
+    for (int h = 0; h < f.n_kv_heads; ++h) {
+        char* kd = (char*)c->kc + kv_layer * layer + (size_t)h * c->ctx_cap * hd * es;
+        HIPCHK(c, hipMemcpy(kd, (const char*)k + (size_t)h * n * hd * es, (size_t)n * hd * es, hipMemcpyHostToDevice));
+        const unsigned char* vs = (const unsigned char*)v + (size_t)h * n * hd * es;
+        for (int s = 0; s < n; ++s)
+            for (size_t e = 0; e < hd; ++e) memcpy(&tr[(e * n + s) * es], vs + ((size_t)s * hd + e) * es, es);
+        char* vd = (char*)c->vt + kv_layer * layer + (size_t)h * hd * c->ctx_cap * es;
+        HIPCHK(c, hipMemcpy2D(vd, (size_t)c->ctx_cap * es, tr.data(), (size_t)n * es, (size_t)n * es, hd,
+                              hipMemcpyHostToDevice));
+    }
+    return CAS_OK;
+}
+
+cas_status cas_kv_read(cas_ctx* c, int32_t layer, void* k, void* v, int32_t n) {
+    if (!c) return CAS_ERR_ARG;
+    const cas_config& f = c->cfg;
+    if (!k || !v) return fail(c, CAS_ERR_ARG, "k and v must not be NULL");
+    if (layer < 0 || layer >= f.n_layers) return fail(c, CAS_ERR_ARG, "layer out of range");
+    if (n < 0 || n > c->ctx_cap) return fail(c, CAS_ERR_CAPACITY, "n exceeds the cache");
+    if (n == 0) return CAS_OK;
+    const size_t es = c->es, hd = f.head_dim;
+    const size_t kv_layer = (size_t)f.n_kv_heads * c->ctx_cap * hd * es;
+    HIPCHK(c, hipStreamSynchronize(c->stream));
+    std::vector<unsigned char> tr((size_t)hd * n * es);
+    for (int h = 0; h < f.n_kv_heads; ++h) {
+        const char* ks = (const char*)c->kc + kv_layer * layer + (size_t)h * c->ctx_cap * hd * es;
+        HIPCHK(c, hipMemcpy((char*)k + (size_t)h * n * hd * es, ks, (size_t)n * hd * es, hipMemcpyDeviceToHost));
+        const char* vs = (const char*)c->vt + kv_layer * layer + (size_t)h * hd * c->ctx_cap * es;
+        HIPCHK(c, hipMemcpy2D(tr.data(), (size_t)n * es, vs, (size_t)c->ctx_cap * es, (size_t)n * es, hd,
+                              hipMemcpyDeviceToHost));
+        unsigned char* vd = (unsigned char*)v + (size_t)h * n * hd * es;
+        for (int s = 0; s < n; ++s)
+            for (size_t e = 0; e < hd; ++e) memcpy(vd + ((size_t)s * hd + e) * es, &tr[(e * n + s) * es], es);
+    }
+    return CAS_OK;
+}
+
+cas_status cas_set_committed(cas_ctx* c, int32_t n) {
+    if (!c) return CAS_ERR_ARG;
+    if (n < 0 || n > c->cfg.max_ctx) return fail(c, CAS_ERR_CAPACITY, "committed length out of range");
+    c->Lc = n;
+    c->n_nodes = 0;
+    c->verified_n = 0;
+    return CAS_OK;
+}
+
+cas_status cas_committed_len(const cas_ctx* c, int32_t* n) {
+    if (!c || !n) return CAS_ERR_ARG;
+    *n = c->Lc;
+    return CAS_OK;
+}
+
+cas_status cas_logits_device(const cas_ctx* c, const float** p, int32_t* n) {
+    if (!c || !p || !n) return CAS_ERR_ARG;
+    *p = c->d_logits;
+    *n = c->logits_rows;
+    return CAS_OK;
+}
+
+cas_status cas_accept_tree(cas_ctx* c, int32_t greedy, int32_t* accepted, int32_t* n_accepted, int32_t* bonus) {
+    if (!c) return CAS_ERR_ARG;
+    if (greedy != 1) return fail(c, CAS_ERR_UNSUPPORTED, "only greedy acceptance is implemented");
+    if (!accepted || !n_accepted || !bonus) return fail(c, CAS_ERR_ARG, "output pointers must not be NULL");
+    if (c->verified_n == 0 || c->verified_n != c->n_nodes)
+        return fail(c, CAS_ERR_STATE, "cas_accept_tree needs a verify call covering the whole round");
+    const int T = c->n_nodes;
+    hipError_t e = timed(c, CAS_K_ACCEPT, [&]() -> hipError_t {
+        return launch_accept(c->d_logits, T, c->cfg.vocab, c->d_rtok, c->d_rpar, c->d_gbuf, c->d_result, c->stream);
+    });
+    if (e != hipSuccess) return hip_fail(c, e, "acceptance launch");
+    HIPCHK(c, hipMemcpyAsync(c->h_result, c->d_result, sizeof(int) * (size_t)(T + 3), hipMemcpyDeviceToHost, c->stream));
+    HIPCHK(c, hipStreamSynchronize(c->stream));
+    if (c->h_result[2]) return fail(c, CAS_ERR_DEVICE, "NaN in the verify logits");
+    const int na = c->h_result[0];
+    if (na < 1 || na > T) return fail(c, CAS_ERR_DEVICE, "acceptance returned an invalid path length");
+    for (int j = 0; j < na; ++j) accepted[j] = c->h_result[3 + j];
+    *n_accepted = na;
+    *bonus = c->h_result[1];
+    return CAS_OK;
+}
+
+cas_status cas_kv_compact(cas_ctx* c, const int32_t* accepted, int32_t n_accepted) {
+    if (!c) return CAS_ERR_ARG;
+    return do_compact(c, accepted, n_accepted);
+}
+
+cas_status cas_set_graphs(cas_ctx* c, int32_t enable) {
+    if (!c) return CAS_ERR_ARG;
+    c->graphs = enable != 0;
+    return CAS_OK;
+}
+
+cas_status cas_profile(cas_ctx* c, int32_t enable) {
+    if (!c) return CAS_ERR_ARG;
+    c->prof = enable != 0;
+    return CAS_OK;
+}
+
+cas_status cas_profile_read(cas_ctx* c, double* ms, int32_t* launches, int32_t reset) {
+    if (!c) return CAS_ERR_ARG;
+    HIPCHK(c, hipStreamSynchronize(c->stream));
+    for (auto& r : c->prec) {
+        float t = 0.f;
+        HIPCHK(c, hipEventElapsedTime(&t, r.a, r.b));
+        c->pms[r.cls] += t;
+        c->pn[r.cls] += 1;
+        c->ev_pool.push_back(r.a);
+        c->ev_pool.push_back(r.b);
+    }
+    c->prec.clear();
+    for (int i = 0; i < CAS_K_COUNT; ++i) {
+        if (ms) ms[i] = c->pms[i];
+        if (launches) launches[i] = c->pn[i];
+    }
+    if (reset) {
+        for (int i = 0; i < CAS_K_COUNT; ++i) {
+            c->pms[i] = 0;
+            c->pn[i] = 0;
+        }
+    }
+    return CAS_OK;
+}
+
+cas_status cas_sync(cas_ctx* c) {
+    if (!c) return CAS_ERR_ARG;
+    HIPCHK(c, hipStreamSynchronize(c->stream));
+    return CAS_OK;
+}
+
+// ---------------------------------------------------------------- kernel-level entry points
+
+cas_status cas_op_gemm(int32_t wtype, const void* W, const void* X, int32_t N, int32_t K, int32_t T, const float* xs,
+                       const float* ws, int32_t epi, void* out, int32_t ldo, void* stream) {
+    if (!W || !X || !out) return CAS_ERR_ARG;
+    if (wtype < CAS_W_F32 || wtype > CAS_W_I8) return CAS_ERR_ARG;
+    if (N < 16 || N % 16 || K < 16 || K % 16 || T < 1 || T > 128 || ldo < N) return CAS_ERR_UNSUPPORTED;
+    if (epi != CAS_EPI_STORE && epi != CAS_EPI_RESID && epi != CAS_EPI_RAW_I32) return CAS_ERR_ARG;
+    if (epi == CAS_EPI_RAW_I32 && wtype != CAS_W_I8) return CAS_ERR_UNSUPPORTED;
+    if (wtype == CAS_W_I8 && epi != CAS_EPI_RAW_I32 && (!xs || !ws)) return CAS_ERR_ARG;
+    GemmArgs a{};
+    a.W = W;
+    a.X = X;
+    a.N = N;
+    a.K = K;
+    a.T = T;
+    a.xs = xs;
+    a.ws = ws;
+    a.out = out;
+    a.ldo = ldo;
+    const int ep = epi == CAS_EPI_STORE ? EPI_STORE : epi == CAS_EPI_RESID ? EPI_RESID : EPI_RAW;
+    hipError_t e = launch_gemm(wtype, ET_F32, ep, a, (hipStream_t)stream);
+    return e == hipSuccess ? CAS_OK : CAS_ERR_DEVICE;
+}
+
+cas_status cas_op_quant_rows(int32_t atype, const void* x, int32_t T, int32_t K, int8_t* q, float* s, void* stream) {
+    if (!x || !q || !s || T < 1 || K < 1) return CAS_ERR_ARG;
+    if (atype != CAS_W_F32 && atype != CAS_W_BF16) return CAS_ERR_ARG;
+    hipError_t e = launch_quant_rows(atype, x, T, K, q, s, (hipStream_t)stream);
+    return e == hipSuccess ? CAS_OK : CAS_ERR_DEVICE;
+}
+
+cas_status cas_op_quant_weight(int32_t wtype, const void* W, int32_t N, int32_t K, int8_t* q, float* s, void* stream) {
+    if (!W || !q || !s || N < 1 || K < 1) return CAS_ERR_ARG;
+    if (wtype != CAS_W_F32 && wtype != CAS_W_BF16) return CAS_ERR_ARG;
+    hipError_t e = launch_quant_weight(wtype, W, N, K, q, s, (hipStream_t)stream);
+    return e == hipSuccess ? CAS_OK : CAS_ERR_DEVICE;
+}
+
+size_t cas_op_attention_work_bytes(int32_t Lc, int32_t n_tree, int32_t T, int32_t H, int32_t hd) {
+    return attention_work_bytes(Lc + n_tree, T, H, hd) + 64;
+}
+
+cas_status cas_op_attention(const void* q, const void* kc, const void* vt, int32_t ctx_cap, int32_t Lc, int32_t n_tree,
+                            int32_t T, int32_t H, int32_t Hkv, int32_t hd, const uint64_t* anc, void* out, void* work,
+                            size_t work_bytes, void* stream) {
+    if (!q || !kc || !vt || !anc || !out || !work) return CAS_ERR_ARG;
+    if (hd != 64 && hd != 128) return CAS_ERR_UNSUPPORTED;
+    if (T < 1 || T > 128 || n_tree < 1 || n_tree > 128 || Lc < 0 || Hkv < 1 || H < 1 || H % Hkv) return CAS_ERR_ARG;
+    if (ctx_cap % 32 || Lc + n_tree > ctx_cap) return CAS_ERR_ARG;
+    if (work_bytes < cas_op_attention_work_bytes(Lc, n_tree, T, H, hd)) return CAS_ERR_ARG;
+    hipStream_t s = (hipStream_t)stream;
+    // the step parameters live at the start of the work buffer
+    StepParams sp{Lc, 0, n_tree, 0};
+    StepParams* dsp = (StepParams*)work;
+    if (hipMemcpyAsync(dsp, &sp, sizeof sp, hipMemcpyHostToDevice, s) != hipSuccess) return CAS_ERR_DEVICE;
+    AttnArgs a{};
+    a.q = q;
+    a.kc = kc;
+    a.vt = vt;
+    a.anc = anc;
+    a.sp = dsp;
+    a.Lc_host = Lc;
+    a.n_tree_host = n_tree;
+    a.out = out;
+    const int S = attention_splits(Lc + n_tree);
+    a.part_o = (float*)((char*)work + 64);
+    a.part_ml = a.part_o + (size_t)S * H * T * hd;
+    a.T = T;
+    a.H = H;
+    a.Hkv = Hkv;
+    a.hd = hd;
+    a.ctx_cap = ctx_cap;
+    hipError_t e = launch_attention(ET_BF16, a, s);
+    if (e == hipSuccess) e = launch_attention_combine(ET_BF16, a, s);
+    if (e == hipSuccess) e = hipStreamSynchronize(s);  // sp lives on the caller's stack
+    return e == hipSuccess ? CAS_OK : CAS_ERR_DEVICE;
+}
+
+cas_status cas_op_copy(void* dst, const void* src, size_t bytes, void* stream) {
+    if (!dst || !src || bytes % 16) return CAS_ERR_ARG;
+    hipError_t e = launch_copy(dst, src, bytes, (hipStream_t)stream);
+    return e == hipSuccess ? CAS_OK : CAS_ERR_DEVICE;
+}
+
+}  // extern "C"

@@ -1,0 +1,314 @@
+"""Forward-level parity of the HIP path against the CPU oracle through the C
+ABI: tree verify, draft calls (layer skip, int8 activations), greedy
+acceptance, KV compaction, prefill, losslessness, error paths.
+
+Tolerances (per tree node row): max_v |gpu - oracle| <= tol * max_v |oracle|,
+tol = 1e-4 for fp32 decoders and 2e-2 for bf16 decoders; 1e-3 for fp32
+decoders with int8 activations (a code one step off at a rounding boundary
+moves one product by s_x * s_w).  bf16 decoders with int8 activations get
+6e-2: the bf16 probabilities of the attention's PV product move about a
+quarter of the attention outputs by one bf16 step, and each such move flips
+the next int8 code with probability ~1/6, a full code step each, so the two
+sides' drafts drift apart by about as much as int8 noise itself (measured
+2.9e-2..3.7e-2 against 3.0e-2..4.5e-2 int8-vs-full); with a single node and
+no context the attention is exact and the int8 path agrees to 1e-3.
+Acceptance and compaction are index and byte work: exact.
+"""
+import dataclasses
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import oracle as O
+from paper_2510_26843_amd import cas, decode, synth
+
+pytestmark = pytest.mark.gpu
+
+TINY = synth.SHAPES["tiny"]
+GQA = synth.ModelShape("gqa_small", 2, 512, 8, 2, 64, 1376, 1024, 5e5, 1e-6, "bf16")
+MHA = synth.ModelShape("mha_small", 2, 1024, 8, 8, 128, 2752, 4096, 1e4, 1e-6, "bf16")
+TOL = {"f32": 1e-4, "bf16": 2e-2}
+
+
+@pytest.fixture(scope="module")
+def weights():
+    return {s.name: synth.gen_weights(s, seed=9) for s in (TINY, GQA, MHA)}
+
+
+def _pair(shape, w, prompt, max_ctx=512, int8=False):
+    g = cas.Model(shape, max_ctx=max_ctx, max_tree=128)
+    g.load_weights(w)
+    if int8:
+        g.build_int8()
+    o = O.OracleModel(shape, w, max_ctx=max_ctx, int8=int8)
+    if len(prompt):
+        g.prefill(prompt)
+        o.prefill(list(prompt))
+    return g, o
+
+
+def _row_err(got, ref):
+    return float((np.abs(got - ref).max(axis=1) / np.abs(ref).max(axis=1)).max())
+
+
+@pytest.mark.parametrize("name,tree,plen", [("tiny", synth.TREE_TINY, 63), ("gqa_small", synth.TREE_7B, 40),
+                                            ("mha_small", synth.TREE_7B, 130), ("tiny", ((2,) * 7, 128), 5)])
+def test_verify_parity(weights, name, tree, plen):
+    shape = {"tiny": TINY, "gqa_small": GQA, "mha_small": MHA}[name]
+    w = weights[name]
+    prompt = synth.gen_prompt(shape.vocab, plen, seed=1)
+    parents = synth.tree_from_branching(*tree)
+    toks = synth.gen_tree_tokens(parents, shape.vocab, seed=2)
+    g, o = _pair(shape, w, prompt)
+    got = g.forward(toks, parents)
+    ref = o.forward(toks, parents)
+    err = _row_err(got, ref)
+    assert err < TOL[shape.dtype], err
+    g.close()
+
+
+@pytest.mark.parametrize("name,skip,aq,tol", [("tiny", [0, 1, 1, 0], False, 1e-4), ("tiny", [0, 1, 1, 0], True, 1e-3),
+                                              ("tiny", [1, 1, 1, 1], False, 1e-4), ("gqa_small", [0, 1], True, 6e-2),
+                                              ("mha_small", [1, 0], False, 2e-2), ("mha_small", [0, 0], True, 6e-2),
+                                              ("gqa_small", [0, 1], False, 2e-2)])
+def test_draft_parity(weights, name, skip, aq, tol):
+    shape = {"tiny": TINY, "gqa_small": GQA, "mha_small": MHA}[name]
+    w = weights[name]
+    prompt = synth.gen_prompt(shape.vocab, 33, seed=3)
+    parents = synth.tree_from_branching((3, 2, 1), 15)
+    toks = synth.gen_tree_tokens(parents, shape.vocab, seed=4)
+    g, o = _pair(shape, w, prompt, int8=aq)
+    # the tree fed depth by depth in appended calls, as tree-parallel drafts do
+    for a, b in ((0, 1), (1, 4), (4, 10), (10, 15)):
+        got = g.forward(toks[a:b], parents[a:b], a, skip=skip, act_quant=aq)
+        ref = o.forward(toks[a:b], parents[a:b], a, skip=skip, act_quant=aq)
+        err = _row_err(got, ref)
+        assert err < tol, (a, err)
+    g.close()
+
+
+@pytest.mark.parametrize("name", ["gqa_small", "mha_small"])
+def test_int8_draft_bf16_single_node(weights, name):
+    """One node with no context: attention returns v exactly on both sides, so
+    the bf16 + int8 path must agree closely (codes, scales, dequantisation,
+    bf16 epilogues)."""
+    shape = {"gqa_small": GQA, "mha_small": MHA}[name]
+    g, o = _pair(shape, weights[name], [], int8=True)
+    for tok in (3, 77, 500):
+        got = g.forward([tok], [-1], act_quant=True)
+        ref = o.forward([tok], [-1], act_quant=True)
+        err = _row_err(got, ref)
+        assert err < 1e-3, (tok, err)
+    g.close()
+
+
+def test_accept_exact_on_identical_logits(weights):
+    shape = GQA
+    prompt = synth.gen_prompt(shape.vocab, 20, seed=5)
+    o = O.OracleModel(shape, weights[shape.name], max_ctx=256)
+    o.prefill(list(prompt[:-1]))
+    ar = O.ar_decode(O.OracleModel(shape, weights[shape.name], max_ctx=256), prompt, 5)
+    g = cas.Model(shape, max_ctx=256)
+    g.load_weights(weights[shape.name])
+    g.prefill(prompt[:-1])
+    # main path = the greedy continuation, plus decoys at every level
+    parents = [-1, 0, 0, 1, 1, 3, 3, 5, 6, 7]
+    toks = [int(prompt[-1]), ar[0], (ar[0] + 1) % shape.vocab, ar[1], (ar[1] + 5) % shape.vocab, ar[2],
+            (ar[2] + 9) % shape.vocab, ar[3], 7, (ar[4] + 1) % shape.vocab]
+    lg = g.forward(toks, parents)
+    path, bonus = g.accept()
+    rpath, rbonus = O.accept_greedy(lg.astype(np.float64), parents, toks)
+    assert (path, bonus) == (rpath, rbonus)
+    g.close()
+    # random trees: identical logits give identical decisions
+    shape = TINY
+    g = cas.Model(shape, max_ctx=256)
+    g.load_weights(weights[shape.name])
+    for seed in range(6):
+        parents = synth.tree_from_branching((4, 2, 2, 1, 1), 32)
+        toks = synth.gen_tree_tokens(parents, shape.vocab, seed=seed)
+        lg = g.forward(toks, parents)
+        # force some acceptances: children carry the parent's argmax
+        am = lg.argmax(axis=1)
+        for i in range(1, 32):
+            if (i + seed) % 3 == 0 and all(toks[c] != am[parents[i]] for c in range(32) if parents[c] == parents[i]):
+                toks[i] = am[parents[i]]
+        lg = g.forward(toks, parents)
+        assert g.accept() == O.accept_greedy(lg.astype(np.float64), parents, toks)
+    g.close()
+
+
+def test_accept_requires_verify_and_rejects_nan_free_state(weights):
+    g = cas.Model(TINY, max_ctx=128)
+    g.load_weights(weights["tiny"])
+    with pytest.raises(cas.CasError) as e:
+        g.accept()
+    assert e.value.status == cas.ERR_STATE
+    parents = [-1, 0, 0]
+    g.forward([1, 2, 3], parents, skip=[0, 1, 0, 0])  # a draft call is not a verify call
+    with pytest.raises(cas.CasError) as e:
+        g.accept()
+    assert e.value.status == cas.ERR_STATE
+    g.close()
+
+
+@pytest.mark.parametrize("name", ["tiny", "mha_small"])
+def test_compaction_moves_exact_bytes(weights, name):
+    shape = {"tiny": TINY, "mha_small": MHA}[name]
+    prompt = synth.gen_prompt(shape.vocab, 50, seed=6)
+    g = cas.Model(shape, max_ctx=256)
+    g.load_weights(weights[name])
+    g.prefill(prompt)
+    Lc = g.committed
+    parents = synth.tree_from_branching((4, 2, 2, 1, 1), 32)
+    toks = synth.gen_tree_tokens(parents, shape.vocab, seed=7)
+    g.forward(toks, parents, logits=False)
+    before = [g.kv_read(l, Lc + 32) for l in range(shape.n_layers)]
+    path = [0, 2, 7, 17, 29]  # a root path: node 7 moves onto node 2's old slot
+    for a, b in zip(path[1:], path[:-1]):
+        assert parents[a] == b
+    g.compact(path)
+    assert g.committed == Lc + len(path)
+    for l in range(shape.n_layers):
+        k, v = g.kv_read(l, Lc + len(path))
+        kb, vb = before[l]
+        assert np.array_equal(k[:, :Lc], kb[:, :Lc]) and np.array_equal(v[:, :Lc], vb[:, :Lc])
+        for j, node in enumerate(path):
+            assert np.array_equal(k[:, Lc + j], kb[:, Lc + node]), (l, j)
+            assert np.array_equal(v[:, Lc + j], vb[:, Lc + node]), (l, j)
+    g.close()
+
+
+def test_prefill_and_compaction_match_oracle_cache(weights):
+    shape = TINY
+    prompt = synth.gen_prompt(shape.vocab, 200, seed=8)  # two chunks of 128 and 72
+    g, o = _pair(shape, weights["tiny"], prompt, max_ctx=512)
+    parents = synth.tree_from_branching((3, 2, 1), 15)
+    toks = synth.gen_tree_tokens(parents, shape.vocab, seed=9)
+    g.forward(toks, parents, logits=False)
+    o.forward(toks, parents)
+    path = [0, 1, 4, 10]
+    g.compact(path)
+    o.compact(path)
+    n = o.committed
+    for l in range(shape.n_layers):
+        k, v = g.kv_read(l, n)
+        for h in range(shape.n_kv_heads):
+            for s in range(0, n, 7):
+                kr, vr = o.get_kv(l, h, s)
+                assert np.abs(k[h, s] - kr).max() <= 1e-4 * (1 + np.abs(kr).max())
+                assert np.abs(v[h, s] - vr).max() <= 1e-4 * (1 + np.abs(vr).max())
+    nxt = synth.gen_tree_tokens([-1, 0, 0, 1], shape.vocab, seed=10)
+    err = _row_err(g.forward(nxt, [-1, 0, 0, 1]), o.forward(nxt, [-1, 0, 0, 1]))
+    assert err < 1e-4, err
+    g.close()
+
+
+def test_cas_decode_lossless_tiny(weights):
+    """Config: tiny fp32 decoder, 64-token prompt, 32 new tokens, two draft
+    levels (skip {1,2}; skip {1,2} + int8 activations) on the static 15-node
+    tree.  The GPU's speculative output equals plain greedy decoding of the
+    oracle and of the GPU, token for token, with tie-excusal by margin."""
+    shape = TINY
+    w = weights["tiny"]
+    prompt = [int(x) for x in synth.gen_prompt(shape.vocab, 64, seed=1)]
+    parents = synth.tree_from_branching(*synth.TREE_TINY)
+    skip = [0, 1, 1, 0]
+    levels = {0: (skip, False), 1: (skip, True), 2: (skip, True)}
+    ref = O.ar_decode(O.OracleModel(shape, w, max_ctx=256), prompt, 32)
+    g = cas.Model(shape, max_ctx=256)
+    g.load_weights(w)
+    g.build_int8()
+    excused = 0
+    out = []
+    while len(out) < 32:
+        st = {}
+        seg = decode.cas_decode_static(g, prompt + out, 32 - len(out), parents, levels, st)
+        i = next((k for k, (a, b) in enumerate(zip(seg, ref[len(out):])) if a != b), None)
+        if i is None:
+            out += seg
+            break
+        pos = len(out) + i
+        seq = prompt + ref[:pos]
+        m = O.OracleModel(shape, w, max_ctx=256)
+        m.prefill(seq[:-1])
+        lg = np.sort(m.forward([seq[-1]], [-1])[0])
+        margin = lg[-1] - lg[-2]
+        assert margin <= 0.05, f"divergence at token {pos} with oracle margin {margin}"
+        excused += 1
+        out = ref[:pos + 1]
+    assert out[:32] == ref
+    assert excused == 0  # fp32 decoder: no near-ties expected at this seed
+    ar = decode.ar_decode(g, prompt, 32)
+    assert ar == ref
+    g.close()
+
+
+@pytest.mark.parametrize("graphs", [True, False])
+def test_graph_replay_matches_direct_launch(weights, graphs):
+    shape = MHA
+    prompt = synth.gen_prompt(shape.vocab, 70, seed=11)
+    parents = synth.tree_from_branching(*synth.TREE_7B)
+    toks = synth.gen_tree_tokens(parents, shape.vocab, seed=12)
+    g = cas.Model(shape, max_ctx=256)
+    g.load_weights(weights[shape.name])
+    g.prefill(prompt)
+    g.set_graphs(False)
+    ref = g.forward(toks, parents)
+    g.set_graphs(graphs)
+    for rep in range(4):
+        got = g.forward(toks, parents)
+        assert np.array_equal(got, ref), rep
+        torch.cuda.synchronize()
+        _ = torch.ones(1024, device="cuda:0").sum().item()  # unrelated eager work between replays
+    g.close()
+
+
+def test_profile_counts_launches(weights):
+    shape = TINY
+    g = cas.Model(shape, max_ctx=128)
+    g.load_weights(weights["tiny"])
+    parents = synth.tree_from_branching((3, 2, 1), 15)
+    toks = synth.gen_tree_tokens(parents, shape.vocab, seed=13)
+    ref = g.forward(toks, parents)
+    g.profile(True)
+    got = g.forward(toks, parents)
+    prof = g.profile_read()
+    g.profile(False)
+    assert np.array_equal(got, ref)
+    assert prof["gemm_qkv"][1] == shape.n_layers and prof["gemm_head"][1] == 1
+    assert all(v[0] >= 0 for v in prof.values())
+    g.close()
+
+
+def test_validation_errors_leave_state_unchanged(weights):
+    shape = TINY
+    g = cas.Model(shape, max_ctx=50, max_tree=16)
+    g.load_weights(weights["tiny"])
+    g.prefill(synth.gen_prompt(shape.vocab, 40, seed=14))
+    toks = [1, 2, 3]
+
+    def expect(status, fn):
+        with pytest.raises(cas.CasError) as e:
+            fn()
+        assert e.value.status == status, str(e.value)
+        assert g.committed == 40
+
+    expect(cas.ERR_TREE, lambda: g.forward(toks, [-1, 2, 0]))             # parent after child
+    expect(cas.ERR_TREE, lambda: g.forward(toks, [0, 0, 1]))              # root with a parent
+    expect(cas.ERR_ARG, lambda: g.forward([1, 2, shape.vocab], [-1, 0, 1]))  # token out of range
+    expect(cas.ERR_CAPACITY, lambda: g.forward(list(range(17)), synth.chain_parents(17)))  # > max_tree
+    expect(cas.ERR_CAPACITY, lambda: g.forward(list(range(16)), synth.chain_parents(16)))  # > max_ctx
+    expect(cas.ERR_STATE, lambda: g.forward(toks, [-1, 0, 1], act_quant=True))  # no int8 copy
+    expect(cas.ERR_TREE, lambda: g.forward(toks, [0, 0, 1], node_offset=3))    # no open round
+    expect(cas.ERR_STATE, lambda: g.accept())
+    expect(cas.ERR_STATE, lambda: g.compact([0]))
+    g.forward(toks, [-1, 0, 1])
+    expect(cas.ERR_TREE, lambda: g.compact([0, 2]))                        # not a path
+    expect(cas.ERR_TREE, lambda: g.compact([1]))                           # not from the root
+    expect(cas.ERR_ARG, lambda: g.forward(toks, [-1, 0, 1], skip=[0, 2, 0, 0]))
+    path, bonus = g.accept()
+    g.compact(path)
+    assert g.committed == 40 + len(path)
+    g.close()

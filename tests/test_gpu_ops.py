@@ -1,0 +1,168 @@
+"""Kernel-level parity of the HIP library against the CPU oracle, through the
+C ABI (include/cas_ops.h), on identical seeded inputs.
+
+Bars: int8 codes, scales and integer accumulators bit-exact; the fp32/bf16
+GEMM within the rigorous fp32 summation bound K * 2^-23 * sum_k |x_k w_k|; the
+bf16 attention within 1e-2 of max |v| (probabilities are rounded to bf16 for
+the PV product: a relative 2^-9 per weight on a convex combination of v).
+"""
+import numpy as np
+import pytest
+import torch
+
+from oracle import oracle as O
+from paper_2510_26843_amd import cas, synth
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda:0"
+
+
+def _bf16_dev(bits: np.ndarray) -> torch.Tensor:
+    return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).to(DEV)
+
+
+def _f32_dev(a: np.ndarray) -> torch.Tensor:
+    return torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to(DEV)
+
+
+def _i8_dev(a: np.ndarray) -> torch.Tensor:
+    return torch.from_numpy(np.ascontiguousarray(a, dtype=np.int8)).to(DEV)
+
+
+def _gemm_bound(x64, w64):
+    K = x64.shape[1]
+    return K * 2.0 ** -23 * (np.abs(x64) @ np.abs(w64).T) + 1e-30
+
+
+@pytest.mark.parametrize("N,K,T", [(64, 4096, 32), (48, 688, 5), (32, 256, 1), (16, 1376, 17), (64, 512, 128),
+                                   (80, 11008, 64), (32, 128, 100)])
+def test_gemm_bf16(N, K, T):
+    w = synth.f32_to_bf16_bits(synth.gen_activations(N, K, seed=N + K, edge_rows=False) * 0.02)
+    x = synth.f32_to_bf16_bits(synth.gen_activations(T, K, seed=T + 7))
+    out = torch.zeros((T, N), dtype=torch.float32, device=DEV)
+    cas.op_gemm(cas.W_BF16, _bf16_dev(w), _bf16_dev(x), N, K, T, out, N)
+    torch.cuda.synchronize()
+    x64 = synth.bf16_bits_to_f32(x).astype(np.float64)
+    w64 = synth.bf16_bits_to_f32(w).astype(np.float64)
+    ref = O.matmul_rows(x64, w, bf16=True)
+    got = out.cpu().numpy()
+    assert (np.abs(got - ref) <= _gemm_bound(x64, w64)).all()
+
+
+@pytest.mark.parametrize("N,K,T", [(32, 256, 15), (16, 688, 3), (2048, 256, 7), (64, 4096, 33)])
+def test_gemm_f32_and_residual(N, K, T):
+    w = synth.gen_activations(N, K, seed=11, edge_rows=False) * np.float32(0.02)
+    x = synth.gen_activations(T, K, seed=12)
+    base = synth.gen_activations(T, N, seed=13, edge_rows=False)
+    out = _f32_dev(base)
+    cas.op_gemm(cas.W_F32, _f32_dev(w), _f32_dev(x), N, K, T, out, N, epi=cas.EPI_RESID)
+    torch.cuda.synchronize()
+    ref = base.astype(np.float64) + O.matmul_rows(x, w, bf16=False)
+    bound = _gemm_bound(x.astype(np.float64), w.astype(np.float64)) + np.abs(ref) * 2.0 ** -23
+    assert (np.abs(out.cpu().numpy() - ref) <= bound).all()
+
+
+@pytest.mark.parametrize("N,K,T", [(64, 4096, 32), (48, 688, 5), (16, 13824, 3), (32, 256, 100), (16, 5120, 64)])
+def test_gemm_int8_bit_exact(N, K, T):
+    rng = np.random.default_rng(N * 7 + K + T)
+    qw = rng.integers(-127, 128, (N, K)).astype(np.int8)
+    qx = rng.integers(-127, 128, (T, K)).astype(np.int8)
+    qx[0, :] = 127
+    qw[0, :] = 127  # largest accumulator magnitude
+    if T > 1:
+        qx[1, :] = 0
+    acc = torch.zeros((T, N), dtype=torch.int32, device=DEV)
+    cas.op_gemm(cas.W_I8, _i8_dev(qw), _i8_dev(qx), N, K, T, acc, N, epi=cas.EPI_RAW_I32)
+    xs = (rng.random(T).astype(np.float32) + np.float32(0.01)) / np.float32(127)
+    ws = (rng.random(N).astype(np.float32) + np.float32(0.01)) / np.float32(127)
+    y = torch.zeros((T, N), dtype=torch.float32, device=DEV)
+    cas.op_gemm(cas.W_I8, _i8_dev(qw), _i8_dev(qx), N, K, T, y, N, epi=cas.EPI_STORE, xs=_f32_dev(xs), ws=_f32_dev(ws))
+    torch.cuda.synchronize()
+    ref = O.dot_i8_matrix(qx, qw)
+    assert np.array_equal(acc.cpu().numpy(), ref)
+    # dequantisation in fp32: (float(acc) * s_x) * s_w
+    want = (ref.astype(np.float32) * xs[:, None]).astype(np.float32) * ws[None, :]
+    assert np.array_equal(y.cpu().numpy().view(np.uint32), want.astype(np.float32).view(np.uint32))
+
+
+@pytest.mark.parametrize("T,K,bf16", [(64, 4096, True), (9, 688, False), (3, 11008, True), (128, 256, False)])
+def test_quant_rows_bit_exact(T, K, bf16):
+    x = synth.gen_activations(T, K, seed=T + K)
+    x[min(4, T - 1), 5] = 1e-30  # tiny values next to a large one
+    if bf16:
+        xb = synth.f32_to_bf16_bits(x)
+        xf = synth.bf16_bits_to_f32(xb)
+        xd = _bf16_dev(xb)
+    else:
+        xf = x
+        xd = _f32_dev(x)
+    q = torch.zeros((T, K), dtype=torch.int8, device=DEV)
+    s = torch.zeros(T, dtype=torch.float32, device=DEV)
+    cas.op_quant_rows(cas.W_BF16 if bf16 else cas.W_F32, xd, T, K, q, s)
+    torch.cuda.synchronize()
+    qr, sr = O.quant_rows(xf)
+    assert np.array_equal(s.cpu().numpy().view(np.uint32), sr.view(np.uint32))
+    assert np.array_equal(q.cpu().numpy(), qr)
+
+
+def test_quant_weight_bit_exact():
+    shape = synth.SHAPES["llama2_7b"]
+    w = synth.gen_tensor(shape.with_layers(1), "wo", 0, seed=3)[:96]
+    q = torch.zeros(w.shape, dtype=torch.int8, device=DEV)
+    s = torch.zeros(w.shape[0], dtype=torch.float32, device=DEV)
+    cas.op_quant_weight(cas.W_BF16, _bf16_dev(w), w.shape[0], w.shape[1], q, s)
+    torch.cuda.synchronize()
+    qr, sr = O.quant_weight(w, bf16=True)
+    assert np.array_equal(s.cpu().numpy().view(np.uint32), sr.view(np.uint32))
+    assert np.array_equal(q.cpu().numpy(), qr)
+
+
+def _attention_case(H, Hkv, hd, Lc, parents, seed):
+    T = len(parents)
+    ctx_cap = ((Lc + T + 127) // 128) * 128
+    rng = np.random.default_rng(seed)
+    q = synth.f32_to_bf16_bits(rng.standard_normal((T, H, hd)).astype(np.float32) * np.float32(1.28))
+    kc = synth.f32_to_bf16_bits(rng.standard_normal((Hkv, ctx_cap, hd)).astype(np.float32) * np.float32(1.28))
+    vv = synth.f32_to_bf16_bits(rng.standard_normal((Hkv, ctx_cap, hd)).astype(np.float32))
+    vt = np.ascontiguousarray(np.transpose(vv, (0, 2, 1)))
+    _, anc = O.tree_metadata(parents)
+    anc_np = np.array([[a & (2 ** 64 - 1), a >> 64] for a in anc], dtype=np.uint64)
+    out = torch.zeros((T, H * hd), dtype=torch.int16, device=DEV)
+    work = torch.zeros(cas.op_attention_work_bytes(Lc, T, T, H, hd) // 4 + 16, dtype=torch.float32, device=DEV)
+    cas.op_attention(_bf16_dev(q), _bf16_dev(kc), _bf16_dev(vt), ctx_cap, Lc, T, T, H, Hkv, hd,
+                     torch.from_numpy(anc_np.view(np.int64)).to(DEV), out, work)
+    torch.cuda.synchronize()
+    got = synth.bf16_bits_to_f32(out.cpu().numpy().view(np.uint16)).reshape(T, H, hd)
+    qf = synth.bf16_bits_to_f32(q)
+    kf = synth.bf16_bits_to_f32(kc)
+    vf = synth.bf16_bits_to_f32(vv)
+    G = H // Hkv
+    worst = 0.0
+    for t in range(T):
+        vis = list(range(Lc)) + [Lc + j for j in range(T) if (anc[t] >> j) & 1]
+        for h in range(H):
+            ref = O.attend(qf[t, h], kf[h // G, vis], vf[h // G, vis])
+            worst = max(worst, np.abs(got[t, h] - ref).max() / np.abs(vf[h // G, vis]).max())
+    return worst
+
+
+@pytest.mark.parametrize("H,Hkv,hd,Lc,tree", [
+    (4, 4, 128, 1000, ((4, 2, 2, 1, 1), 32)),
+    (8, 2, 64, 77, ((3, 2, 1), 15)),
+    (4, 1, 128, 0, ((2, 2, 2), 9)),
+    (2, 2, 128, 0, ((), 1)),
+    (4, 2, 128, 300, ((2,) * 7, 128)),
+    (8, 8, 64, 129, ((4, 4, 4), 20)),
+])
+def test_attention_tree_mask(H, Hkv, hd, Lc, tree):
+    parents = synth.tree_from_branching(*tree) if tree[0] else [-1]
+    worst = _attention_case(H, Hkv, hd, Lc, parents, seed=Lc + hd + H)
+    assert worst < 1e-2, worst
+
+
+def test_copy_kernel():
+    src = torch.randint(-2 ** 31, 2 ** 31 - 1, (1 << 20,), dtype=torch.int32, device=DEV)
+    dst = torch.zeros_like(src)
+    cas.op_copy(dst, src, src.numel() * 4)
+    torch.cuda.synchronize()
+    assert torch.equal(src, dst)
