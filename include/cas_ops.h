@@ -33,12 +33,16 @@ typedef enum {
  *   xs, ws: for CAS_W_I8 the per-row activation scales [T] and per-output
  *           channel weight scales [N]; y = (float(acc) * xs[t]) * ws[n]
  *           (ignored for the other types; unused with CAS_EPI_RAW_I32)
+ *   work: device scratch of at least cas_op_gemm_work_bytes(...) bytes; the
+ *         operands are first rearranged there into the fragment-tiled layout
+ *         the kernel streams (the layout the library keeps its weights in)
  * Limits: N multiple of 16, K multiple of 16, 1 <= T <= 128.
  * Accumulation: fp32 (float32, bf16 inputs), exact int32 (int8 inputs).
  */
+size_t cas_op_gemm_work_bytes(int32_t wtype, int32_t N, int32_t K, int32_t T);
 cas_status cas_op_gemm(int32_t wtype, const void* W, const void* X, int32_t N, int32_t K, int32_t T,
                        const float* xs, const float* ws, int32_t epi, void* out, int32_t ldo,
-                       void* stream);
+                       void* work, size_t work_bytes, void* stream);
 
 /*
  * Per-row symmetric int8 quantisation of activations (App. C, activation
@@ -50,9 +54,12 @@ cas_status cas_op_quant_rows(int32_t atype, const void* x, int32_t T, int32_t K,
                              int8_t* q, float* s, void* stream);
 
 /* Per-output-channel int8 copy of W [N][K] (same rule, one row per output
- * channel).  wtype: CAS_W_F32 or CAS_W_BF16. */
+ * channel), through the library's tiled weight layout: q [N][K] row-major,
+ * s [N].  wtype: CAS_W_F32 or CAS_W_BF16; N and K multiples of 16; work:
+ * device scratch of cas_op_quant_weight_work_bytes(...) bytes. */
+size_t cas_op_quant_weight_work_bytes(int32_t wtype, int32_t N, int32_t K);
 cas_status cas_op_quant_weight(int32_t wtype, const void* W, int32_t N, int32_t K,
-                               int8_t* q, float* s, void* stream);
+                               int8_t* q, float* s, void* work, size_t work_bytes, void* stream);
 
 /*
  * Tree-masked attention of one layer (bf16 storage, fp32 softmax):

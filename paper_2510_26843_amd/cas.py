@@ -32,8 +32,9 @@ KCLASS = ["embed", "rmsnorm", "gemm_qkv", "attn", "attn_combine", "gemm_o", "gem
 EXPORTS = ("cas_create", "cas_destroy", "cas_last_error", "cas_create_error", "cas_load_tensor", "cas_build_int8",
            "cas_prefill", "cas_kv_load", "cas_kv_read", "cas_set_committed", "cas_committed_len", "cas_forward",
            "cas_logits_device", "cas_accept_tree", "cas_kv_compact", "cas_tree_info", "cas_set_graphs",
-           "cas_profile", "cas_profile_read", "cas_sync", "cas_op_gemm", "cas_op_quant_rows",
-           "cas_op_quant_weight", "cas_op_attention", "cas_op_attention_work_bytes", "cas_op_copy")
+           "cas_profile", "cas_profile_read", "cas_sync", "cas_op_gemm", "cas_op_gemm_work_bytes",
+           "cas_op_quant_rows", "cas_op_quant_weight", "cas_op_quant_weight_work_bytes", "cas_op_attention",
+           "cas_op_attention_work_bytes", "cas_op_copy")
 
 
 class CasError(RuntimeError):
@@ -79,9 +80,11 @@ def lib():
             "cas_profile": ([P, I], I),
             "cas_profile_read": ([P, P, P, I], I),
             "cas_sync": ([P], I),
-            "cas_op_gemm": ([I, P, P, I, I, I, P, P, I, P, I, P], I),
+            "cas_op_gemm": ([I, P, P, I, I, I, P, P, I, P, I, P, Z, P], I),
+            "cas_op_gemm_work_bytes": ([I, I, I, I], Z),
             "cas_op_quant_rows": ([I, P, I, I, P, P, P], I),
-            "cas_op_quant_weight": ([I, P, I, I, P, P, P], I),
+            "cas_op_quant_weight": ([I, P, I, I, P, P, P, Z, P], I),
+            "cas_op_quant_weight_work_bytes": ([I, I, I], Z),
             "cas_op_attention": ([P, P, P, I, I, I, I, I, I, I, P, P, P, Z, P], I),
             "cas_op_attention_work_bytes": ([I, I, I, I, I], Z),
             "cas_op_copy": ([P, P, Z, P], I),
@@ -261,10 +264,17 @@ def _ochk(st: int, what: str) -> None:
         raise CasError(st, what)
 
 
+def _work(nbytes: int):
+    import torch
+    return torch.empty(max(int(nbytes), 16), dtype=torch.uint8, device="cuda")
+
+
 def op_gemm(wtype: int, W, X, N: int, K: int, T: int, out, ldo: int, epi: int = EPI_STORE,
-            xs=None, ws=None, stream=None) -> None:
-    _ochk(lib().cas_op_gemm(wtype, _dp(W), _dp(X), N, K, T, _dp(xs), _dp(ws), epi, _dp(out), ldo, _stream(stream)),
-          "cas_op_gemm")
+            xs=None, ws=None, stream=None, work=None) -> None:
+    need = int(lib().cas_op_gemm_work_bytes(wtype, N, K, T))
+    work = _work(need) if work is None else work
+    _ochk(lib().cas_op_gemm(wtype, _dp(W), _dp(X), N, K, T, _dp(xs), _dp(ws), epi, _dp(out), ldo, _dp(work),
+                            int(work.numel() * work.element_size()), _stream(stream)), "cas_op_gemm")
 
 
 def op_quant_rows(atype: int, x, T: int, K: int, q, s, stream=None) -> None:
@@ -272,7 +282,9 @@ def op_quant_rows(atype: int, x, T: int, K: int, q, s, stream=None) -> None:
 
 
 def op_quant_weight(wtype: int, W, N: int, K: int, q, s, stream=None) -> None:
-    _ochk(lib().cas_op_quant_weight(wtype, _dp(W), N, K, _dp(q), _dp(s), _stream(stream)), "cas_op_quant_weight")
+    work = _work(lib().cas_op_quant_weight_work_bytes(wtype, N, K))
+    _ochk(lib().cas_op_quant_weight(wtype, _dp(W), N, K, _dp(q), _dp(s), _dp(work),
+                                    int(work.numel()), _stream(stream)), "cas_op_quant_weight")
 
 
 def op_attention_work_bytes(Lc: int, n_tree: int, T: int, H: int, hd: int) -> int:

@@ -9,6 +9,37 @@ namespace cas {
 
 enum ElemType { ET_F32 = 0, ET_BF16 = 1, ET_I8 = 2 };
 
+// ---------------------------------------------------------------------------
+// Fragment-tiled operand layout of the weight-streaming GEMM.
+//
+// A 16-byte fragment holds E consecutive k of one row (E = 4 fp32, 8 bf16, 16
+// int8).  A chunk covers KC = 16E consecutive k as 4 steps u x 4 lane groups
+// g: lane (g, r) holds k = c*KC + g*4E + u*E + [0, E) of row r at step u.
+// Weights are stored as 16-row tiles, each a run of chunks, each chunk 4
+// steps of 64 lane fragments (1 KB per step): a wave's load of one step is
+// 1 KB of contiguous memory.  Activations (the GEMM's B operand, T rows padded
+// to NT 16-row column tiles) are stored chunk by chunk, step by step, column
+// tile by column tile, again 1 KB per (step, column tile).  K is padded with
+// zeros to a multiple of KC.
+constexpr int FRAG_U = 4;
+__host__ __device__ inline int frag_elems(int et) { return et == ET_F32 ? 4 : (et == ET_BF16 ? 8 : 16); }
+__host__ __device__ inline int frag_elem_bytes(int et) { return et == ET_F32 ? 4 : (et == ET_BF16 ? 2 : 1); }
+__host__ __device__ inline int chunk_k(int et) { return 4 * FRAG_U * frag_elems(et); }
+__host__ __device__ inline int pad_k(int K, int et) { return (K + chunk_k(et) - 1) / chunk_k(et) * chunk_k(et); }
+// column tiles of the activation layout for T rows (the GEMM's NT)
+__host__ __device__ inline int col_tiles(int T) { return T <= 32 ? 2 : (T <= 64 ? 4 : 8); }
+// element offset of W[n][k] (padded width Kp) and of X[t][k] (NT column tiles)
+__host__ __device__ inline size_t wt_off(int n, int k, int Kp, int E) {
+    const int KC = 16 * E, c = k / KC, kk = k % KC;
+    const int g = kk / (4 * E), u = (kk / E) & 3, e = kk % E, lane = g * 16 + (n & 15);
+    return ((((size_t)(n >> 4) * (Kp / KC) + c) * FRAG_U + u) * 64 + lane) * E + e;
+}
+__host__ __device__ inline size_t xt_off(int t, int k, int NT, int E) {
+    const int KC = 16 * E, c = k / KC, kk = k % KC;
+    const int g = kk / (4 * E), u = (kk / E) & 3, e = kk % E, lane = g * 16 + (t & 15);
+    return ((((size_t)c * FRAG_U + u) * NT + (t >> 4)) * 64 + lane) * E + e;
+}
+
 // GEMM epilogues.  Rows n of the weight matrix produce output column n.
 enum Epilogue {
     EPI_STORE = 0,   // out_f32[t*ldo + n] = y
@@ -28,13 +59,14 @@ struct StepParams {
 };
 
 struct GemmArgs {
-    const void* W;      // [N][K] weights (element type wtype)
-    const void* X;      // [T][K] activations (same element type)
-    int N, K, T;
+    const void* W;      // tiled weights, N rows, padded width Kp (element type wtype)
+    const void* X;      // tiled activations, T rows in col_tiles(T) column tiles (same type)
+    int N, Kp, T;
     const float* xs;    // int8: per-row activation scales [T]
     const float* ws;    // int8: per-output-channel weight scales [N]
-    void* out;          // epilogue output
+    void* out;          // epilogue output (EPI_SWIGLU: tiled activations of width out_k)
     int ldo;
+    int out_k;          // EPI_SWIGLU: width of the output rows (the pad up to pad_k is zeroed)
     // EPI_QKV
     const float* rope_cos;  // [ctx_cap][head_dim/2]
     const float* rope_sin;
@@ -56,7 +88,8 @@ struct AttnArgs {
     const uint64_t* anc;  // [T][2]
     const StepParams* sp; // Lc, n_tree (device)
     int Lc_host, n_tree_host;  // the same values, known on the host when launching
-    void* out;            // [T][H*hd]
+    void* out;            // T rows of H*hd: tiled activations (out_tiled) or row-major
+    int out_tiled;
     float* part_o;        // [splits][H][T][hd]
     float* part_ml;       // [splits][H][T][2]
     int T, H, Hkv, hd, ctx_cap;
@@ -69,14 +102,25 @@ hipError_t launch_attention(int atype, const AttnArgs& a, hipStream_t s);
 hipError_t launch_attention_combine(int atype, const AttnArgs& a, hipStream_t s);
 
 // RMSNorm of rows of the fp32 residual stream h [T][d] with gains g:
-// writes the normalised rows in act type (out) or, with q != NULL, their int8
-// quantisation (q [T][d], qs [T]) instead.
+// writes the normalised rows as tiled activations of act type (out) or, with
+// q != NULL, their int8 quantisation (tiled int8 q, scales qs [T]) instead.
 hipError_t launch_rmsnorm(int atype, const float* h, const float* g, int T, int d, float eps,
                           void* out, int8_t* q, float* qs, hipStream_t s);
-// Per-row int8 quantisation of x [T][K] (act type).
-hipError_t launch_quant_rows(int atype, const void* x, int T, int K, int8_t* q, float* qs, hipStream_t s);
-// Per-row int8 copy of a weight matrix [N][K] (act type).
+// Per-row int8 quantisation of x [T][K] (act type).  tiled = 1: x is tiled
+// activations and q is written tiled; tiled = 0: both row-major.
+hipError_t launch_quant_rows(int atype, const void* x, int T, int K, int8_t* q, float* qs, int tiled,
+                             hipStream_t s);
+// Tiled int8 copy of a tiled weight matrix (N rows, width K): per-row scales.
 hipError_t launch_quant_weight(int wtype, const void* w, int N, int K, int8_t* q, float* qs, hipStream_t s);
+// Row-major W [rows][K] (act type) -> tiled weights of width pad_k(K).
+// Source row i lands at tiled row row0 + map(i): mode 0 map(i) = i; mode 1
+// (q/k heads of hd rows) puts rows i and i + hd/2 of a head next to each
+// other; mode 2 map(i) = 2i (interleave with another matrix at 2i + 1).
+hipError_t launch_tile_weight(int atype, const void* src, int rows, int K, void* dst, int row0, int mode, int hd,
+                              hipStream_t s);
+hipError_t launch_untile_weight_i8(const int8_t* src, int N, int K, int8_t* dst, hipStream_t s);
+// Row-major X [T][K] -> tiled activations (col_tiles(T) tiles, width pad_k).
+hipError_t launch_tile_act(int atype, const void* src, int T, int K, void* dst, hipStream_t s);
 // Embedding gather for the call's rows plus tree metadata (depth -> position,
 // slot, ancestor masks) from the round's parent array.
 hipError_t launch_embed(int atype, const void* embed, int d, const int* round_tokens, const int* round_parent,

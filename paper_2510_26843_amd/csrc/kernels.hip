@@ -99,72 +99,86 @@ __device__ __forceinline__ typename WTr<WT>::acc_t mfma_step(i32x4 a, i32x4 b, t
     }
 }
 
-// One workgroup = 16 output rows (weight rows n0..n0+15) x all T columns.
-// Its WAVES waves split the K range into contiguous runs of chunks; each wave
-// streams its weight rows through a D-stage register ring (weights and the
-// matching activation fragments are issued D chunks ahead of use, so the
+// Weights are read with ordinary loads: on gfx950 the nontemporal hint on the
+// weight stream, mixed with the activation fragments' L2 hits, cost a third of
+// the bandwidth (measured 4.3 vs 6.1 TB/s at 22016x4096, T=32).
+//
+// One workgroup = 16 output rows (one weight tile) x all T columns.  Its
+// WAVES waves split the tile's chunks into contiguous runs; each wave streams
+// its run through a D-stage register ring of UC-step stages (weights and the
+// matching activation fragments are issued D stages ahead of use, so the
 // oldest-first wait of the vector memory counter never stalls on a fresher
-// load).  Partial tiles are summed in LDS in wave order (deterministic).
-template <int WT, int NT, int U, int D, int WAVES, int EPI, typename AT>
+// load).  With the tiled layouts every load instruction of a wave reads 1 KB
+// of contiguous memory.  Every load in the ring is unconditional, so the
+// outstanding loads at the loop entry equal those at its back edge and each
+// wait is exact.  Partial tiles are summed in LDS in wave order
+// (deterministic).
+template <int WT, int NT, int UC, int D, int WAVES, int EPI, typename AT>
 __global__ void __launch_bounds__(64 * WAVES) k_gemm(const GemmArgs a) {
     using Tr = WTr<WT>;
     using ACC = typename Tr::acc_t;
-    constexpr int E = Tr::E, EB = Tr::EB;
-    constexpr int KC = 4 * U * E;  // k covered by one chunk
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    constexpr int E = Tr::E;
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // uniform: scalar branches
     const int r = lane & 15, g = lane >> 4;
-    const int n0 = blockIdx.x * 16;
-    const int K = a.K, T = a.T;
-    const int C = (K + KC - 1) / KC;
+    const int tile = blockIdx.x;
+    const int T = a.T;
+    const int C = a.Kp / (16 * E);  // chunks of the tile
     const int c0 = (wave * C) / WAVES, c1 = ((wave + 1) * C) / WAVES;
-    const int kl = g * U * E;  // this lane's first k inside a chunk
+    const int S0 = c0 * (FRAG_U / UC), S1 = c1 * (FRAG_U / UC);  // stages of UC steps
 
-    const char* wrow = (const char*)a.W + (size_t)(n0 + r) * K * EB;
-    const char* xrow[NT];
-    bool xok[NT];
-#pragma unroll
-    for (int j = 0; j < NT; ++j) {
-        const int t = 16 * j + r;
-        xok[j] = t < T;
-        xrow[j] = (const char*)a.X + (size_t)(xok[j] ? t : 0) * K * EB;
-    }
-    const i32x4 zero = {0, 0, 0, 0};
+    const char* wb = (const char*)a.W + ((size_t)tile * C * FRAG_U * 64 + lane) * 16;
+    const char* xb = (const char*)a.X + (size_t)lane * 16;
     ACC acc[NT];
 #pragma unroll
     for (int j = 0; j < NT; ++j) acc[j] = ACC{0, 0, 0, 0};
 
-    i32x4 A[D][U];
-    i32x4 B[D][NT][U];
+    i32x4 A[D][UC];
+    i32x4 B[D][NT][UC];
 
-#define CAS_GEMM_LOAD(st, cc)                                                                   \
-    do {                                                                                        \
-        _Pragma("unroll") for (int u = 0; u < U; ++u) {                                        \
-            const int k = (cc) * KC + kl + u * E;                                               \
-            const bool kv = k < K;                                                              \
-            const size_t ko = (size_t)(kv ? k : 0) * EB;                                        \
-            A[st][u] = kv ? __builtin_nontemporal_load((const i32x4*)(wrow + ko)) : zero;       \
-            _Pragma("unroll") for (int j = 0; j < NT; ++j) B[st][j][u] =                        \
-                (kv && xok[j]) ? *(const i32x4*)(xrow[j] + ko) : zero;                          \
-        }                                                                                       \
+#define CAS_GEMM_LOAD(st, stage)                                                                 \
+    do {                                                                                         \
+        const size_t q = (size_t)(stage) * UC;                                                   \
+        _Pragma("unroll") for (int u = 0; u < UC; ++u) {                                        \
+            A[st][u] = *(const i32x4*)(wb + (q + u) * 1024);                                     \
+            _Pragma("unroll") for (int j = 0; j < NT; ++j) B[st][j][u] =                         \
+                *(const i32x4*)(xb + ((q + u) * NT + j) * 1024);                                 \
+        }                                                                                        \
+    } while (0)
+#define CAS_GEMM_MMA(st)                                                                         \
+    do {                                                                                         \
+        _Pragma("unroll") for (int u = 0; u < UC; ++u)                                          \
+            _Pragma("unroll") for (int j = 0; j < NT; ++j) acc[j] =                              \
+                mfma_step<WT>(A[st][u], B[st][j][u], acc[j]);                                    \
     } while (0)
 
+    if (S1 > S0) {
 #pragma unroll
-    for (int s = 0; s < D; ++s)
-        if (c0 + s < c1) CAS_GEMM_LOAD(s, c0 + s);
-
-    for (int c = c0; c < c1; c += D) {
+        for (int s = 0; s < D; ++s) CAS_GEMM_LOAD(s, min(S0 + s, S1 - 1));
+        int c = S0;
+        for (; c + 2 * D <= S1; c += D) {
 #pragma unroll
-        for (int s = 0; s < D; ++s) {
-            const int cc = c + s;
-            if (cc < c1) {
-#pragma unroll
-                for (int u = 0; u < U; ++u)
-#pragma unroll
-                    for (int j = 0; j < NT; ++j) acc[j] = mfma_step<WT>(A[s][u], B[s][j][u], acc[j]);
-                if (cc + D < c1) CAS_GEMM_LOAD(s, cc + D);
+            for (int s = 0; s < D; ++s) {
+                CAS_GEMM_MMA(s);
+                // keep each refill behind the MMAs that free its registers
+                __builtin_amdgcn_sched_barrier(0);
+                CAS_GEMM_LOAD(s, c + s + D);
+                __builtin_amdgcn_sched_barrier(0);
             }
         }
+        // drain: fewer than 2D stages left, ring slot s holds stage c + s
+#pragma unroll
+        for (int s = 0; s < D; ++s) {
+            if (c + s < S1) {
+                CAS_GEMM_MMA(s);
+                if (c + s + D < S1) CAS_GEMM_LOAD(s, c + s + D);
+            }
+        }
+#pragma unroll
+        for (int s = 0; s < D; ++s)
+            if (c + D + s < S1) CAS_GEMM_MMA(s);
     }
+#undef CAS_GEMM_MMA
 #undef CAS_GEMM_LOAD
 
     if constexpr (WAVES > 1) {
@@ -186,7 +200,7 @@ __global__ void __launch_bounds__(64 * WAVES) k_gemm(const GemmArgs a) {
     }
 
     // ---- epilogue: lane holds y[n = n0 + 4g + i][t = 16j + r], i = 0..3
-    const int nb = n0 + 4 * g;
+    const int nb = tile * 16 + 4 * g;
 #pragma unroll
     for (int j = 0; j < NT; ++j) {
         const int t = 16 * j + r;
@@ -219,11 +233,11 @@ __global__ void __launch_bounds__(64 * WAVES) k_gemm(const GemmArgs a) {
 #pragma unroll
             for (int i = 0; i < 4; ++i) o[i] += v[i];
         } else if constexpr (EPI == EPI_SWIGLU) {
-            AT* o = (AT*)a.out + (size_t)t * a.ldo + nb / 2;
+            constexpr int EO = 16 / sizeof(AT);
 #pragma unroll
             for (int p = 0; p < 2; ++p) {
                 const float gt = v[2 * p], up = v[2 * p + 1];
-                Act<AT>::st(o, p, gt / (1.0f + expf(-gt)) * up);
+                Act<AT>::st((AT*)a.out, xt_off(t, nb / 2 + p, NT, EO), gt / (1.0f + expf(-gt)) * up);
             }
         } else if constexpr (EPI == EPI_QKV) {
             const int hd = a.hd, qrows = a.H * hd, krows = a.Hkv * hd;
@@ -259,27 +273,38 @@ __global__ void __launch_bounds__(64 * WAVES) k_gemm(const GemmArgs a) {
             }
         }
     }
+    if constexpr (EPI == EPI_SWIGLU) {
+        // the last tile also zeroes the pad columns of the output rows
+        constexpr int EO = 16 / sizeof(AT);
+        if (tile == (int)gridDim.x - 1) {
+            const int kp = (a.out_k + 16 * EO - 1) / (16 * EO) * (16 * EO);
+            const int w = kp - a.out_k;
+            for (int idx = lane; idx < T * w; idx += 64)
+                Act<AT>::st((AT*)a.out, xt_off(idx / w, a.out_k + idx % w, NT, EO), 0.f);
+        }
+    }
 }
 
 template <int WT, int NT, int EPI, typename AT>
 static hipError_t gemm_go(const GemmArgs& a, hipStream_t s) {
-    constexpr int U = NT <= 2 ? 4 : (NT == 4 ? 2 : 1);
-    constexpr int D = NT <= 2 ? 2 : 4;
-    constexpr int WAVES = 4;
-    hipLaunchKernelGGL((k_gemm<WT, NT, U, D, WAVES, EPI, AT>), dim3(a.N / 16), dim3(64 * WAVES), 0, s, a);
+    constexpr int UC = NT == 2 ? 4 : (NT == 4 ? 2 : 1);
+    constexpr int D = NT == 2 ? 2 : 4;
+    hipLaunchKernelGGL((k_gemm<WT, NT, UC, D, 4, EPI, AT>), dim3(a.N / 16), dim3(256), 0, s, a);
     return hipGetLastError();
 }
 
 template <int WT, int EPI, typename AT>
 static hipError_t gemm_nt(const GemmArgs& a, hipStream_t s) {
-    if (a.T <= 16) return gemm_go<WT, 1, EPI, AT>(a, s);
-    if (a.T <= 32) return gemm_go<WT, 2, EPI, AT>(a, s);
-    if (a.T <= 64) return gemm_go<WT, 4, EPI, AT>(a, s);
-    return gemm_go<WT, 8, EPI, AT>(a, s);
+    switch (col_tiles(a.T)) {
+    case 2: return gemm_go<WT, 2, EPI, AT>(a, s);
+    case 4: return gemm_go<WT, 4, EPI, AT>(a, s);
+    default: return gemm_go<WT, 8, EPI, AT>(a, s);
+    }
 }
 
 hipError_t launch_gemm(int wtype, int atype, int epi, const GemmArgs& a, hipStream_t s) {
-    if (a.N % 16 || a.K % 16 || a.T < 1 || a.T > 128) return hipErrorInvalidValue;
+    if (a.N % 16 || a.Kp % chunk_k(wtype) || a.Kp < chunk_k(wtype) || a.T < 1 || a.T > 128)
+        return hipErrorInvalidValue;
     const bool bf = atype == ET_BF16;
     switch (wtype) {
     case ET_F32:
@@ -311,6 +336,84 @@ hipError_t launch_gemm(int wtype, int atype, int epi, const GemmArgs& a, hipStre
         break;
     }
     return hipErrorInvalidValue;
+}
+
+// ---------------------------------------------------------------- operand tiling
+
+// Row-major weights -> tiled: one thread per 16-byte destination fragment.
+template <typename T>
+__global__ void k_tile_weight(const T* src, int rows, int K, int Kp, T* dst, int row0, int mode, int hd) {
+    constexpr int E = 16 / sizeof(T);
+    const int fpr = Kp / E;
+    const size_t total = (size_t)rows * fpr;
+    for (size_t idx = blockIdx.x * (size_t)blockDim.x + threadIdx.x; idx < total;
+         idx += (size_t)gridDim.x * blockDim.x) {
+        const int i = (int)(idx / fpr), k0 = (int)(idx % fpr) * E;
+        int dr;
+        if (mode == 1) {
+            const int head = i / hd, j = i % hd, half = hd / 2;
+            dr = head * hd + (j < half ? 2 * j : 2 * (j - half) + 1);
+        } else if (mode == 2) {
+            dr = 2 * i;
+        } else {
+            dr = i;
+        }
+        T* o = dst + wt_off(row0 + dr, k0, Kp, E);
+#pragma unroll
+        for (int e = 0; e < E; ++e) o[e] = (k0 + e < K) ? src[(size_t)i * K + k0 + e] : (T)0;
+    }
+}
+
+// Row-major activations -> tiled (pad rows and pad columns are zero).
+template <typename T>
+__global__ void k_tile_act(const T* src, int Tn, int K, int Kp, int NT, T* dst) {
+    constexpr int E = 16 / sizeof(T);
+    const int fpr = Kp / E;
+    const size_t total = (size_t)NT * 16 * fpr;
+    for (size_t idx = blockIdx.x * (size_t)blockDim.x + threadIdx.x; idx < total;
+         idx += (size_t)gridDim.x * blockDim.x) {
+        const int t = (int)(idx / fpr), k0 = (int)(idx % fpr) * E;
+        T* o = dst + xt_off(t, k0, NT, E);
+#pragma unroll
+        for (int e = 0; e < E; ++e) o[e] = (t < Tn && k0 + e < K) ? src[(size_t)t * K + k0 + e] : (T)0;
+    }
+}
+
+static unsigned grid_for(size_t n) {
+    size_t b = (n + 255) / 256;
+    if (b > 16384) b = 16384;
+    return (unsigned)(b ? b : 1);
+}
+
+hipError_t launch_tile_weight(int atype, const void* src, int rows, int K, void* dst, int row0, int mode, int hd,
+                              hipStream_t s) {
+    const int Kp = pad_k(K, atype);
+    const size_t n = (size_t)rows * (Kp / frag_elems(atype));
+    if (atype == ET_BF16)
+        hipLaunchKernelGGL(k_tile_weight<uint16_t>, dim3(grid_for(n)), dim3(256), 0, s, (const uint16_t*)src, rows, K,
+                           Kp, (uint16_t*)dst, row0, mode, hd);
+    else if (atype == ET_F32)
+        hipLaunchKernelGGL(k_tile_weight<float>, dim3(grid_for(n)), dim3(256), 0, s, (const float*)src, rows, K, Kp,
+                           (float*)dst, row0, mode, hd);
+    else
+        hipLaunchKernelGGL(k_tile_weight<int8_t>, dim3(grid_for(n)), dim3(256), 0, s, (const int8_t*)src, rows, K, Kp,
+                           (int8_t*)dst, row0, mode, hd);
+    return hipGetLastError();
+}
+
+hipError_t launch_tile_act(int atype, const void* src, int Tn, int K, void* dst, hipStream_t s) {
+    const int Kp = pad_k(K, atype), NT = col_tiles(Tn);
+    const size_t n = (size_t)NT * 16 * (Kp / frag_elems(atype));
+    if (atype == ET_BF16)
+        hipLaunchKernelGGL(k_tile_act<uint16_t>, dim3(grid_for(n)), dim3(256), 0, s, (const uint16_t*)src, Tn, K, Kp,
+                           NT, (uint16_t*)dst);
+    else if (atype == ET_F32)
+        hipLaunchKernelGGL(k_tile_act<float>, dim3(grid_for(n)), dim3(256), 0, s, (const float*)src, Tn, K, Kp, NT,
+                           (float*)dst);
+    else
+        hipLaunchKernelGGL(k_tile_act<int8_t>, dim3(grid_for(n)), dim3(256), 0, s, (const int8_t*)src, Tn, K, Kp, NT,
+                           (int8_t*)dst);
+    return hipGetLastError();
 }
 
 // ---------------------------------------------------------------- attention
@@ -511,7 +614,9 @@ __global__ void k_attn_combine(const AttnArgs a, int S) {
         L += a.part_ml[b * 2 + 1] * w;
         o += a.part_o[b * hd + d] * w;
     }
-    Act<AT>::st((AT*)a.out, (size_t)t * H * hd + (size_t)h * hd + d, L > 0.f ? o / L : 0.f);
+    const size_t oi = a.out_tiled ? xt_off(t, h * hd + d, col_tiles(T), 16 / (int)sizeof(AT))
+                                  : (size_t)t * H * hd + (size_t)h * hd + d;
+    Act<AT>::st((AT*)a.out, oi, L > 0.f ? o / L : 0.f);
 }
 
 // fp32 storage: plain attention, one workgroup per (token, head); scores of
@@ -550,7 +655,9 @@ __global__ void __launch_bounds__(256) k_attn_f32(const AttnArgs a, float scale)
     for (int d = threadIdx.x; d < hd; d += 256) {
         float o = 0.f;
         for (int s = 0; s < n_slots; ++s) o += sc[s] * vb[(size_t)d * a.ctx_cap + s];
-        ((float*)a.out)[(size_t)t * a.H * hd + (size_t)h * hd + d] = o / sum;
+        const size_t oi = a.out_tiled ? xt_off(t, h * hd + d, col_tiles(a.T), 4)
+                                      : (size_t)t * a.H * hd + (size_t)h * hd + d;
+        ((float*)a.out)[oi] = o / sum;
     }
 }
 
@@ -584,53 +691,83 @@ hipError_t launch_attention_combine(int atype, const AttnArgs& a, hipStream_t s)
 
 // ---------------------------------------------------------------- norms, quantisation
 
-static constexpr int NORM_MAXE = 32;  // rows up to 8192 elements
+static constexpr int NORM_MAXV = 8;  // float4 per thread: rows up to 8192 elements
 
+// Store 4 consecutive k (k4 a multiple of 4) of one row into tiled
+// activations: they are contiguous inside one fragment.
+__device__ __forceinline__ void st4(float* out, size_t o, float a, float b, float c, float d) {
+    *(float4*)(out + o) = make_float4(a, b, c, d);
+}
+__device__ __forceinline__ void st4(uint16_t* out, size_t o, float a, float b, float c, float d) {
+    const uint32_t lo = (uint32_t)f2bf(a) | ((uint32_t)f2bf(b) << 16);
+    const uint32_t hi = (uint32_t)f2bf(c) | ((uint32_t)f2bf(d) << 16);
+    *(uint2*)(out + o) = make_uint2(lo, hi);
+}
+__device__ __forceinline__ void st4q(int8_t* q, size_t o, float a, float b, float c, float d) {
+    const uint32_t v = (uint32_t)(uint8_t)(int8_t)a | ((uint32_t)(uint8_t)(int8_t)b << 8) |
+                       ((uint32_t)(uint8_t)(int8_t)c << 16) | ((uint32_t)(uint8_t)(int8_t)d << 24);
+    *(uint32_t*)(q + o) = v;
+}
+__device__ __forceinline__ float q8(float x, float sc) {
+    return sc != 0.f ? fminf(fmaxf(rintf(x / sc), -127.f), 127.f) : 0.f;
+}
+
+// RMSNorm of one row of the residual stream, written as tiled activations
+// (pad columns zero) or, with Q, straight to the row's int8 quantisation.
+// Loads are float4, unconditional (clamped into the row) so they issue back
+// to back; d is a multiple of 16.
 template <typename AT, bool Q>
 __global__ void __launch_bounds__(256) k_rmsnorm(const float* h, const float* gain, int d, float eps,
                                                  AT* out, int8_t* q, float* qs) {
     __shared__ float red[4];
-    const int t = blockIdx.x;
+    const int t = blockIdx.x, NT = col_tiles(gridDim.x);
     const float* x = h + (size_t)t * d;
-    float v[NORM_MAXE];
+    float4 v[NORM_MAXV], gv[NORM_MAXV];
     float ss = 0.f;
 #pragma unroll
-    for (int e = 0; e < NORM_MAXE; ++e) {
-        const int k = threadIdx.x + 256 * e;
-        v[e] = k < d ? x[k] : 0.f;
-        ss += v[e] * v[e];
+    for (int i = 0; i < NORM_MAXV; ++i) {
+        const int k4 = (threadIdx.x + 256 * i) * 4;
+        const int kc = min(k4, d - 4);
+        v[i] = *(const float4*)(x + kc);
+        gv[i] = *(const float4*)(gain + kc);
+        if (k4 >= d) v[i] = make_float4(0.f, 0.f, 0.f, 0.f);
+        ss += v[i].x * v[i].x + v[i].y * v[i].y + v[i].z * v[i].z + v[i].w * v[i].w;
     }
     ss = block_sum256(ss, red);
     const float inv = 1.0f / sqrtf(ss / (float)d + eps);
     float amax = 0.f;
 #pragma unroll
-    for (int e = 0; e < NORM_MAXE; ++e) {
-        const int k = threadIdx.x + 256 * e;
-        if (k < d) {
-            v[e] = Act<AT>::round(v[e] * inv * gain[k]);
-            if constexpr (!Q) Act<AT>::st(out, (size_t)t * d + k, v[e]);
-            amax = fmaxf(amax, fabsf(v[e]));
-        }
+    for (int i = 0; i < NORM_MAXV; ++i) {
+        v[i].x = Act<AT>::round(v[i].x * inv * gv[i].x);
+        v[i].y = Act<AT>::round(v[i].y * inv * gv[i].y);
+        v[i].z = Act<AT>::round(v[i].z * inv * gv[i].z);
+        v[i].w = Act<AT>::round(v[i].w * inv * gv[i].w);
+        amax = fmaxf(amax, fmaxf(fmaxf(fabsf(v[i].x), fabsf(v[i].y)), fmaxf(fabsf(v[i].z), fabsf(v[i].w))));
     }
-    if constexpr (Q) {
+    if constexpr (!Q) {
+        constexpr int EA = 16 / sizeof(AT);
+        const int kpa = (d + 16 * EA - 1) / (16 * EA) * (16 * EA);
+#pragma unroll
+        for (int i = 0; i < NORM_MAXV; ++i) {
+            const int k4 = (threadIdx.x + 256 * i) * 4;
+            if (k4 < kpa) st4(out, xt_off(t, k4, NT, EA), v[i].x, v[i].y, v[i].z, v[i].w);  // zero past d
+        }
+    } else {
         amax = block_max256(amax, red);
         const float sc = amax / 127.0f;
         if (threadIdx.x == 0) qs[t] = sc;
+        const int kpq = (d + 255) / 256 * 256;
 #pragma unroll
-        for (int e = 0; e < NORM_MAXE; ++e) {
-            const int k = threadIdx.x + 256 * e;
-            if (k < d) {
-                float rq = 0.f;
-                if (sc != 0.f) rq = fminf(fmaxf(rintf(v[e] / sc), -127.f), 127.f);
-                q[(size_t)t * d + k] = (int8_t)rq;
-            }
+        for (int i = 0; i < NORM_MAXV; ++i) {
+            const int k4 = (threadIdx.x + 256 * i) * 4;
+            if (k4 < kpq) st4q(q, xt_off(t, k4, NT, 16), q8(v[i].x, sc), q8(v[i].y, sc), q8(v[i].z, sc), q8(v[i].w, sc));
         }
     }
 }
 
 hipError_t launch_rmsnorm(int atype, const float* h, const float* g, int T, int d, float eps, void* out,
                           int8_t* q, float* qs, hipStream_t s) {
-    if (d > 256 * NORM_MAXE) return hipErrorInvalidValue;
+    if (d > 1024 * NORM_MAXV || d % 16) return hipErrorInvalidValue;
     if (atype == ET_BF16) {
         if (q) hipLaunchKernelGGL((k_rmsnorm<uint16_t, true>), dim3(T), dim3(256), 0, s, h, g, d, eps, (uint16_t*)out, q, qs);
         else hipLaunchKernelGGL((k_rmsnorm<uint16_t, false>), dim3(T), dim3(256), 0, s, h, g, d, eps, (uint16_t*)out, q, qs);
@@ -642,31 +779,90 @@ hipError_t launch_rmsnorm(int atype, const float* h, const float* g, int T, int 
 }
 
 // Per-row symmetric int8: s = amax / 127, q = clamp(rne(x / s), -127, 127).
-template <typename AT>
+// TILED: x is tiled activations (act type) and q is written tiled (pad zero);
+// otherwise both are row-major [T][K].
+template <typename AT, bool TILED>
 __global__ void __launch_bounds__(256) k_quant_rows(const AT* x, int K, int8_t* q, float* qs) {
     __shared__ float red[4];
-    const int t = blockIdx.x;
-    const AT* row = x + (size_t)t * K;
+    const int t = blockIdx.x, NT = col_tiles(gridDim.x);
+    constexpr int EA = 16 / sizeof(AT);
+    auto at = [&](int k) -> size_t { return TILED ? xt_off(t, k, NT, EA) : (size_t)t * K + k; };
     float amax = 0.f;
-    for (int k = threadIdx.x; k < K; k += 256) amax = fmaxf(amax, fabsf(Act<AT>::ld(row, k)));
+    for (int k = threadIdx.x; k < K; k += 256) amax = fmaxf(amax, fabsf(Act<AT>::ld(x, at(k))));
     amax = block_max256(amax, red);
     const float sc = amax / 127.0f;
     if (threadIdx.x == 0) qs[t] = sc;
-    for (int k = threadIdx.x; k < K; k += 256) {
+    const int kq = TILED ? (K + 255) / 256 * 256 : K;
+    for (int k = threadIdx.x; k < kq; k += 256) {
         float rq = 0.f;
-        if (sc != 0.f) rq = fminf(fmaxf(rintf(Act<AT>::ld(row, k) / sc), -127.f), 127.f);
-        q[(size_t)t * K + k] = (int8_t)rq;
+        if (k < K && sc != 0.f) rq = fminf(fmaxf(rintf(Act<AT>::ld(x, at(k)) / sc), -127.f), 127.f);
+        q[TILED ? xt_off(t, k, NT, 16) : (size_t)t * K + k] = (int8_t)rq;
     }
 }
 
-hipError_t launch_quant_rows(int atype, const void* x, int T, int K, int8_t* q, float* qs, hipStream_t s) {
-    if (atype == ET_BF16) hipLaunchKernelGGL(k_quant_rows<uint16_t>, dim3(T), dim3(256), 0, s, (const uint16_t*)x, K, q, qs);
-    else hipLaunchKernelGGL(k_quant_rows<float>, dim3(T), dim3(256), 0, s, (const float*)x, K, q, qs);
+hipError_t launch_quant_rows(int atype, const void* x, int T, int K, int8_t* q, float* qs, int tiled, hipStream_t s) {
+    if (atype == ET_BF16) {
+        if (tiled) hipLaunchKernelGGL((k_quant_rows<uint16_t, true>), dim3(T), dim3(256), 0, s, (const uint16_t*)x, K, q, qs);
+        else hipLaunchKernelGGL((k_quant_rows<uint16_t, false>), dim3(T), dim3(256), 0, s, (const uint16_t*)x, K, q, qs);
+    } else {
+        if (tiled) hipLaunchKernelGGL((k_quant_rows<float, true>), dim3(T), dim3(256), 0, s, (const float*)x, K, q, qs);
+        else hipLaunchKernelGGL((k_quant_rows<float, false>), dim3(T), dim3(256), 0, s, (const float*)x, K, q, qs);
+    }
     return hipGetLastError();
 }
 
+// Tiled weights (act type) -> tiled int8 copy with per-row scales, one
+// workgroup per 16-row tile: row amax over the whole row, then the codes.
+template <typename AT>
+__global__ void __launch_bounds__(256) k_quant_weight(const AT* w, int K, int8_t* q, float* qs) {
+    __shared__ unsigned amax_bits[16];
+    __shared__ float scale[16];
+    constexpr int EA = 16 / sizeof(AT);
+    const int tile = blockIdx.x, n0 = tile * 16;
+    const int Kpa = (K + 16 * EA - 1) / (16 * EA) * (16 * EA), Kpq = (K + 255) / 256 * 256;
+    if (threadIdx.x < 16) amax_bits[threadIdx.x] = 0u;
+    __syncthreads();
+    const int r = threadIdx.x & 15;
+    float m = 0.f;
+    for (int k = threadIdx.x >> 4; k < K; k += 16) m = fmaxf(m, fabsf(Act<AT>::ld(w, wt_off(n0 + r, k, Kpa, EA))));
+    atomicMax(&amax_bits[r], __float_as_uint(m));  // non-negative floats order like their bits
+    __syncthreads();
+    if (threadIdx.x < 16) {
+        const float sc = __uint_as_float(amax_bits[threadIdx.x]) / 127.0f;
+        scale[threadIdx.x] = sc;
+        qs[n0 + threadIdx.x] = sc;
+    }
+    __syncthreads();
+    const float sc = scale[r];
+    for (int k = threadIdx.x >> 4; k < Kpq; k += 16) {
+        float rq = 0.f;
+        if (k < K && sc != 0.f)
+            rq = fminf(fmaxf(rintf(Act<AT>::ld(w, wt_off(n0 + r, k, Kpa, EA)) / sc), -127.f), 127.f);
+        q[wt_off(n0 + r, k, Kpq, 16)] = (int8_t)rq;
+    }
+}
+
 hipError_t launch_quant_weight(int wtype, const void* w, int N, int K, int8_t* q, float* qs, hipStream_t s) {
-    return launch_quant_rows(wtype, w, N, K, q, qs, s);
+    if (N % 16) return hipErrorInvalidValue;
+    if (wtype == ET_BF16)
+        hipLaunchKernelGGL(k_quant_weight<uint16_t>, dim3(N / 16), dim3(256), 0, s, (const uint16_t*)w, K, q, qs);
+    else
+        hipLaunchKernelGGL(k_quant_weight<float>, dim3(N / 16), dim3(256), 0, s, (const float*)w, K, q, qs);
+    return hipGetLastError();
+}
+
+// Tiled int8 weights -> row-major (for checking the copy).
+__global__ void k_untile_weight_i8(const int8_t* src, int N, int K, int8_t* dst) {
+    const int Kp = (K + 255) / 256 * 256;
+    const size_t total = (size_t)N * K;
+    for (size_t idx = blockIdx.x * (size_t)blockDim.x + threadIdx.x; idx < total;
+         idx += (size_t)gridDim.x * blockDim.x)
+        dst[idx] = src[wt_off((int)(idx / K), (int)(idx % K), Kp, 16)];
+}
+
+hipError_t launch_untile_weight_i8(const int8_t* src, int N, int K, int8_t* dst, hipStream_t s) {
+    hipLaunchKernelGGL(k_untile_weight_i8, dim3(grid_for((size_t)N * K)), dim3(256), 0, s, src, N, K, dst);
+    return hipGetLastError();
 }
 
 // ---------------------------------------------------------------- embedding + tree metadata
@@ -675,14 +871,17 @@ template <typename AT>
 __global__ void __launch_bounds__(256) k_embed(const AT* E, int d, const int* rtok, const int* rpar,
                                                const StepParams* sp, float* h, int* row_pos, int* row_slot,
                                                uint64_t* row_anc) {
+    __shared__ int par[128];
     const int t = blockIdx.x;
-    const int node = sp->node_offset + t, Lc = sp->Lc;
+    const int node = sp->node_offset + t, Lc = sp->Lc, n_tree = sp->n_tree;
+    if (threadIdx.x < n_tree) par[threadIdx.x] = rpar[threadIdx.x];
     const int tok = rtok[node];
     for (int k = threadIdx.x; k < d; k += 256) h[(size_t)t * d + k] = Act<AT>::ld(E, (size_t)tok * d + k);
+    __syncthreads();
     if (threadIdx.x == 0) {
         int depth = 0;
         uint64_t a0 = 0, a1 = 0;
-        for (int x = node; x >= 0; x = rpar[x]) {
+        for (int x = node; x >= 0; x = par[x]) {
             if (x < 64) a0 |= 1ull << x;
             else a1 |= 1ull << (x - 64);
             if (x != node) ++depth;
@@ -707,15 +906,21 @@ hipError_t launch_embed(int atype, const void* embed, int d, const int* rtok, co
 
 // ---------------------------------------------------------------- greedy acceptance
 
-// Per-row argmax, lowest index on ties; per-row NaN flag.
+// Per-row argmax, lowest index on ties, in ACC_PARTS contiguous parts per
+// row (one workgroup each); per-part NaN flag.  The walk merges the parts in
+// increasing order, so a tie across parts also keeps the lowest index.
+static constexpr int ACC_PARTS = 8;
+
 __global__ void __launch_bounds__(256) k_accept_argmax(const float* logits, int V, int* gbuf) {
     __shared__ float sv[4];
     __shared__ int si[4], sn[4];
-    const int t = blockIdx.x;
+    const int t = blockIdx.y, part = blockIdx.x;
+    const int len = (V + ACC_PARTS - 1) / ACC_PARTS;
+    const int lo = part * len, hi = min(V, lo + len);
     const float* row = logits + (size_t)t * V;
     float best = -INFINITY;
     int bi = 0x7fffffff, nan = 0;
-    for (int v = threadIdx.x; v < V; v += 256) {
+    for (int v = lo + threadIdx.x; v < hi; v += 256) {
         const float x = row[v];
         if (x != x) nan = 1;
         else if (bi == 0x7fffffff || x > best) { best = x; bi = v; }
@@ -735,29 +940,39 @@ __global__ void __launch_bounds__(256) k_accept_argmax(const float* logits, int 
             if (sv[k] > best || (sv[k] == best && si[k] < bi)) { best = sv[k]; bi = si[k]; }
             nan |= sn[k];
         }
-        gbuf[2 * t] = bi;
-        gbuf[2 * t + 1] = nan;
+        int* o = gbuf + ((size_t)t * ACC_PARTS + part) * 3;
+        o[0] = bi;
+        o[1] = __float_as_int(best);
+        o[2] = nan;
     }
 }
 
-// Walk from the root: next = lowest-id child whose token equals the current
-// node's argmax.  result: [0] n_accepted, [1] bonus, [2] NaN, [3..] node ids.
+// Merge the parts of every row, then walk from the root: next = lowest-id
+// child whose token equals the current node's argmax.
+// result: [0] n_accepted, [1] bonus, [2] NaN, [3..] node ids.
 __global__ void __launch_bounds__(128) k_accept_walk(const int* gbuf, int T, const int* rtok, const int* rpar, int* result) {
     __shared__ int fmc[128], gs[128];
     __shared__ int nanf;
     const int i = threadIdx.x;
     if (i == 0) nanf = 0;
-    if (i < T) {
-        fmc[i] = 0x7fffffff;
-        gs[i] = gbuf[2 * i];
-    }
     __syncthreads();
     if (i < T) {
-        if (gbuf[2 * i + 1]) atomicOr(&nanf, 1);
-        if (i > 0) {
-            const int p = rpar[i];
-            if (rtok[i] == gs[p]) atomicMin(&fmc[p], i);
+        fmc[i] = 0x7fffffff;
+        float best = -INFINITY;
+        int bi = 0x7fffffff, nan = 0;
+        for (int p = 0; p < ACC_PARTS; ++p) {
+            const int* g = gbuf + ((size_t)i * ACC_PARTS + p) * 3;
+            const float b = __int_as_float(g[1]);
+            nan |= g[2];
+            if (g[0] != 0x7fffffff && (bi == 0x7fffffff || b > best)) { best = b; bi = g[0]; }
         }
+        gs[i] = bi;
+        if (nan) atomicOr(&nanf, 1);
+    }
+    __syncthreads();
+    if (i > 0 && i < T) {
+        const int p = rpar[i];
+        if (rtok[i] == gs[p]) atomicMin(&fmc[p], i);
     }
     __syncthreads();
     if (i == 0) {
@@ -777,7 +992,7 @@ __global__ void __launch_bounds__(128) k_accept_walk(const int* gbuf, int T, con
 hipError_t launch_accept(const float* logits, int T, int V, const int* rtok, const int* rpar, int* gbuf, int* result,
                          hipStream_t s) {
     if (T < 1 || T > 128) return hipErrorInvalidValue;
-    hipLaunchKernelGGL(k_accept_argmax, dim3(T), dim3(256), 0, s, logits, V, gbuf);
+    hipLaunchKernelGGL(k_accept_argmax, dim3(ACC_PARTS, T), dim3(256), 0, s, logits, V, gbuf);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(k_accept_walk, dim3(1), dim3(128), 0, s, gbuf, T, rtok, rpar, result);

@@ -56,6 +56,10 @@ struct cas_ctx {
     int et = ET_BF16;
     size_t es = 2;
     int qrows = 0, krows = 0, qkv_rows = 0, ctx_cap = 0;
+    // padded widths of the tiled weights (model type) and of the int8 copies
+    int kp_d = 0, kp_q = 0, kp_f = 0, kq_d = 0, kq_q = 0, kq_f = 0;
+    void* stage_dev = nullptr;  // device staging of one row-major tensor during loads
+    size_t stage_dev_bytes = 0;
 
     void* embed = nullptr;
     void* lm_head = nullptr;
@@ -258,6 +262,7 @@ hipError_t enqueue_forward(cas_ctx* c, int T, const uint8_t* skip, int aq) {
     at.anc = c->d_row_anc;
     at.sp = c->d_sp;
     at.out = c->d_ao;
+    at.out_tiled = 1;
     at.T = T;
     at.H = H;
     at.Hkv = Hkv;
@@ -282,7 +287,7 @@ hipError_t enqueue_forward(cas_ctx* c, int T, const uint8_t* skip, int aq) {
         GemmArgs g{};
         g.T = T;
         g.N = c->qkv_rows;
-        g.K = d;
+        g.Kp = aq ? c->kq_d : c->kp_d;
         g.W = aq ? (const void*)w.q8[0] : w.wqkv;
         g.X = aq ? (const void*)c->d_xq : c->d_xn;
         g.xs = c->d_xs;
@@ -303,11 +308,11 @@ hipError_t enqueue_forward(cas_ctx* c, int T, const uint8_t* skip, int aq) {
         at.vt = vt;
         RUN(CAS_K_ATTN, launch_attention(et, at, s));
         if (et == ET_BF16) RUN(CAS_K_ATTN_COMBINE, launch_attention_combine(et, at, s));
-        if (aq) RUN(CAS_K_QUANT, launch_quant_rows(et, c->d_ao, T, H * hd, c->d_xq, c->d_xs, s));
+        if (aq) RUN(CAS_K_QUANT, launch_quant_rows(et, c->d_ao, T, H * hd, c->d_xq, c->d_xs, 1, s));
         GemmArgs go{};
         go.T = T;
         go.N = d;
-        go.K = H * hd;
+        go.Kp = aq ? c->kq_q : c->kp_q;
         go.W = aq ? (const void*)w.q8[1] : w.wo;
         go.X = aq ? (const void*)c->d_xq : c->d_ao;
         go.xs = c->d_xs;
@@ -321,19 +326,20 @@ hipError_t enqueue_forward(cas_ctx* c, int T, const uint8_t* skip, int aq) {
         GemmArgs gu{};
         gu.T = T;
         gu.N = 2 * ffn;
-        gu.K = d;
+        gu.Kp = aq ? c->kq_d : c->kp_d;
         gu.W = aq ? (const void*)w.q8[2] : w.wgu;
         gu.X = aq ? (const void*)c->d_xq : c->d_xn;
         gu.xs = c->d_xs;
         gu.ws = w.s8[2];
         gu.out = c->d_sw;
         gu.ldo = ffn;
+        gu.out_k = ffn;
         RUN(CAS_K_GEMM_GATEUP, launch_gemm(wq, et, EPI_SWIGLU, gu, s));
-        if (aq) RUN(CAS_K_QUANT, launch_quant_rows(et, c->d_sw, T, ffn, c->d_xq, c->d_xs, s));
+        if (aq) RUN(CAS_K_QUANT, launch_quant_rows(et, c->d_sw, T, ffn, c->d_xq, c->d_xs, 1, s));
         GemmArgs gd{};
         gd.T = T;
         gd.N = d;
-        gd.K = ffn;
+        gd.Kp = aq ? c->kq_f : c->kp_f;
         gd.W = aq ? (const void*)w.q8[3] : w.wd;
         gd.X = aq ? (const void*)c->d_xq : c->d_sw;
         gd.xs = c->d_xs;
@@ -346,7 +352,7 @@ hipError_t enqueue_forward(cas_ctx* c, int T, const uint8_t* skip, int aq) {
     GemmArgs gh{};
     gh.T = T;
     gh.N = f.vocab;
-    gh.K = d;
+    gh.Kp = c->kp_d;
     gh.W = c->lm_head;
     gh.X = c->d_xn;
     gh.out = c->d_logits;
@@ -565,6 +571,8 @@ cas_status cas_create(const cas_config* cfg, int device, void* stream, cas_ctx**
     if (f.d_model % 16 || f.ffn_dim % 16 || f.vocab % 16)
         return bad(CAS_ERR_UNSUPPORTED, "d_model, ffn_dim and vocab must be multiples of 16");
     if (f.d_model > 8192 || f.ffn_dim > 65536) return bad(CAS_ERR_UNSUPPORTED, "d_model above 8192");
+    if ((f.n_heads * f.head_dim) % (f.dtype == CAS_BF16 ? 128 : 64))
+        return bad(CAS_ERR_UNSUPPORTED, "n_heads * head_dim must be a multiple of 128 (bf16) or 64 (fp32)");
     if (f.dtype != CAS_F32 && f.dtype != CAS_BF16) return bad(CAS_ERR_ARG, "dtype");
     if (f.max_tree < 1 || f.max_tree > 128) return bad(CAS_ERR_UNSUPPORTED, "max_tree must be in [1, 128]");
     if (f.max_ctx < f.max_tree) return bad(CAS_ERR_ARG, "max_ctx must be >= max_tree");
@@ -602,13 +610,19 @@ cas_status cas_create(const cas_config* cfg, int device, void* stream, cas_ctx**
     }
     const size_t es = c->es, d = f.d_model, ffn = f.ffn_dim, T = f.max_tree;
     ALLOC(c->embed, (size_t)f.vocab * d * es);
-    ALLOC(c->lm_head, (size_t)f.vocab * d * es);
+    c->kp_d = pad_k(f.d_model, c->et);
+    c->kp_q = pad_k(c->qrows, c->et);
+    c->kp_f = pad_k(f.ffn_dim, c->et);
+    c->kq_d = pad_k(f.d_model, ET_I8);
+    c->kq_q = pad_k(c->qrows, ET_I8);
+    c->kq_f = pad_k(f.ffn_dim, ET_I8);
+    ALLOC(c->lm_head, (size_t)f.vocab * c->kp_d * es);
     ALLOC(c->final_norm, d * 4);
     for (auto& w : c->layers) {
-        ALLOC(w.wqkv, (size_t)c->qkv_rows * d * es);
-        ALLOC(w.wo, d * c->qrows * es);
-        ALLOC(w.wgu, 2 * ffn * d * es);
-        ALLOC(w.wd, d * ffn * es);
+        ALLOC(w.wqkv, (size_t)c->qkv_rows * c->kp_d * es);
+        ALLOC(w.wo, d * c->kp_q * es);
+        ALLOC(w.wgu, 2 * ffn * c->kp_d * es);
+        ALLOC(w.wd, d * c->kp_f * es);
         ALLOC(w.attn_norm, d * 4);
         ALLOC(w.ffn_norm, d * 4);
     }
@@ -640,17 +654,19 @@ cas_status cas_create(const cas_config* cfg, int device, void* stream, cas_ctx**
     ALLOC(c->d_row_slot, T * 4);
     ALLOC(c->d_row_anc, T * 16);
     ALLOC(c->d_h, T * d * 4);
-    const size_t wmax = std::max(std::max(d, ffn), (size_t)c->qrows);
-    ALLOC(c->d_xn, T * wmax * es);
-    ALLOC(c->d_xq, T * wmax);
+    // tiled activations hold 128 rows (8 column tiles) of the padded width
+    const size_t kpmax = std::max(std::max(c->kp_d, c->kp_q), c->kp_f);
+    const size_t kqmax = std::max(std::max(c->kq_d, c->kq_q), c->kq_f);
+    ALLOC(c->d_xn, 128 * kpmax * es);
+    ALLOC(c->d_xq, 128 * kqmax);
     ALLOC(c->d_xs, T * 4);
     ALLOC(c->d_q, T * c->qrows * es);
-    ALLOC(c->d_ao, T * c->qrows * es);
-    ALLOC(c->d_sw, T * ffn * es);
+    ALLOC(c->d_ao, 128 * (size_t)c->kp_q * es);
+    ALLOC(c->d_sw, 128 * (size_t)c->kp_f * es);
     ALLOC(c->d_logits, T * (size_t)f.vocab * 4);
     c->part_bytes = attention_work_bytes(c->ctx_cap, (int)T, f.n_heads, f.head_dim);
     ALLOC(c->d_part, c->part_bytes);
-    ALLOC(c->d_gbuf, T * 8);
+    ALLOC(c->d_gbuf, T * 8 * 3 * 4);  // per row: 8 argmax parts of (index, value, NaN flag)
     ALLOC(c->d_result, (T + 4) * 4);
     ALLOC(c->d_acc, (T + 1) * 4);
     if (hipMemset(c->d_rtok, 0, T * 4) != hipSuccess || hipMemset(c->d_rpar, 0xff, T * 4) != hipSuccess)
@@ -681,40 +697,43 @@ cas_status cas_load_tensor(cas_ctx* c, int32_t kind, int32_t layer, const void* 
     const size_t want = tensor_elems(c, kind) * el;
     if (bytes != want)
         return fail(c, CAS_ERR_ARG, "tensor size " + std::to_string(bytes) + " bytes, expected " + std::to_string(want));
-    const size_t d = f.d_model, hd = f.head_dim, es = c->es, row = d * es;
     LayerW* w = is_global(kind) ? nullptr : &c->layers[layer];
-    auto cp = [&](void* dst) { return hipMemcpy(dst, host, bytes, hipMemcpyHostToDevice); };
     hipError_t e = hipSuccess;
-    switch (kind) {
-    case CAS_T_EMBED: e = cp(c->embed); break;
-    case CAS_T_LM_HEAD: e = cp(c->lm_head); break;
-    case CAS_T_FINAL_NORM: e = cp(c->final_norm); break;
-    case CAS_T_ATTN_NORM: e = cp(w->attn_norm); break;
-    case CAS_T_FFN_NORM: e = cp(w->ffn_norm); break;
-    case CAS_T_WO: e = cp(w->wo); break;
-    case CAS_T_W_DOWN: e = cp(w->wd); break;
-    case CAS_T_WV: e = hipMemcpy((char*)w->wqkv + (size_t)(c->qrows + c->krows) * row, host, bytes,
-                                 hipMemcpyHostToDevice); break;
-    case CAS_T_WQ:
-    case CAS_T_WK: {
-        // rows of each head reordered so RoPE pairs (i, i + hd/2) are adjacent
-        const int heads = kind == CAS_T_WQ ? f.n_heads : f.n_kv_heads;
-        char* base = (char*)w->wqkv + (kind == CAS_T_WQ ? 0 : (size_t)c->qrows * row);
-        for (int h = 0; h < heads && e == hipSuccess; ++h) {
-            const char* src = (const char*)host + (size_t)h * hd * row;
-            char* dst = base + (size_t)h * hd * row;
-            e = hipMemcpy2D(dst, 2 * row, src, row, row, hd / 2, hipMemcpyHostToDevice);
-            if (e == hipSuccess)
-                e = hipMemcpy2D(dst + row, 2 * row, src + (hd / 2) * row, row, row, hd / 2, hipMemcpyHostToDevice);
+    if (is_norm(kind) || kind == CAS_T_EMBED) {
+        void* dst = kind == CAS_T_EMBED ? c->embed
+                    : kind == CAS_T_FINAL_NORM ? (void*)c->final_norm
+                    : kind == CAS_T_ATTN_NORM ? (void*)w->attn_norm : (void*)w->ffn_norm;
+        e = hipMemcpy(dst, host, bytes, hipMemcpyHostToDevice);
+    } else {
+        // projections and the LM head: stage row-major on the device, then tile
+        if (c->stage_dev_bytes < bytes) {
+            if (c->stage_dev) {
+                (void)hipFree(c->stage_dev);
+                for (auto& p : c->allocs)
+                    if (p == c->stage_dev) p = nullptr;
+                c->stage_dev = nullptr;
+                c->stage_dev_bytes = 0;
+            }
+            if (dalloc(c, &c->stage_dev, bytes) != hipSuccess) return fail(c, CAS_ERR_OOM, "hipMalloc of the load staging buffer");
+            c->stage_dev_bytes = bytes;
         }
-        break;
-    }
-    case CAS_T_W_GATE:
-    case CAS_T_W_UP: {
-        char* dst = (char*)w->wgu + (kind == CAS_T_W_UP ? row : 0);
-        e = hipMemcpy2D(dst, 2 * row, host, row, row, f.ffn_dim, hipMemcpyHostToDevice);
-        break;
-    }
+        HIPCHK(c, hipStreamSynchronize(c->stream));
+        HIPCHK(c, hipMemcpy(c->stage_dev, host, bytes, hipMemcpyHostToDevice));
+        const int d = f.d_model, hd = f.head_dim;
+        void* dst = nullptr;
+        int rows = 0, K = d, row0 = 0, mode = 0;
+        switch (kind) {
+        case CAS_T_LM_HEAD: dst = c->lm_head; rows = f.vocab; break;
+        case CAS_T_WQ: dst = w->wqkv; rows = c->qrows; mode = 1; break;
+        case CAS_T_WK: dst = w->wqkv; rows = c->krows; row0 = c->qrows; mode = 1; break;
+        case CAS_T_WV: dst = w->wqkv; rows = c->krows; row0 = c->qrows + c->krows; break;
+        case CAS_T_WO: dst = w->wo; rows = d; K = c->qrows; break;
+        case CAS_T_W_GATE: dst = w->wgu; rows = f.ffn_dim; mode = 2; break;
+        case CAS_T_W_UP: dst = w->wgu; rows = f.ffn_dim; row0 = 1; mode = 2; break;
+        case CAS_T_W_DOWN: dst = w->wd; rows = d; K = f.ffn_dim; break;
+        }
+        e = launch_tile_weight(c->et, c->stage_dev, rows, K, dst, row0, mode, hd, c->stream);
+        if (e == hipSuccess) e = hipStreamSynchronize(c->stream);
     }
     if (e != hipSuccess) return hip_fail(c, e, "weight upload");
     if (w) {
@@ -736,9 +755,10 @@ cas_status cas_build_int8(cas_ctx* c) {
         const void* src[4] = {w.wqkv, w.wo, w.wgu, w.wd};
         const size_t N[4] = {(size_t)c->qkv_rows, d, 2 * ffn, d};
         const size_t K[4] = {d, (size_t)c->qrows, d, ffn};
+        const size_t KQ[4] = {(size_t)c->kq_d, (size_t)c->kq_q, (size_t)c->kq_d, (size_t)c->kq_f};
         for (int i = 0; i < 4; ++i) {
             if (!w.q8[i]) {
-                if (dalloc(c, &w.q8[i], N[i] * K[i]) != hipSuccess || dalloc(c, &w.s8[i], N[i] * 4) != hipSuccess)
+                if (dalloc(c, &w.q8[i], N[i] * KQ[i]) != hipSuccess || dalloc(c, &w.s8[i], N[i] * 4) != hipSuccess)
                     return fail(c, CAS_ERR_OOM, "hipMalloc of the int8 weight copy");
             }
             hipError_t e = launch_quant_weight(c->et, src[i], (int)N[i], (int)K[i], w.q8[i], w.s8[i], c->stream);
@@ -922,40 +942,68 @@ cas_status cas_sync(cas_ctx* c) {
 
 // ---------------------------------------------------------------- kernel-level entry points
 
+static size_t align256(size_t x) { return (x + 255) / 256 * 256; }
+
+size_t cas_op_gemm_work_bytes(int32_t wtype, int32_t N, int32_t K, int32_t T) {
+    if (wtype < CAS_W_F32 || wtype > CAS_W_I8 || N < 1 || K < 1 || T < 1 || T > 128) return 0;
+    const size_t Kp = pad_k(K, wtype), eb = frag_elem_bytes(wtype);
+    return align256((size_t)N * Kp * eb) + align256((size_t)16 * col_tiles(T) * Kp * eb);
+}
+
 cas_status cas_op_gemm(int32_t wtype, const void* W, const void* X, int32_t N, int32_t K, int32_t T, const float* xs,
-                       const float* ws, int32_t epi, void* out, int32_t ldo, void* stream) {
-    if (!W || !X || !out) return CAS_ERR_ARG;
+                       const float* ws, int32_t epi, void* out, int32_t ldo, void* work, size_t work_bytes,
+                       void* stream) {
+    if (!W || !X || !out || !work) return CAS_ERR_ARG;
     if (wtype < CAS_W_F32 || wtype > CAS_W_I8) return CAS_ERR_ARG;
     if (N < 16 || N % 16 || K < 16 || K % 16 || T < 1 || T > 128 || ldo < N) return CAS_ERR_UNSUPPORTED;
     if (epi != CAS_EPI_STORE && epi != CAS_EPI_RESID && epi != CAS_EPI_RAW_I32) return CAS_ERR_ARG;
     if (epi == CAS_EPI_RAW_I32 && wtype != CAS_W_I8) return CAS_ERR_UNSUPPORTED;
     if (wtype == CAS_W_I8 && epi != CAS_EPI_RAW_I32 && (!xs || !ws)) return CAS_ERR_ARG;
+    if (work_bytes < cas_op_gemm_work_bytes(wtype, N, K, T)) return CAS_ERR_ARG;
+    hipStream_t s = (hipStream_t)stream;
+    const size_t Kp = pad_k(K, wtype), eb = frag_elem_bytes(wtype);
+    void* wt = work;
+    void* xt = (char*)work + align256((size_t)N * Kp * eb);
     GemmArgs a{};
-    a.W = W;
-    a.X = X;
+    a.W = wt;
+    a.X = xt;
     a.N = N;
-    a.K = K;
+    a.Kp = (int)Kp;
     a.T = T;
     a.xs = xs;
     a.ws = ws;
     a.out = out;
     a.ldo = ldo;
     const int ep = epi == CAS_EPI_STORE ? EPI_STORE : epi == CAS_EPI_RESID ? EPI_RESID : EPI_RAW;
-    hipError_t e = launch_gemm(wtype, ET_F32, ep, a, (hipStream_t)stream);
+    hipError_t e = launch_tile_weight(wtype, W, N, K, wt, 0, 0, 0, s);
+    if (e == hipSuccess) e = launch_tile_act(wtype, X, T, K, xt, s);
+    if (e == hipSuccess) e = launch_gemm(wtype, ET_F32, ep, a, s);
     return e == hipSuccess ? CAS_OK : CAS_ERR_DEVICE;
 }
 
 cas_status cas_op_quant_rows(int32_t atype, const void* x, int32_t T, int32_t K, int8_t* q, float* s, void* stream) {
     if (!x || !q || !s || T < 1 || K < 1) return CAS_ERR_ARG;
     if (atype != CAS_W_F32 && atype != CAS_W_BF16) return CAS_ERR_ARG;
-    hipError_t e = launch_quant_rows(atype, x, T, K, q, s, (hipStream_t)stream);
+    hipError_t e = launch_quant_rows(atype, x, T, K, q, s, 0, (hipStream_t)stream);
     return e == hipSuccess ? CAS_OK : CAS_ERR_DEVICE;
 }
 
-cas_status cas_op_quant_weight(int32_t wtype, const void* W, int32_t N, int32_t K, int8_t* q, float* s, void* stream) {
-    if (!W || !q || !s || N < 1 || K < 1) return CAS_ERR_ARG;
+size_t cas_op_quant_weight_work_bytes(int32_t wtype, int32_t N, int32_t K) {
+    if ((wtype != CAS_W_F32 && wtype != CAS_W_BF16) || N < 1 || K < 1) return 0;
+    return align256((size_t)N * pad_k(K, wtype) * frag_elem_bytes(wtype)) + align256((size_t)N * pad_k(K, ET_I8));
+}
+
+cas_status cas_op_quant_weight(int32_t wtype, const void* W, int32_t N, int32_t K, int8_t* q, float* s, void* work,
+                               size_t work_bytes, void* stream) {
+    if (!W || !q || !s || !work || N < 16 || N % 16 || K < 16 || K % 16) return CAS_ERR_ARG;
     if (wtype != CAS_W_F32 && wtype != CAS_W_BF16) return CAS_ERR_ARG;
-    hipError_t e = launch_quant_weight(wtype, W, N, K, q, s, (hipStream_t)stream);
+    if (work_bytes < cas_op_quant_weight_work_bytes(wtype, N, K)) return CAS_ERR_ARG;
+    hipStream_t st = (hipStream_t)stream;
+    void* wt = work;
+    int8_t* qt = (int8_t*)((char*)work + align256((size_t)N * pad_k(K, wtype) * frag_elem_bytes(wtype)));
+    hipError_t e = launch_tile_weight(wtype, W, N, K, wt, 0, 0, 0, st);
+    if (e == hipSuccess) e = launch_quant_weight(wtype, wt, N, K, qt, s, st);
+    if (e == hipSuccess) e = launch_untile_weight_i8(qt, N, K, q, st);
     return e == hipSuccess ? CAS_OK : CAS_ERR_DEVICE;
 }
 
@@ -985,6 +1033,7 @@ cas_status cas_op_attention(const void* q, const void* kc, const void* vt, int32
     a.Lc_host = Lc;
     a.n_tree_host = n_tree;
     a.out = out;
+    a.out_tiled = 0;
     const int S = attention_splits(Lc + n_tree);
     a.part_o = (float*)((char*)work + 64);
     a.part_ml = a.part_o + (size_t)S * H * T * hd;
