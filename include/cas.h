@@ -64,7 +64,8 @@ typedef enum { CAS_F32 = 0, CAS_BF16 = 1 } cas_dtype;
  * grouped-query attention (query head h uses kv head h/(n_heads/n_kv_heads)),
  * SwiGLU FFN, no biases, untied embedding and LM head.
  * Limits: d_model, ffn_dim multiples of 16; head_dim 64 or 128;
- * max_tree <= 128; fp32 models need max_ctx <= 4096. */
+ * n_heads * head_dim a multiple of 128 (bf16) or 64 (fp32); max_tree <= 128;
+ * max_ctx <= 16256 (fp32 models: <= 3968). */
 typedef struct {
     int32_t n_layers, d_model, n_heads, n_kv_heads, head_dim, ffn_dim, vocab;
     float rope_theta, rms_eps;
@@ -184,9 +185,9 @@ cas_status cas_set_graphs(cas_ctx* ctx, int32_t enable);
  * milliseconds and the launch count since the last reset (synchronises). */
 typedef enum {
     CAS_K_EMBED = 0, CAS_K_RMSNORM = 1, CAS_K_GEMM_QKV = 2, CAS_K_ATTN = 3,
-    CAS_K_ATTN_COMBINE = 4, CAS_K_GEMM_O = 5, CAS_K_GEMM_GATEUP = 6,
-    CAS_K_GEMM_DOWN = 7, CAS_K_GEMM_HEAD = 8, CAS_K_QUANT = 9,
-    CAS_K_ACCEPT = 10, CAS_K_COMPACT = 11, CAS_K_COUNT = 12
+    CAS_K_GEMM_O = 4, CAS_K_GEMM_GATEUP = 5, CAS_K_GEMM_DOWN = 6,
+    CAS_K_GEMM_HEAD = 7, CAS_K_QUANT = 8, CAS_K_ACCEPT = 9, CAS_K_COMPACT = 10,
+    CAS_K_COUNT = 11
 } cas_kclass;
 cas_status cas_profile(cas_ctx* ctx, int32_t enable);
 cas_status cas_profile_read(cas_ctx* ctx, double* ms, int32_t* launches, int32_t reset);

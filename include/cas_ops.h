@@ -64,23 +64,23 @@ cas_status cas_op_quant_weight(int32_t wtype, const void* W, int32_t N, int32_t 
 /*
  * Tree-masked attention of one layer (bf16 storage, fp32 softmax):
  *   q:   [T][n_heads][head_dim] bf16 (after RoPE)
- *   kc:  [n_kv_heads][ctx_cap][head_dim] bf16 key cache
- *   vt:  [n_kv_heads][head_dim][ctx_cap] bf16 value cache, slot-contiguous
+ *   k:   [n_kv_heads][ctx_cap][head_dim] bf16 keys (row-major)
+ *   v:   [n_kv_heads][ctx_cap][head_dim] bf16 values (row-major)
  *   anc: [T][2] 64-bit ancestor-or-self masks over the round's nodes
  *        (bit j = node j, whose slot is Lc + j)
  *   out: [T][n_heads*head_dim] bf16
  * Query row t sees slots [0, Lc) and the slots Lc + j of the nodes j set in
  * anc[t]; n_tree nodes exist (Lc + n_tree <= ctx_cap, n_tree <= 128;
- * ctx_cap a multiple of 32: key tiles of 32 slots are read whole).
- * head_dim 64 or 128; T <= 128.  Uses `work` (device, at least
- * cas_op_attention_work_bytes(...) bytes) for split partial results.
+ * ctx_cap a multiple of 32).  head_dim 64 or 128; T <= 128.  work: device
+ * scratch of cas_op_attention_work_bytes(...) bytes (the keys and values are
+ * first copied there into the library's cache layout).
  */
-cas_status cas_op_attention(const void* q, const void* kc, const void* vt, int32_t ctx_cap,
+cas_status cas_op_attention(const void* q, const void* k, const void* v, int32_t ctx_cap,
                             int32_t Lc, int32_t n_tree, int32_t T, int32_t n_heads,
                             int32_t n_kv_heads, int32_t head_dim, const uint64_t* anc,
                             void* out, void* work, size_t work_bytes, void* stream);
 size_t cas_op_attention_work_bytes(int32_t Lc, int32_t n_tree, int32_t T, int32_t n_heads,
-                                   int32_t head_dim);
+                                   int32_t head_dim, int32_t n_kv_heads, int32_t ctx_cap);
 
 /* Plain device copy kernel (16-byte vector loads and stores): the reference
  * traffic for calibrating HBM byte counters.  bytes must be a multiple of 16. */

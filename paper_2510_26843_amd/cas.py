@@ -25,8 +25,8 @@ W_F32, W_BF16, W_I8 = 0, 1, 2
 EPI_STORE, EPI_RESID, EPI_RAW_I32 = 0, 1, 2
 TENSOR = {"embed": 0, "lm_head": 1, "final_norm": 2, "attn_norm": 3, "ffn_norm": 4, "wq": 5, "wk": 6,
           "wv": 7, "wo": 8, "w_gate": 9, "w_up": 10, "w_down": 11}
-KCLASS = ["embed", "rmsnorm", "gemm_qkv", "attn", "attn_combine", "gemm_o", "gemm_gateup", "gemm_down",
-          "gemm_head", "quant", "accept", "compact"]
+KCLASS = ["embed", "rmsnorm", "gemm_qkv", "attn", "gemm_o", "gemm_gateup", "gemm_down", "gemm_head", "quant",
+          "accept", "compact"]
 
 # every symbol the two headers declare
 EXPORTS = ("cas_create", "cas_destroy", "cas_last_error", "cas_create_error", "cas_load_tensor", "cas_build_int8",
@@ -86,7 +86,7 @@ def lib():
             "cas_op_quant_weight": ([I, P, I, I, P, P, P, Z, P], I),
             "cas_op_quant_weight_work_bytes": ([I, I, I], Z),
             "cas_op_attention": ([P, P, P, I, I, I, I, I, I, I, P, P, P, Z, P], I),
-            "cas_op_attention_work_bytes": ([I, I, I, I, I], Z),
+            "cas_op_attention_work_bytes": ([I, I, I, I, I, I, I], Z),
             "cas_op_copy": ([P, P, Z, P], I),
         }
         for name, (args, res) in sig.items():
@@ -287,15 +287,12 @@ def op_quant_weight(wtype: int, W, N: int, K: int, q, s, stream=None) -> None:
                                     int(work.numel()), _stream(stream)), "cas_op_quant_weight")
 
 
-def op_attention_work_bytes(Lc: int, n_tree: int, T: int, H: int, hd: int) -> int:
-    return int(lib().cas_op_attention_work_bytes(Lc, n_tree, T, H, hd))
-
-
-def op_attention(q, kc, vt, ctx_cap: int, Lc: int, n_tree: int, T: int, H: int, Hkv: int, hd: int, anc, out,
-                 work, stream=None) -> None:
-    _ochk(lib().cas_op_attention(_dp(q), _dp(kc), _dp(vt), ctx_cap, Lc, n_tree, T, H, Hkv, hd, _dp(anc), _dp(out),
-                                 _dp(work), int(work.numel() * work.element_size()), _stream(stream)),
-          "cas_op_attention")
+def op_attention(q, k, v, ctx_cap: int, Lc: int, n_tree: int, T: int, H: int, Hkv: int, hd: int, anc, out,
+                 stream=None) -> None:
+    """k, v: [Hkv][ctx_cap][hd] bf16 row-major device tensors."""
+    work = _work(lib().cas_op_attention_work_bytes(Lc, n_tree, T, H, hd, Hkv, ctx_cap))
+    _ochk(lib().cas_op_attention(_dp(q), _dp(k), _dp(v), ctx_cap, Lc, n_tree, T, H, Hkv, hd, _dp(anc), _dp(out),
+                                 _dp(work), int(work.numel()), _stream(stream)), "cas_op_attention")
 
 
 def op_copy(dst, src, nbytes: int, stream=None) -> None:

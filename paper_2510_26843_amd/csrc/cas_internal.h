@@ -40,6 +40,32 @@ __host__ __device__ inline size_t xt_off(int t, int k, int NT, int E) {
     return ((((size_t)c * FRAG_U + u) * NT + (t >> 4)) * 64 + lane) * E + e;
 }
 
+// ---------------------------------------------------------------------------
+// KV cache layout: one block of ctx_cap x hd elements per (layer, kv head).
+// fp32 models: K row-major [slot][hd], V slot-contiguous [hd][slot].
+// bf16 models: 32-slot tiles of 32*hd elements, each laid out as the MFMA
+// fragments the tree attention reads, so every wave load is 1 KB contiguous:
+//   K: fragment (h2, u) of 64 lanes x 8 elements; lane (g, r) holds key
+//      slot 8*(r/4) + 4*h2 + r%4 of the tile, d = g*hd/4 + u*8 + [0, 8)
+//   V: fragment dt of 64 lanes x 8 elements; lane (g, r) holds d = 16*dt + r,
+//      slots 8*g + [0, 8) of the tile
+__host__ __device__ inline size_t kv_k_tiled(int slot, int d, int hd) {
+    const int ti = slot >> 5, sl = slot & 31;
+    const int r = 4 * (sl >> 3) + (sl & 3), h2 = (sl >> 2) & 1;
+    const int dg = hd / 4, g = d / dg, u = (d % dg) >> 3, e = d & 7;
+    return (size_t)ti * 32 * hd + ((size_t)(h2 * (hd / 32) + u) * 64 + g * 16 + r) * 8 + e;
+}
+__host__ __device__ inline size_t kv_v_tiled(int slot, int d, int hd) {
+    const int ti = slot >> 5, sl = slot & 31;
+    return (size_t)ti * 32 * hd + ((size_t)(d >> 4) * 64 + (sl >> 3) * 16 + (d & 15)) * 8 + (sl & 7);
+}
+__host__ __device__ inline size_t kv_k_off(int et, int slot, int d, int hd, int ctx_cap) {
+    return et == ET_BF16 ? kv_k_tiled(slot, d, hd) : (size_t)slot * hd + d;
+}
+__host__ __device__ inline size_t kv_v_off(int et, int slot, int d, int hd, int ctx_cap) {
+    return et == ET_BF16 ? kv_v_tiled(slot, d, hd) : (size_t)d * ctx_cap + slot;
+}
+
 // GEMM epilogues.  Rows n of the weight matrix produce output column n.
 enum Epilogue {
     EPI_STORE = 0,   // out_f32[t*ldo + n] = y
@@ -72,8 +98,8 @@ struct GemmArgs {
     const float* rope_sin;
     const int* row_pos;     // [T] RoPE position of each row
     const int* row_slot;    // [T] KV slot of each row
-    void* kc;               // [Hkv][ctx_cap][hd] (act type)
-    void* vt;               // [Hkv][hd][ctx_cap] (act type)
+    void* kc;               // key cache of the layer (act type, cache layout)
+    void* vt;               // value cache of the layer (act type, cache layout)
     int H, Hkv, hd, ctx_cap;
 };
 
@@ -83,8 +109,8 @@ hipError_t launch_gemm(int wtype, int atype, int epi, const GemmArgs& a, hipStre
 
 struct AttnArgs {
     const void* q;        // [T][H][hd]
-    const void* kc;       // [Hkv][ctx_cap][hd]
-    const void* vt;       // [Hkv][hd][ctx_cap]
+    const void* kc;       // key cache of the layer, Hkv blocks (cache layout)
+    const void* vt;       // value cache of the layer, Hkv blocks (cache layout)
     const uint64_t* anc;  // [T][2]
     const StepParams* sp; // Lc, n_tree (device)
     int Lc_host, n_tree_host;  // the same values, known on the host when launching
@@ -96,10 +122,13 @@ struct AttnArgs {
 };
 size_t attention_work_bytes(int n_slots, int T, int H, int hd);
 int attention_splits(int n_slots);
-// atype: ET_BF16 (MFMA path, then launch_attention_combine merges the KV
-// splits) or ET_F32 (plain path, ctx_cap <= 4096, no combine step)
+// atype: ET_BF16 (MFMA path, then the merge of the KV splits) or ET_F32
+// (plain path, ctx_cap <= 4096)
 hipError_t launch_attention(int atype, const AttnArgs& a, hipStream_t s);
-hipError_t launch_attention_combine(int atype, const AttnArgs& a, hipStream_t s);
+// Copy n slots of every kv head between the row-major [Hkv][n][hd] form and
+// the cache layout of one layer (to_cache = 1: into the cache).
+hipError_t launch_kv_convert(int atype, void* kc, void* vt, const void* k_rows, const void* v_rows, int Hkv,
+                             int n, int hd, int ctx_cap, int to_cache, hipStream_t s);
 
 // RMSNorm of rows of the fp32 residual stream h [T][d] with gains g:
 // writes the normalised rows as tiled activations of act type (out) or, with

@@ -9,6 +9,7 @@
 //                fp32 logits (LM head)
 //   k_attn_bf16  tree-masked attention: QK^T and PV on MFMA, ancestor masks
 //                in registers, fp32 online softmax, split over KV slots
+//   k_attn_merge merge of the KV splits
 //   k_rmsnorm    RMSNorm (optionally straight to per-token int8)
 //   k_accept_*   greedy acceptance (argmax + tree walk)
 //   k_compact    KV compaction of the accepted path
@@ -99,107 +100,11 @@ __device__ __forceinline__ typename WTr<WT>::acc_t mfma_step(i32x4 a, i32x4 b, t
     }
 }
 
-// Weights are read with ordinary loads: on gfx950 the nontemporal hint on the
-// weight stream, mixed with the activation fragments' L2 hits, cost a third of
-// the bandwidth (measured 4.3 vs 6.1 TB/s at 22016x4096, T=32).
-//
-// One workgroup = 16 output rows (one weight tile) x all T columns.  Its
-// WAVES waves split the tile's chunks into contiguous runs; each wave streams
-// its run through a D-stage register ring of UC-step stages (weights and the
-// matching activation fragments are issued D stages ahead of use, so the
-// oldest-first wait of the vector memory counter never stalls on a fresher
-// load).  With the tiled layouts every load instruction of a wave reads 1 KB
-// of contiguous memory.  Every load in the ring is unconditional, so the
-// outstanding loads at the loop entry equal those at its back edge and each
-// wait is exact.  Partial tiles are summed in LDS in wave order
-// (deterministic).
-template <int WT, int NT, int UC, int D, int WAVES, int EPI, typename AT>
-__global__ void __launch_bounds__(64 * WAVES) k_gemm(const GemmArgs a) {
-    using Tr = WTr<WT>;
-    using ACC = typename Tr::acc_t;
-    constexpr int E = Tr::E;
-    const int lane = threadIdx.x & 63;
-    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // uniform: scalar branches
-    const int r = lane & 15, g = lane >> 4;
-    const int tile = blockIdx.x;
-    const int T = a.T;
-    const int C = a.Kp / (16 * E);  // chunks of the tile
-    const int c0 = (wave * C) / WAVES, c1 = ((wave + 1) * C) / WAVES;
-    const int S0 = c0 * (FRAG_U / UC), S1 = c1 * (FRAG_U / UC);  // stages of UC steps
-
-    const char* wb = (const char*)a.W + ((size_t)tile * C * FRAG_U * 64 + lane) * 16;
-    const char* xb = (const char*)a.X + (size_t)lane * 16;
-    ACC acc[NT];
-#pragma unroll
-    for (int j = 0; j < NT; ++j) acc[j] = ACC{0, 0, 0, 0};
-
-    i32x4 A[D][UC];
-    i32x4 B[D][NT][UC];
-
-#define CAS_GEMM_LOAD(st, stage)                                                                 \
-    do {                                                                                         \
-        const size_t q = (size_t)(stage) * UC;                                                   \
-        _Pragma("unroll") for (int u = 0; u < UC; ++u) {                                        \
-            A[st][u] = *(const i32x4*)(wb + (q + u) * 1024);                                     \
-            _Pragma("unroll") for (int j = 0; j < NT; ++j) B[st][j][u] =                         \
-                *(const i32x4*)(xb + ((q + u) * NT + j) * 1024);                                 \
-        }                                                                                        \
-    } while (0)
-#define CAS_GEMM_MMA(st)                                                                         \
-    do {                                                                                         \
-        _Pragma("unroll") for (int u = 0; u < UC; ++u)                                          \
-            _Pragma("unroll") for (int j = 0; j < NT; ++j) acc[j] =                              \
-                mfma_step<WT>(A[st][u], B[st][j][u], acc[j]);                                    \
-    } while (0)
-
-    if (S1 > S0) {
-#pragma unroll
-        for (int s = 0; s < D; ++s) CAS_GEMM_LOAD(s, min(S0 + s, S1 - 1));
-        int c = S0;
-        for (; c + 2 * D <= S1; c += D) {
-#pragma unroll
-            for (int s = 0; s < D; ++s) {
-                CAS_GEMM_MMA(s);
-                // keep each refill behind the MMAs that free its registers
-                __builtin_amdgcn_sched_barrier(0);
-                CAS_GEMM_LOAD(s, c + s + D);
-                __builtin_amdgcn_sched_barrier(0);
-            }
-        }
-        // drain: fewer than 2D stages left, ring slot s holds stage c + s
-#pragma unroll
-        for (int s = 0; s < D; ++s) {
-            if (c + s < S1) {
-                CAS_GEMM_MMA(s);
-                if (c + s + D < S1) CAS_GEMM_LOAD(s, c + s + D);
-            }
-        }
-#pragma unroll
-        for (int s = 0; s < D; ++s)
-            if (c + D + s < S1) CAS_GEMM_MMA(s);
-    }
-#undef CAS_GEMM_MMA
-#undef CAS_GEMM_LOAD
-
-    if constexpr (WAVES > 1) {
-        using S = typename std::conditional<WT == ET_I8, int, float>::type;
-        __shared__ S red[WAVES - 1][NT][4][64];
-        if (wave > 0) {
-#pragma unroll
-            for (int j = 0; j < NT; ++j)
-#pragma unroll
-                for (int i = 0; i < 4; ++i) red[wave - 1][j][i][lane] = acc[j][i];
-        }
-        __syncthreads();
-        if (wave != 0) return;
-        for (int w = 1; w < WAVES; ++w)
-#pragma unroll
-            for (int j = 0; j < NT; ++j)
-#pragma unroll
-                for (int i = 0; i < 4; ++i) acc[j][i] += red[w - 1][j][i][lane];
-    }
-
-    // ---- epilogue: lane holds y[n = n0 + 4g + i][t = 16j + r], i = 0..3
+// Epilogue of one 16-row weight tile: lane holds y[n = 16*tile + 4g + i][t = 16j + r].
+template <int WT, int NT, int EPI, typename AT>
+__device__ __forceinline__ void gemm_epilogue(const GemmArgs& a, const typename WTr<WT>::acc_t (&acc)[NT], int tile,
+                                              int last_tile, int lane) {
+    const int r = lane & 15, g = lane >> 4, T = a.T;
     const int nb = tile * 16 + 4 * g;
 #pragma unroll
     for (int j = 0; j < NT; ++j) {
@@ -259,24 +164,26 @@ __global__ void __launch_bounds__(64 * WAVES) k_gemm(const GemmArgs a) {
                         Act<AT>::st(o, pp, lo);
                         Act<AT>::st(o, pp + half, hi);
                     } else {
-                        AT* o = (AT*)a.kc + ((size_t)head * a.ctx_cap + slot) * hd;
-                        Act<AT>::st(o, pp, lo);
-                        Act<AT>::st(o, pp + half, hi);
+                        constexpr int ET = sizeof(AT) == 2 ? ET_BF16 : ET_F32;
+                        AT* o = (AT*)a.kc + (size_t)head * a.ctx_cap * hd;
+                        Act<AT>::st(o, kv_k_off(ET, slot, pp, hd, a.ctx_cap), lo);
+                        Act<AT>::st(o, kv_k_off(ET, slot, pp + half, hd, a.ctx_cap), hi);
                     }
                 }
             } else {
+                constexpr int ET = sizeof(AT) == 2 ? ET_BF16 : ET_F32;
                 const int rel = nb - qrows - krows;
                 const int head = rel / hd, dd = rel % hd;
-                AT* o = (AT*)a.vt + ((size_t)head * hd + dd) * a.ctx_cap + slot;
+                AT* o = (AT*)a.vt + (size_t)head * a.ctx_cap * hd;
 #pragma unroll
-                for (int i = 0; i < 4; ++i) Act<AT>::st(o, (size_t)i * a.ctx_cap, v[i]);
+                for (int i = 0; i < 4; ++i) Act<AT>::st(o, kv_v_off(ET, slot, dd + i, hd, a.ctx_cap), v[i]);
             }
         }
     }
     if constexpr (EPI == EPI_SWIGLU) {
         // the last tile also zeroes the pad columns of the output rows
         constexpr int EO = 16 / sizeof(AT);
-        if (tile == (int)gridDim.x - 1) {
+        if (tile == last_tile) {
             const int kp = (a.out_k + 16 * EO - 1) / (16 * EO) * (16 * EO);
             const int w = kp - a.out_k;
             for (int idx = lane; idx < T * w; idx += 64)
@@ -285,9 +192,195 @@ __global__ void __launch_bounds__(64 * WAVES) k_gemm(const GemmArgs a) {
     }
 }
 
+// Weights are streamed with nontemporal loads (read once per forward; the
+// hint keeps them from displacing the activation fragments, which every
+// workgroup re-reads from L2).
+//
+// One workgroup = 16 output rows (one weight tile) x all T columns.  Its
+// WAVES waves split the tile's chunks into contiguous runs; each wave streams
+// its run through a D-stage register ring of UC-step stages (weights and the
+// matching activation fragments are issued D stages ahead of use, so the
+// oldest-first wait of the vector memory counter never stalls on a fresher
+// load).  With the tiled layouts every load instruction of a wave reads 1 KB
+// of contiguous memory.  Every load in the ring is unconditional, so the
+// outstanding loads at the loop entry equal those at its back edge and each
+// wait is exact.  Partial tiles are summed in LDS in wave order
+// (deterministic).
+template <int WT, int NT, int UC, int D, int WAVES, int EPI, typename AT>
+__global__ void __launch_bounds__(64 * WAVES) k_gemm(const GemmArgs a) {
+    using Tr = WTr<WT>;
+    using ACC = typename Tr::acc_t;
+    constexpr int E = Tr::E;
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // uniform: scalar branches
+    const int r = lane & 15, g = lane >> 4;
+    const int tile = blockIdx.x;
+    const int T = a.T;
+    const int C = a.Kp / (16 * E);  // chunks of the tile
+    const int c0 = (wave * C) / WAVES, c1 = ((wave + 1) * C) / WAVES;
+    const int S0 = c0 * (FRAG_U / UC), S1 = c1 * (FRAG_U / UC);  // stages of UC steps
+
+    const char* wb = (const char*)a.W + ((size_t)tile * C * FRAG_U * 64 + lane) * 16;
+    const char* xb = (const char*)a.X + (size_t)lane * 16;
+    ACC acc[NT];
+#pragma unroll
+    for (int j = 0; j < NT; ++j) acc[j] = ACC{0, 0, 0, 0};
+
+    i32x4 A[D][UC];
+    i32x4 B[D][NT][UC];
+
+#define CAS_GEMM_LOAD(st, stage)                                                                 \
+    do {                                                                                         \
+        const size_t q = (size_t)(stage) * UC;                                                   \
+        _Pragma("unroll") for (int u = 0; u < UC; ++u) {                                        \
+            A[st][u] = __builtin_nontemporal_load((const i32x4*)(wb + (q + u) * 1024));          \
+            _Pragma("unroll") for (int j = 0; j < NT; ++j) B[st][j][u] =                         \
+                *(const i32x4*)(xb + ((q + u) * NT + j) * 1024);                                 \
+        }                                                                                        \
+    } while (0)
+#define CAS_GEMM_MMA(st)                                                                         \
+    do {                                                                                         \
+        _Pragma("unroll") for (int u = 0; u < UC; ++u)                                          \
+            _Pragma("unroll") for (int j = 0; j < NT; ++j) acc[j] =                              \
+                mfma_step<WT>(A[st][u], B[st][j][u], acc[j]);                                    \
+    } while (0)
+
+    if (S1 > S0) {
+#pragma unroll
+        for (int s = 0; s < D; ++s) CAS_GEMM_LOAD(s, min(S0 + s, S1 - 1));
+        int c = S0;
+        for (; c + 2 * D <= S1; c += D) {
+#pragma unroll
+            for (int s = 0; s < D; ++s) {
+                CAS_GEMM_MMA(s);
+                // keep each refill behind the MMAs that free its registers
+                __builtin_amdgcn_sched_barrier(0);
+                CAS_GEMM_LOAD(s, c + s + D);
+                __builtin_amdgcn_sched_barrier(0);
+            }
+        }
+        // drain: fewer than 2D stages left, ring slot s holds stage c + s
+#pragma unroll
+        for (int s = 0; s < D; ++s) {
+            if (c + s < S1) {
+                CAS_GEMM_MMA(s);
+                if (c + s + D < S1) CAS_GEMM_LOAD(s, c + s + D);
+            }
+        }
+#pragma unroll
+        for (int s = 0; s < D; ++s)
+            if (c + D + s < S1) CAS_GEMM_MMA(s);
+    }
+#undef CAS_GEMM_MMA
+#undef CAS_GEMM_LOAD
+
+    if constexpr (WAVES > 1) {
+        using S = typename std::conditional<WT == ET_I8, int, float>::type;
+        __shared__ S red[WAVES - 1][NT][4][64];
+        if (wave > 0) {
+#pragma unroll
+            for (int j = 0; j < NT; ++j)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) red[wave - 1][j][i][lane] = acc[j][i];
+        }
+        __syncthreads();
+        if (wave != 0) return;
+        for (int w = 1; w < WAVES; ++w)
+#pragma unroll
+            for (int j = 0; j < NT; ++j)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) acc[j][i] += red[w - 1][j][i][lane];
+    }
+
+    gemm_epilogue<WT, NT, EPI, AT>(a, acc, blockIdx.x, (int)gridDim.x - 1, lane);
+}
+
+// Wide variant for tall weight matrices: the four waves of a workgroup own
+// four adjacent 16-row tiles over the whole K range, and the activation
+// fragments of each stage are loaded once per workgroup (each thread one
+// 16-byte piece of a contiguous 4 KB run) into a two-slot LDS ring that all
+// four waves read: four times less activation traffic than one tile per
+// workgroup.  One barrier per stage; register stages as in k_gemm.
+template <int WT, int NT, int UC, int D, int EPI, typename AT>
+__global__ void __launch_bounds__(256) k_gemm_wide(const GemmArgs a) {
+    using Tr = WTr<WT>;
+    using ACC = typename Tr::acc_t;
+    constexpr int E = Tr::E;
+    constexpr int NB = NT * UC;  // 1 KB activation blocks per stage
+    constexpr int LPT = NB / 4;  // 16-byte loads per thread per stage
+    static_assert(NB % 4 == 0 && D % 2 == 0, "stage shape");
+    __shared__ __attribute__((aligned(16))) char lds[2][NB * 1024];
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int tile = blockIdx.x * 4 + wave;
+    const int C = a.Kp / (16 * E);
+    const int NS = C * (FRAG_U / UC);  // stages over the whole K range
+    const char* wb = (const char*)a.W + ((size_t)tile * C * FRAG_U * 64 + lane) * 16;
+    const char* xb = (const char*)a.X + (size_t)threadIdx.x * 16;
+    ACC acc[NT];
+#pragma unroll
+    for (int j = 0; j < NT; ++j) acc[j] = ACC{0, 0, 0, 0};
+    i32x4 A[D][UC];
+    i32x4 Bv[D][LPT];
+
+#define CAS_W_LOAD(st, stage)                                                                    \
+    do {                                                                                         \
+        const size_t q = (size_t)(stage) * UC;                                                   \
+        _Pragma("unroll") for (int u = 0; u < UC; ++u) A[st][u] =                               \
+            __builtin_nontemporal_load((const i32x4*)(wb + (q + u) * 1024));                     \
+        _Pragma("unroll") for (int p = 0; p < LPT; ++p) Bv[st][p] =                             \
+            *(const i32x4*)(xb + ((size_t)(stage) * NB + 4 * p) * 1024);                         \
+    } while (0)
+#define CAS_W_STAGE(st, slot)                                                                    \
+    do {                                                                                         \
+        _Pragma("unroll") for (int p = 0; p < LPT; ++p)                                         \
+            *(i32x4*)(&lds[slot][4 * p * 1024 + threadIdx.x * 16]) = Bv[st][p];                  \
+        __syncthreads();                                                                         \
+        _Pragma("unroll") for (int u = 0; u < UC; ++u)                                          \
+            _Pragma("unroll") for (int j = 0; j < NT; ++j) {                                    \
+                const i32x4 b = *(const i32x4*)(&lds[slot][(u * NT + j) * 1024 + lane * 16]);    \
+                acc[j] = mfma_step<WT>(A[st][u], b, acc[j]);                                     \
+            }                                                                                    \
+    } while (0)
+
+#pragma unroll
+    for (int s = 0; s < D; ++s) CAS_W_LOAD(s, min(s, NS - 1));
+    int c = 0;
+    for (; c + 2 * D <= NS; c += D) {
+#pragma unroll
+        for (int s = 0; s < D; ++s) {
+            CAS_W_STAGE(s, s & 1);
+            __builtin_amdgcn_sched_barrier(0);
+            CAS_W_LOAD(s, c + s + D);
+            __builtin_amdgcn_sched_barrier(0);
+        }
+    }
+    // drain (c is a multiple of the even D, so stage c + s uses LDS slot s & 1)
+#pragma unroll
+    for (int s = 0; s < D; ++s) {
+        if (c + s < NS) {
+            CAS_W_STAGE(s, s & 1);
+            if (c + s + D < NS) CAS_W_LOAD(s, c + s + D);
+        }
+    }
+#pragma unroll
+    for (int s = 0; s < D; ++s)
+        if (c + D + s < NS) CAS_W_STAGE(s, s & 1);
+#undef CAS_W_STAGE
+#undef CAS_W_LOAD
+    gemm_epilogue<WT, NT, EPI, AT>(a, acc, tile, a.N / 16 - 1, lane);
+}
+
+// Matrices with at least 8192 rows (a multiple of 64) take the wide variant;
+// shorter ones split K across the waves of a 16-row workgroup so that the
+// grid still covers every CU.
 template <int WT, int NT, int EPI, typename AT>
 static hipError_t gemm_go(const GemmArgs& a, hipStream_t s) {
     constexpr int UC = NT == 2 ? 4 : (NT == 4 ? 2 : 1);
+    if (a.N >= 8192 && a.N % 64 == 0) {
+        hipLaunchKernelGGL((k_gemm_wide<WT, NT, UC, 4, EPI, AT>), dim3(a.N / 64), dim3(256), 0, s, a);
+        return hipGetLastError();
+    }
     constexpr int D = NT == 2 ? 2 : 4;
     hipLaunchKernelGGL((k_gemm<WT, NT, UC, D, 4, EPI, AT>), dim3(a.N / 16), dim3(256), 0, s, a);
     return hipGetLastError();
@@ -418,10 +511,22 @@ hipError_t launch_tile_act(int atype, const void* src, int Tn, int K, void* dst,
 
 // ---------------------------------------------------------------- attention
 
-// Slots covered by one split: 4 waves x 32 slots.
+// Store 4 consecutive k (k4 a multiple of 4) of one row into tiled
+// activations: they are contiguous inside one fragment.
+__device__ __forceinline__ void st4(float* out, size_t o, float a, float b, float c, float d) {
+    *(float4*)(out + o) = make_float4(a, b, c, d);
+}
+__device__ __forceinline__ void st4(uint16_t* out, size_t o, float a, float b, float c, float d) {
+    const uint32_t lo = (uint32_t)f2bf(a) | ((uint32_t)f2bf(b) << 16);
+    const uint32_t hi = (uint32_t)f2bf(c) | ((uint32_t)f2bf(d) << 16);
+    *(uint2*)(out + o) = make_uint2(lo, hi);
+}
+
+// A workgroup covers 4 waves x ATT_TPW key tiles of 32 slots.
 static constexpr int ATT_WAVES = 4;
-static constexpr int ATT_TILE = 32;
-static constexpr int ATT_SPLIT = ATT_WAVES * ATT_TILE;
+static constexpr int ATT_TPW = 2;
+static constexpr int ATT_SPLIT = ATT_WAVES * ATT_TPW * 32;
+static constexpr int ATT_MAX_SPLITS = 64;  // contexts up to 16384 slots
 
 int attention_splits(int n_slots) { return (n_slots + ATT_SPLIT - 1) / ATT_SPLIT; }
 size_t attention_work_bytes(int n_slots, int T, int H, int hd) {
@@ -436,25 +541,44 @@ __device__ __forceinline__ bool anc_bit(uint64_t a0, uint64_t a1, int node) {
 // Workgroup = (split of KV slots, kv head, chunk of 32 query rows).  The query
 // rows of a kv head are its G query heads x T tokens (each head padded to a
 // multiple of 16 rows), so GQA groups share every K/V fragment.  Scores come
-// out of the QK^T MFMA with slots along the row index; the key rows are loaded
-// in the order that puts slots 8g..8g+7 of the tile in lane group g, which is
-// exactly the k-order of the P operand of the PV MFMA, so probabilities never
-// leave registers.  V is stored slot-contiguous ([hd][slot]) so its fragments
-// are plain 16-byte loads as well.
+// out of the QK^T MFMA with slots along the row index; the cache puts slots
+// 8g..8g+7 of a tile in lane group g, which is exactly the k-order of the P
+// operand of the PV MFMA, so probabilities never leave registers.  Each wave
+// issues the K and V fragments of both its tiles before any arithmetic.  The
+// four waves merge in LDS and write the split's partial; k_attn_merge then
+// merges the splits in split order (deterministic).  (Merging inside this
+// kernel by its last-arriving workgroup needs device-scope fences that cost
+// more than the separate launch on gfx950.)
 template <int HD>
 __global__ void __launch_bounds__(256) k_attn_bf16(const AttnArgs a, float scale_log2) {
     constexpr int UD = HD / 32;   // k-steps of QK^T over head_dim
     constexpr int DG = HD / 4;    // head_dim span of one lane group
     constexpr int NDT = HD / 16;  // output d tiles
+    constexpr int TE = 32 * HD;   // elements per key tile
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int r = lane & 15, g = lane >> 4;
     const int split = blockIdx.x, kvh = blockIdx.y, rc = blockIdx.z;
     const int Lc = a.sp->Lc, n_tree = a.sp->n_tree, n_slots = Lc + n_tree;
+    const int n_tiles = (n_slots + 31) >> 5;
     const int T = a.T, Tp = (T + 15) & ~15, G = a.H / a.Hkv;
     const int nct = G * Tp / 16;
     const uint16_t* q = (const uint16_t*)a.q;
-    const uint16_t* kbase = (const uint16_t*)a.kc + (size_t)kvh * a.ctx_cap * HD;
-    const uint16_t* vbase = (const uint16_t*)a.vt + (size_t)kvh * HD * a.ctx_cap;
+    const uint16_t* kbase = (const uint16_t*)a.kc + (size_t)kvh * a.ctx_cap * HD + lane * 8;
+    const uint16_t* vbase = (const uint16_t*)a.vt + (size_t)kvh * a.ctx_cap * HD + lane * 8;
+
+    // K and V fragments of this wave's tiles first: the longest latency
+    const int tile0 = (split * ATT_WAVES + wave) * ATT_TPW;
+    i32x4 Kf[ATT_TPW][2][UD], Vf[ATT_TPW][NDT];
+#pragma unroll
+    for (int tt = 0; tt < ATT_TPW; ++tt) {
+        const size_t tb = (size_t)min(tile0 + tt, n_tiles - 1) * TE;
+#pragma unroll
+        for (int h2 = 0; h2 < 2; ++h2)
+#pragma unroll
+            for (int u = 0; u < UD; ++u) Kf[tt][h2][u] = *(const i32x4*)(kbase + tb + (h2 * UD + u) * 512);
+#pragma unroll
+        for (int dt = 0; dt < NDT; ++dt) Vf[tt][dt] = *(const i32x4*)(vbase + tb + dt * 512);
+    }
 
     bool tv[2];
     int head[2], t0[2];
@@ -484,21 +608,11 @@ __global__ void __launch_bounds__(256) k_attn_bf16(const AttnArgs a, float scale
 #pragma unroll
         for (int j = 0; j < 2; ++j) O[dt][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-    const int ws = split * ATT_SPLIT + wave * ATT_TILE;
-    if (ws < n_slots && (tv[0] || tv[1])) {
-        const int tb = ws;
-        i32x4 Kf[2][UD];
 #pragma unroll
-        for (int h2 = 0; h2 < 2; ++h2) {
-            const int slot = tb + 8 * (r >> 2) + 4 * h2 + (r & 3);
-#pragma unroll
-            for (int u = 0; u < UD; ++u) Kf[h2][u] = *(const i32x4*)(kbase + (size_t)slot * HD + g * DG + u * 8);
-        }
-        i32x4 Vf[NDT];
-#pragma unroll
-        for (int dt = 0; dt < NDT; ++dt)
-            Vf[dt] = *(const i32x4*)(vbase + (size_t)(16 * dt + r) * a.ctx_cap + tb + 8 * g);
-
+    for (int tt = 0; tt < ATT_TPW; ++tt) {
+        const int ti = tile0 + tt;
+        if (ti >= n_tiles || !(tv[0] || tv[1])) continue;
+        const int tb = ti * 32;
         f32x4 S[2][2];
 #pragma unroll
         for (int h2 = 0; h2 < 2; ++h2)
@@ -506,7 +620,7 @@ __global__ void __launch_bounds__(256) k_attn_bf16(const AttnArgs a, float scale
             for (int j = 0; j < 2; ++j) {
                 S[h2][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-                for (int u = 0; u < UD; ++u) S[h2][j] = mfma_step<ET_BF16>(Kf[h2][u], Qf[j][u], S[h2][j]);
+                for (int u = 0; u < UD; ++u) S[h2][j] = mfma_step<ET_BF16>(Kf[tt][h2][u], Qf[j][u], S[h2][j]);
             }
         i32x4 Pf[2];
 #pragma unroll
@@ -547,10 +661,10 @@ __global__ void __launch_bounds__(256) k_attn_bf16(const AttnArgs a, float scale
 #pragma unroll
         for (int dt = 0; dt < NDT; ++dt)
 #pragma unroll
-            for (int j = 0; j < 2; ++j) O[dt][j] = mfma_step<ET_BF16>(Vf[dt], Pf[j], O[dt][j]);
+            for (int j = 0; j < 2; ++j) O[dt][j] = mfma_step<ET_BF16>(Vf[tt][dt], Pf[j], O[dt][j]);
     }
 
-    // ---- combine the four waves in LDS (wave order), then write the split's partial
+    // ---- merge the four waves in LDS (wave order)
     __shared__ float sm_m[ATT_WAVES][2][16], sm_l[ATT_WAVES][2][16];
     __shared__ float sm_o[2][HD][16];
     if (g == 0) {
@@ -561,11 +675,11 @@ __global__ void __launch_bounds__(256) k_attn_bf16(const AttnArgs a, float scale
         }
     }
     __syncthreads();
-    float M[2], f[2];
+    float f[2];
 #pragma unroll
     for (int j = 0; j < 2; ++j) {
-        M[j] = fmaxf(fmaxf(sm_m[0][j][r], sm_m[1][j][r]), fmaxf(sm_m[2][j][r], sm_m[3][j][r]));
-        f[j] = exp2f(m[j] - M[j]);
+        const float M = fmaxf(fmaxf(sm_m[0][j][r], sm_m[1][j][r]), fmaxf(sm_m[2][j][r], sm_m[3][j][r]));
+        f[j] = exp2f(m[j] - M);
     }
     for (int w = 0; w < ATT_WAVES; ++w) {
         if (wave == w) {
@@ -582,11 +696,11 @@ __global__ void __launch_bounds__(256) k_attn_bf16(const AttnArgs a, float scale
         }
         __syncthreads();
     }
-    for (int idx = threadIdx.x; idx < 2 * HD * 16; idx += 256) {
-        const int j = idx / (HD * 16), rem = idx % (HD * 16), d = rem / 16, rr = rem % 16;
-        if (!tv[j]) continue;
+    // ---- this split's partial for every valid (row, d), d fastest (coalesced)
+    for (int idx = threadIdx.x; idx < 2 * 16 * HD; idx += 256) {
+        const int row = idx / HD, d = idx % HD, j = row >> 4, rr = row & 15;
         const int t = t0[j] + rr;
-        if (t >= T) continue;
+        if (!tv[j] || t >= T) continue;
         const size_t o = ((size_t)split * a.H + head[j]) * T + t;
         a.part_o[o * HD + d] = sm_o[j][d][rr];
         if (d == 0) {
@@ -599,24 +713,61 @@ __global__ void __launch_bounds__(256) k_attn_bf16(const AttnArgs a, float scale
     }
 }
 
-// Merge the split partials of every (token, head): softmax-weighted in the
-// log2 domain, splits in increasing order.
-template <typename AT>
-__global__ void k_attn_combine(const AttnArgs a, int S) {
-    const int t = blockIdx.x, h = blockIdx.y, d = threadIdx.x;
-    const int hd = a.hd, T = a.T, H = a.H;
-    float M = -1e30f;
-    for (int s = 0; s < S; ++s) M = fmaxf(M, a.part_ml[(((size_t)s * H + h) * T + t) * 2]);
-    float L = 0.f, o = 0.f;
-    for (int s = 0; s < S; ++s) {
-        const size_t b = ((size_t)s * H + h) * T + t;
-        const float w = exp2f(a.part_ml[b * 2] - M);
-        L += a.part_ml[b * 2 + 1] * w;
-        o += a.part_o[b * hd + d] * w;
+// Merge the KV splits of 16 query rows of one head: the split weights
+// exp2(m_s - M) / L of every row are formed once (all (row, split) pairs
+// loaded in parallel), then float4 runs of the partial outputs are summed in
+// split order.
+template <int HD>
+__global__ void __launch_bounds__(256) k_attn_merge(const AttnArgs a, int S) {
+    __shared__ float sm[16][ATT_MAX_SPLITS], sl[16][ATT_MAX_SPLITS], sw[16][ATT_MAX_SPLITS];
+    const int h = blockIdx.y, t0 = blockIdx.x * 16, T = a.T;
+    for (int i = threadIdx.x; i < 16 * S; i += 256) {
+        const int rr = i / S, sp = i % S, t = min(t0 + rr, T - 1);
+        const float* ml = a.part_ml + (((size_t)sp * a.H + h) * T + t) * 2;
+        sm[rr][sp] = ml[0];
+        sl[rr][sp] = ml[1];
     }
-    const size_t oi = a.out_tiled ? xt_off(t, h * hd + d, col_tiles(T), 16 / (int)sizeof(AT))
-                                  : (size_t)t * H * hd + (size_t)h * hd + d;
-    Act<AT>::st((AT*)a.out, oi, L > 0.f ? o / L : 0.f);
+    __syncthreads();
+    if (threadIdx.x < 16) {
+        const int rr = threadIdx.x;
+        float M = -1e30f;
+        for (int sp = 0; sp < S; ++sp) M = fmaxf(M, sm[rr][sp]);
+        float L = 0.f;
+        for (int sp = 0; sp < S; ++sp) {
+            const float w = exp2f(sm[rr][sp] - M);
+            sw[rr][sp] = w;
+            L += sl[rr][sp] * w;
+        }
+        const float inv = L > 0.f ? 1.f / L : 0.f;
+        for (int sp = 0; sp < S; ++sp) sw[rr][sp] *= inv;
+    }
+    __syncthreads();
+    const int NTo = col_tiles(T);
+    const size_t sstride = (size_t)a.H * T * HD;
+    for (int idx = threadIdx.x; idx < 16 * (HD / 4); idx += 256) {
+        const int rr = idx / (HD / 4), d4 = (idx % (HD / 4)) * 4, t = t0 + rr;
+        if (t >= T) continue;
+        const float* po = a.part_o + ((size_t)h * T + t) * HD + d4;
+        float4 acc4 = make_float4(0.f, 0.f, 0.f, 0.f);
+        for (int sp = 0; sp < S; ++sp) {
+            const float4 v = *(const float4*)(po + sp * sstride);
+            const float w = sw[rr][sp];
+            acc4.x += v.x * w;
+            acc4.y += v.y * w;
+            acc4.z += v.z * w;
+            acc4.w += v.w * w;
+        }
+        const int k = h * HD + d4;
+        if (a.out_tiled) {
+            st4((uint16_t*)a.out, xt_off(t, k, NTo, 8), acc4.x, acc4.y, acc4.z, acc4.w);
+        } else {
+            uint16_t* o = (uint16_t*)a.out + (size_t)t * a.H * HD + k;
+            o[0] = f2bf(acc4.x);
+            o[1] = f2bf(acc4.y);
+            o[2] = f2bf(acc4.z);
+            o[3] = f2bf(acc4.w);
+        }
+    }
 }
 
 // fp32 storage: plain attention, one workgroup per (token, head); scores of
@@ -672,20 +823,52 @@ hipError_t launch_attention(int atype, const AttnArgs& a, hipStream_t s) {
     const int S = attention_splits(n_slots);
     const int G = a.H / a.Hkv, Tp = (a.T + 15) & ~15;
     const int nct = G * Tp / 16, nrc = (nct + 1) / 2;
+    if (a.ctx_cap % 32 || S > ATT_MAX_SPLITS) return hipErrorInvalidValue;
     const float scale_log2 = (1.0f / sqrtf((float)a.hd)) * 1.4426950408889634f;
-    if (a.hd == 128)
+    const dim3 mg((a.T + 15) / 16, a.H);
+    if (a.hd == 128) {
         hipLaunchKernelGGL(k_attn_bf16<128>, dim3(S, a.Hkv, nrc), dim3(256), 0, s, a, scale_log2);
-    else if (a.hd == 64)
+        hipLaunchKernelGGL(k_attn_merge<128>, mg, dim3(256), 0, s, a, S);
+    } else if (a.hd == 64) {
         hipLaunchKernelGGL(k_attn_bf16<64>, dim3(S, a.Hkv, nrc), dim3(256), 0, s, a, scale_log2);
-    else
+        hipLaunchKernelGGL(k_attn_merge<64>, mg, dim3(256), 0, s, a, S);
+    } else {
         return hipErrorInvalidValue;
+    }
     return hipGetLastError();
 }
 
-hipError_t launch_attention_combine(int atype, const AttnArgs& a, hipStream_t s) {
-    if (atype == ET_F32) return hipSuccess;  // the fp32 path writes its output directly
-    const int S = attention_splits(a.Lc_host + a.n_tree_host);
-    hipLaunchKernelGGL(k_attn_combine<uint16_t>, dim3(a.T, a.H), dim3(a.hd), 0, s, a, S);
+// Row-major [Hkv][n][hd] <-> cache layout, one thread per (head, slot, d).
+template <typename AT>
+__global__ void k_kv_convert(AT* kc, AT* vt, const AT* kr, const AT* vr, int Hkv, int n, int hd, int ctx_cap,
+                             int to_cache) {
+    constexpr int ET = sizeof(AT) == 2 ? ET_BF16 : ET_F32;
+    const size_t total = (size_t)Hkv * n * hd;
+    for (size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x; i < total; i += (size_t)gridDim.x * blockDim.x) {
+        const int d = (int)(i % hd), slot = (int)((i / hd) % n), h = (int)(i / ((size_t)hd * n));
+        const size_t base = (size_t)h * ctx_cap * hd;
+        const size_t ko = base + kv_k_off(ET, slot, d, hd, ctx_cap), vo = base + kv_v_off(ET, slot, d, hd, ctx_cap);
+        if (to_cache) {
+            kc[ko] = kr[i];
+            vt[vo] = vr[i];
+        } else {
+            ((AT*)kr)[i] = kc[ko];
+            ((AT*)vr)[i] = vt[vo];
+        }
+    }
+}
+
+hipError_t launch_kv_convert(int atype, void* kc, void* vt, const void* k_rows, const void* v_rows, int Hkv, int n,
+                             int hd, int ctx_cap, int to_cache, hipStream_t s) {
+    size_t total = (size_t)Hkv * n * hd, b = (total + 255) / 256;
+    if (b > 16384) b = 16384;
+    if (b == 0) return hipSuccess;
+    if (atype == ET_BF16)
+        hipLaunchKernelGGL(k_kv_convert<uint16_t>, dim3((unsigned)b), dim3(256), 0, s, (uint16_t*)kc, (uint16_t*)vt,
+                           (const uint16_t*)k_rows, (const uint16_t*)v_rows, Hkv, n, hd, ctx_cap, to_cache);
+    else
+        hipLaunchKernelGGL(k_kv_convert<float>, dim3((unsigned)b), dim3(256), 0, s, (float*)kc, (float*)vt,
+                           (const float*)k_rows, (const float*)v_rows, Hkv, n, hd, ctx_cap, to_cache);
     return hipGetLastError();
 }
 
@@ -693,16 +876,6 @@ hipError_t launch_attention_combine(int atype, const AttnArgs& a, hipStream_t s)
 
 static constexpr int NORM_MAXV = 8;  // float4 per thread: rows up to 8192 elements
 
-// Store 4 consecutive k (k4 a multiple of 4) of one row into tiled
-// activations: they are contiguous inside one fragment.
-__device__ __forceinline__ void st4(float* out, size_t o, float a, float b, float c, float d) {
-    *(float4*)(out + o) = make_float4(a, b, c, d);
-}
-__device__ __forceinline__ void st4(uint16_t* out, size_t o, float a, float b, float c, float d) {
-    const uint32_t lo = (uint32_t)f2bf(a) | ((uint32_t)f2bf(b) << 16);
-    const uint32_t hi = (uint32_t)f2bf(c) | ((uint32_t)f2bf(d) << 16);
-    *(uint2*)(out + o) = make_uint2(lo, hi);
-}
 __device__ __forceinline__ void st4q(int8_t* q, size_t o, float a, float b, float c, float d) {
     const uint32_t v = (uint32_t)(uint8_t)(int8_t)a | ((uint32_t)(uint8_t)(int8_t)b << 8) |
                        ((uint32_t)(uint8_t)(int8_t)c << 16) | ((uint32_t)(uint8_t)(int8_t)d << 24);
@@ -1001,26 +1174,26 @@ hipError_t launch_accept(const float* logits, int T, int V, const int* rtok, con
 
 // ---------------------------------------------------------------- KV compaction
 
-// One workgroup per (layer, kv head): stage the accepted rows (K) and
-// columns (V) in LDS, then write them to slots Lc .. Lc+n_acc-1.  Staging all
-// reads before any write makes the move safe when a destination is a later
-// node's source.
+// One workgroup per (layer, kv head): stage the accepted slots' K and V in
+// LDS, then write them to slots Lc .. Lc+n_acc-1.  Staging all reads before
+// any write makes the move safe when a destination is a later node's source.
 template <typename AT>
 __global__ void __launch_bounds__(256) k_compact(AT* kc, AT* vt, int hd, int ctx_cap, const StepParams* sp,
                                                  const int* acc, int n_acc) {
+    constexpr int ET = sizeof(AT) == 2 ? ET_BF16 : ET_F32;
     extern __shared__ unsigned char smem[];
     AT* buf = (AT*)smem;
     const int Lc = sp->Lc;
     AT* kb = kc + (size_t)blockIdx.x * ctx_cap * hd;
-    AT* vb = vt + (size_t)blockIdx.x * hd * ctx_cap;
+    AT* vb = vt + (size_t)blockIdx.x * ctx_cap * hd;
     const int n = n_acc * hd;
-    for (int i = threadIdx.x; i < n; i += 256) buf[i] = kb[(size_t)(Lc + acc[i / hd]) * hd + i % hd];
+    for (int i = threadIdx.x; i < n; i += 256) buf[i] = kb[kv_k_off(ET, Lc + acc[i / hd], i % hd, hd, ctx_cap)];
     __syncthreads();
-    for (int i = threadIdx.x; i < n; i += 256) kb[(size_t)(Lc + i / hd) * hd + i % hd] = buf[i];
+    for (int i = threadIdx.x; i < n; i += 256) kb[kv_k_off(ET, Lc + i / hd, i % hd, hd, ctx_cap)] = buf[i];
     __syncthreads();
-    for (int i = threadIdx.x; i < n; i += 256) buf[i] = vb[(size_t)(i / n_acc) * ctx_cap + Lc + acc[i % n_acc]];
+    for (int i = threadIdx.x; i < n; i += 256) buf[i] = vb[kv_v_off(ET, Lc + acc[i / hd], i % hd, hd, ctx_cap)];
     __syncthreads();
-    for (int i = threadIdx.x; i < n; i += 256) vb[(size_t)(i / n_acc) * ctx_cap + Lc + i % n_acc] = buf[i];
+    for (int i = threadIdx.x; i < n; i += 256) vb[kv_v_off(ET, Lc + i / hd, i % hd, hd, ctx_cap)] = buf[i];
 }
 
 hipError_t launch_compact(int atype, void* kc, void* vt, int L, int Hkv, int hd, int ctx_cap, const StepParams* sp,

@@ -307,7 +307,6 @@ hipError_t enqueue_forward(cas_ctx* c, int T, const uint8_t* skip, int aq) {
         at.kc = kc;
         at.vt = vt;
         RUN(CAS_K_ATTN, launch_attention(et, at, s));
-        if (et == ET_BF16) RUN(CAS_K_ATTN_COMBINE, launch_attention_combine(et, at, s));
         if (aq) RUN(CAS_K_QUANT, launch_quant_rows(et, c->d_ao, T, H * hd, c->d_xq, c->d_xs, 1, s));
         GemmArgs go{};
         go.T = T;
@@ -577,6 +576,7 @@ cas_status cas_create(const cas_config* cfg, int device, void* stream, cas_ctx**
     if (f.max_tree < 1 || f.max_tree > 128) return bad(CAS_ERR_UNSUPPORTED, "max_tree must be in [1, 128]");
     if (f.max_ctx < f.max_tree) return bad(CAS_ERR_ARG, "max_ctx must be >= max_tree");
     if (f.dtype == CAS_F32 && f.max_ctx > 4096 - 128) return bad(CAS_ERR_UNSUPPORTED, "fp32 models need max_ctx <= 3968");
+    if (f.max_ctx > 16384 - 128) return bad(CAS_ERR_UNSUPPORTED, "max_ctx must be <= 16256");
     if (!(f.rms_eps > 0.f) || !(f.rope_theta > 1.f)) return bad(CAS_ERR_ARG, "rms_eps / rope_theta");
 
     hipError_t e = hipSetDevice(device);
@@ -800,52 +800,46 @@ cas_status cas_prefill(cas_ctx* c, const int32_t* tokens, int32_t n) {
     return CAS_OK;
 }
 
-cas_status cas_kv_load(cas_ctx* c, int32_t layer, const void* k, const void* v, int32_t n) {
-    if (!c) return CAS_ERR_ARG;
+// Row-major [Hkv][n][hd] host data <-> one layer's cache, through a device staging buffer.
+static cas_status kv_transfer(cas_ctx* c, int32_t layer, void* k, void* v, int32_t n, bool to_cache) {
     const cas_config& f = c->cfg;
     if (!k || !v) return fail(c, CAS_ERR_ARG, "k and v must not be NULL");
     if (layer < 0 || layer >= f.n_layers) return fail(c, CAS_ERR_ARG, "layer out of range");
     if (n < 0 || n > f.max_ctx) return fail(c, CAS_ERR_CAPACITY, "n exceeds max_ctx");
     if (n == 0) return CAS_OK;
-    const size_t es = c->es, hd = f.head_dim;
-    const size_t kv_layer = (size_t)f.n_kv_heads * c->ctx_cap * hd * es;
+    const size_t bytes = (size_t)f.n_kv_heads * n * f.head_dim * c->es;
+    const size_t kv_layer = (size_t)f.n_kv_heads * c->ctx_cap * f.head_dim * c->es;
+    void* tmp = nullptr;
     HIPCHK(c, hipStreamSynchronize(c->stream));
-    std::vector<unsigned char> tr((size_t)hd * n * es);
-    for (int h = 0; h < f.n_kv_heads; ++h) {
-        char* kd = (char*)c->kc + kv_layer * layer + (size_t)h * c->ctx_cap * hd * es;
-        HIPCHK(c, hipMemcpy(kd, (const char*)k + (size_t)h * n * hd * es, (size_t)n * hd * es, hipMemcpyHostToDevice));
-        const unsigned char* vs = (const unsigned char*)v + (size_t)h * n * hd * es;
-        for (int s = 0; s < n; ++s)
-            for (size_t e = 0; e < hd; ++e) memcpy(&tr[(e * n + s) * es], vs + ((size_t)s * hd + e) * es, es);
-        char* vd = (char*)c->vt + kv_layer * layer + (size_t)h * hd * c->ctx_cap * es;
-        HIPCHK(c, hipMemcpy2D(vd, (size_t)c->ctx_cap * es, tr.data(), (size_t)n * es, (size_t)n * es, hd,
-                              hipMemcpyHostToDevice));
+    HIPCHK(c, hipMalloc(&tmp, 2 * bytes));
+    char* tk = (char*)tmp;
+    char* tv = tk + bytes;
+    hipError_t e = hipSuccess;
+    if (to_cache) {
+        e = hipMemcpy(tk, k, bytes, hipMemcpyHostToDevice);
+        if (e == hipSuccess) e = hipMemcpy(tv, v, bytes, hipMemcpyHostToDevice);
     }
+    if (e == hipSuccess)
+        e = launch_kv_convert(c->et, (char*)c->kc + kv_layer * layer, (char*)c->vt + kv_layer * layer, tk, tv,
+                              f.n_kv_heads, n, f.head_dim, c->ctx_cap, to_cache ? 1 : 0, c->stream);
+    if (e == hipSuccess) e = hipStreamSynchronize(c->stream);
+    if (e == hipSuccess && !to_cache) {
+        e = hipMemcpy(k, tk, bytes, hipMemcpyDeviceToHost);
+        if (e == hipSuccess) e = hipMemcpy(v, tv, bytes, hipMemcpyDeviceToHost);
+    }
+    (void)hipFree(tmp);
+    if (e != hipSuccess) return hip_fail(c, e, "kv transfer");
     return CAS_OK;
+}
+
+cas_status cas_kv_load(cas_ctx* c, int32_t layer, const void* k, const void* v, int32_t n) {
+    if (!c) return CAS_ERR_ARG;
+    return kv_transfer(c, layer, (void*)k, (void*)v, n, true);
 }
 
 cas_status cas_kv_read(cas_ctx* c, int32_t layer, void* k, void* v, int32_t n) {
     if (!c) return CAS_ERR_ARG;
-    const cas_config& f = c->cfg;
-    if (!k || !v) return fail(c, CAS_ERR_ARG, "k and v must not be NULL");
-    if (layer < 0 || layer >= f.n_layers) return fail(c, CAS_ERR_ARG, "layer out of range");
-    if (n < 0 || n > c->ctx_cap) return fail(c, CAS_ERR_CAPACITY, "n exceeds the cache");
-    if (n == 0) return CAS_OK;
-    const size_t es = c->es, hd = f.head_dim;
-    const size_t kv_layer = (size_t)f.n_kv_heads * c->ctx_cap * hd * es;
-    HIPCHK(c, hipStreamSynchronize(c->stream));
-    std::vector<unsigned char> tr((size_t)hd * n * es);
-    for (int h = 0; h < f.n_kv_heads; ++h) {
-        const char* ks = (const char*)c->kc + kv_layer * layer + (size_t)h * c->ctx_cap * hd * es;
-        HIPCHK(c, hipMemcpy((char*)k + (size_t)h * n * hd * es, ks, (size_t)n * hd * es, hipMemcpyDeviceToHost));
-        const char* vs = (const char*)c->vt + kv_layer * layer + (size_t)h * hd * c->ctx_cap * es;
-        HIPCHK(c, hipMemcpy2D(tr.data(), (size_t)n * es, vs, (size_t)c->ctx_cap * es, (size_t)n * es, hd,
-                              hipMemcpyDeviceToHost));
-        unsigned char* vd = (unsigned char*)v + (size_t)h * n * hd * es;
-        for (int s = 0; s < n; ++s)
-            for (size_t e = 0; e < hd; ++e) memcpy(vd + ((size_t)s * hd + e) * es, &tr[(e * n + s) * es], es);
-    }
-    return CAS_OK;
+    return kv_transfer(c, layer, k, v, n, false);
 }
 
 cas_status cas_set_committed(cas_ctx* c, int32_t n) {
@@ -1007,27 +1001,34 @@ cas_status cas_op_quant_weight(int32_t wtype, const void* W, int32_t N, int32_t 
     return e == hipSuccess ? CAS_OK : CAS_ERR_DEVICE;
 }
 
-size_t cas_op_attention_work_bytes(int32_t Lc, int32_t n_tree, int32_t T, int32_t H, int32_t hd) {
-    return attention_work_bytes(Lc + n_tree, T, H, hd) + 64;
+size_t cas_op_attention_work_bytes(int32_t Lc, int32_t n_tree, int32_t T, int32_t H, int32_t hd, int32_t Hkv,
+                                   int32_t ctx_cap) {
+    return 256 + 2 * align256((size_t)Hkv * ctx_cap * hd * 2) +
+           attention_work_bytes(Lc + n_tree, T, H, hd);
 }
 
-cas_status cas_op_attention(const void* q, const void* kc, const void* vt, int32_t ctx_cap, int32_t Lc, int32_t n_tree,
+cas_status cas_op_attention(const void* q, const void* k, const void* v, int32_t ctx_cap, int32_t Lc, int32_t n_tree,
                             int32_t T, int32_t H, int32_t Hkv, int32_t hd, const uint64_t* anc, void* out, void* work,
                             size_t work_bytes, void* stream) {
-    if (!q || !kc || !vt || !anc || !out || !work) return CAS_ERR_ARG;
+    if (!q || !k || !v || !anc || !out || !work) return CAS_ERR_ARG;
     if (hd != 64 && hd != 128) return CAS_ERR_UNSUPPORTED;
     if (T < 1 || T > 128 || n_tree < 1 || n_tree > 128 || Lc < 0 || Hkv < 1 || H < 1 || H % Hkv) return CAS_ERR_ARG;
     if (ctx_cap % 32 || Lc + n_tree > ctx_cap) return CAS_ERR_ARG;
-    if (work_bytes < cas_op_attention_work_bytes(Lc, n_tree, T, H, hd)) return CAS_ERR_ARG;
+    if (work_bytes < cas_op_attention_work_bytes(Lc, n_tree, T, H, hd, Hkv, ctx_cap)) return CAS_ERR_ARG;
     hipStream_t s = (hipStream_t)stream;
-    // the step parameters live at the start of the work buffer
+    // work: step parameters | K cache | V cache | split partials
     StepParams sp{Lc, 0, n_tree, 0};
-    StepParams* dsp = (StepParams*)work;
+    char* w = (char*)work;
+    StepParams* dsp = (StepParams*)w;
+    char* kcache = w + 256;
+    char* vcache = kcache + align256((size_t)Hkv * ctx_cap * hd * 2);
+    float* part = (float*)(vcache + align256((size_t)Hkv * ctx_cap * hd * 2));
     if (hipMemcpyAsync(dsp, &sp, sizeof sp, hipMemcpyHostToDevice, s) != hipSuccess) return CAS_ERR_DEVICE;
+    hipError_t e = launch_kv_convert(ET_BF16, kcache, vcache, k, v, Hkv, ctx_cap, hd, ctx_cap, 1, s);
     AttnArgs a{};
     a.q = q;
-    a.kc = kc;
-    a.vt = vt;
+    a.kc = kcache;
+    a.vt = vcache;
     a.anc = anc;
     a.sp = dsp;
     a.Lc_host = Lc;
@@ -1035,15 +1036,14 @@ cas_status cas_op_attention(const void* q, const void* kc, const void* vt, int32
     a.out = out;
     a.out_tiled = 0;
     const int S = attention_splits(Lc + n_tree);
-    a.part_o = (float*)((char*)work + 64);
+    a.part_o = part;
     a.part_ml = a.part_o + (size_t)S * H * T * hd;
     a.T = T;
     a.H = H;
     a.Hkv = Hkv;
     a.hd = hd;
     a.ctx_cap = ctx_cap;
-    hipError_t e = launch_attention(ET_BF16, a, s);
-    if (e == hipSuccess) e = launch_attention_combine(ET_BF16, a, s);
+    if (e == hipSuccess) e = launch_attention(ET_BF16, a, s);
     if (e == hipSuccess) e = hipStreamSynchronize(s);  // sp lives on the caller's stack
     return e == hipSuccess ? CAS_OK : CAS_ERR_DEVICE;
 }

@@ -34,8 +34,10 @@ def _gemm_bound(x64, w64):
     return K * 2.0 ** -23 * (np.abs(x64) @ np.abs(w64).T) + 1e-30
 
 
+# N >= 8192 with N % 64 == 0 takes the four-tile workgroup variant; 8208 does not
 @pytest.mark.parametrize("N,K,T", [(64, 4096, 32), (48, 688, 5), (32, 256, 1), (16, 1376, 17), (64, 512, 128),
-                                   (80, 11008, 64), (32, 128, 100)])
+                                   (80, 11008, 64), (32, 128, 100), (8192, 512, 32), (8256, 256, 5),
+                                   (8192, 384, 128), (8208, 256, 9), (8320, 128, 1)])
 def test_gemm_bf16(N, K, T):
     w = synth.f32_to_bf16_bits(synth.gen_activations(N, K, seed=N + K, edge_rows=False) * 0.02)
     x = synth.f32_to_bf16_bits(synth.gen_activations(T, K, seed=T + 7))
@@ -49,7 +51,8 @@ def test_gemm_bf16(N, K, T):
     assert (np.abs(got - ref) <= _gemm_bound(x64, w64)).all()
 
 
-@pytest.mark.parametrize("N,K,T", [(32, 256, 15), (16, 688, 3), (2048, 256, 7), (64, 4096, 33)])
+@pytest.mark.parametrize("N,K,T", [(32, 256, 15), (16, 688, 3), (2048, 256, 7), (64, 4096, 33), (8192, 256, 20),
+                                   (8256, 128, 1)])
 def test_gemm_f32_and_residual(N, K, T):
     w = synth.gen_activations(N, K, seed=11, edge_rows=False) * np.float32(0.02)
     x = synth.gen_activations(T, K, seed=12)
@@ -62,7 +65,8 @@ def test_gemm_f32_and_residual(N, K, T):
     assert (np.abs(out.cpu().numpy() - ref) <= bound).all()
 
 
-@pytest.mark.parametrize("N,K,T", [(64, 4096, 32), (48, 688, 5), (16, 13824, 3), (32, 256, 100), (16, 5120, 64)])
+@pytest.mark.parametrize("N,K,T", [(64, 4096, 32), (48, 688, 5), (16, 13824, 3), (32, 256, 100), (16, 5120, 64),
+                                   (8192, 512, 32), (8256, 256, 1), (8192, 256, 65)])
 def test_gemm_int8_bit_exact(N, K, T):
     rng = np.random.default_rng(N * 7 + K + T)
     qw = rng.integers(-127, 128, (N, K)).astype(np.int8)
@@ -124,13 +128,11 @@ def _attention_case(H, Hkv, hd, Lc, parents, seed):
     q = synth.f32_to_bf16_bits(rng.standard_normal((T, H, hd)).astype(np.float32) * np.float32(1.28))
     kc = synth.f32_to_bf16_bits(rng.standard_normal((Hkv, ctx_cap, hd)).astype(np.float32) * np.float32(1.28))
     vv = synth.f32_to_bf16_bits(rng.standard_normal((Hkv, ctx_cap, hd)).astype(np.float32))
-    vt = np.ascontiguousarray(np.transpose(vv, (0, 2, 1)))
     _, anc = O.tree_metadata(parents)
     anc_np = np.array([[a & (2 ** 64 - 1), a >> 64] for a in anc], dtype=np.uint64)
     out = torch.zeros((T, H * hd), dtype=torch.int16, device=DEV)
-    work = torch.zeros(cas.op_attention_work_bytes(Lc, T, T, H, hd) // 4 + 16, dtype=torch.float32, device=DEV)
-    cas.op_attention(_bf16_dev(q), _bf16_dev(kc), _bf16_dev(vt), ctx_cap, Lc, T, T, H, Hkv, hd,
-                     torch.from_numpy(anc_np.view(np.int64)).to(DEV), out, work)
+    cas.op_attention(_bf16_dev(q), _bf16_dev(kc), _bf16_dev(vv), ctx_cap, Lc, T, T, H, Hkv, hd,
+                     torch.from_numpy(anc_np.view(np.int64)).to(DEV), out)
     torch.cuda.synchronize()
     got = synth.bf16_bits_to_f32(out.cpu().numpy().view(np.uint16)).reshape(T, H, hd)
     qf = synth.bf16_bits_to_f32(q)
