@@ -15,6 +15,7 @@ stream (cas_profile); the dominant kernel's achieved HBM rate is its
 algorithmic bytes per launch over its mean duration.
 """
 import argparse
+import hashlib
 import json
 import os
 import sys
@@ -26,6 +27,27 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBPS = 8000.0  # MI355X HBM3E
+KERNELS_SRC = os.path.join(ROOT, "paper_2510_26843_amd", "csrc", "kernels.hip")
+TRAFFIC_RECORD = os.path.join(ROOT, "profiles", "gemm_gateup_7b_t32_traffic.json")
+
+
+def kernels_sha256():
+    with open(KERNELS_SRC, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()
+
+
+def measured_traffic():
+    """HBM bytes per gate/up launch from the stored rocprofv3 counter record,
+    or None when the record is missing or the kernel source has changed since
+    the counters were taken."""
+    try:
+        with open(TRAFFIC_RECORD) as f:
+            rec = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if rec.get("kernels_sha256") != kernels_sha256():
+        return None
+    return rec.get("hbm_bytes_per_launch")
 
 
 def algorithmic_bytes(shape, T, Lc, run_layers, es=2):
@@ -45,36 +67,30 @@ def gemm_bytes(N, K, T, out_bytes):
     return N * K * 2 + T * K * 2 + out_bytes
 
 
-def cpu_baseline(shape, weights, parents, toks, Lc):
-    """The oracle's verify forward on the host cores, on a bounded sample:
-    two of the 32 layers (over a synthetic 1024-slot KV cache) plus the LM
-    head, and the head alone; scaled to the full 32-layer forward."""
+def cpu_baseline(shape, weights, parents, toks, Lc, min_s=10.0, max_reps=3):
+    """The oracle's verify forward on the host cores: whole 32-layer forwards
+    of the same tree over a synthetic 1024-slot committed KV cache, repeated
+    until at least min_s seconds of work (at most max_reps forwards)."""
     from oracle import oracle as O
     from paper_2510_26843_amd import synth
     O.set_threads(min(16, os.cpu_count() or 1))
-    keep = [0, 1]
-    w = dict(weights)
-    w["layers"] = [weights["layers"][l] if l in keep else None for l in range(shape.n_layers)]
-    om = O.OracleModel(shape, w, max_ctx=Lc + len(parents))
-    k, v = synth.gen_kv(len(keep), shape.n_kv_heads, Lc, shape.head_dim, seed=4)
-    for i, l in enumerate(keep):
-        om.set_kv(l, synth.bf16_bits_to_f32(synth.f32_to_bf16_bits(k[i])),
-                  synth.bf16_bits_to_f32(synth.f32_to_bf16_bits(v[i])))
+    om = O.OracleModel(shape, weights, max_ctx=Lc + len(parents))
+    k, v = synth.gen_kv(shape.n_layers, shape.n_kv_heads, Lc, shape.head_dim, seed=4)
+    for l in range(shape.n_layers):
+        om.set_kv(l, synth.bf16_bits_to_f32(synth.f32_to_bf16_bits(k[l])),
+                  synth.bf16_bits_to_f32(synth.f32_to_bf16_bits(v[l])))
+    del k, v
     om.set_committed(Lc)
-    skip2 = [0 if l in keep else 1 for l in range(shape.n_layers)]
-    t0 = time.perf_counter()
-    om.forward(toks, parents, 0, skip=skip2)
-    t_two = time.perf_counter() - t0
-    t0 = time.perf_counter()
-    om.forward(toks, parents, 0, skip=[1] * shape.n_layers)
-    t_head = time.perf_counter() - t0
-    per_layer = max(t_two - t_head, 1e-9) / len(keep)
-    t_full = shape.n_layers * per_layer + t_head
-    return {"value": round(len(parents) / t_full, 3), "unit": "tree tokens/s", "cores": O.threads(),
+    reps, t = 0, 0.0
+    while reps < max_reps and (reps == 0 or t < min_s):
+        t0 = time.perf_counter()
+        om.forward(toks, parents, 0)
+        t += time.perf_counter() - t0
+        reps += 1
+    return {"value": round(len(parents) * reps / t, 3), "unit": "tree tokens/s", "cores": O.threads(),
             "kind": "oracle",
-            "sample": (f"fp64 oracle verify forward, T={len(parents)}, ctx {Lc}: layers 0-1 over a synthetic "
-                       f"KV cache ({t_two:.1f} s) and the LM head alone ({t_head:.1f} s), scaled to "
-                       f"{shape.n_layers} layers ({t_full:.1f} s per forward)")}
+            "sample": (f"{reps} fp64 oracle verify forward(s) of the full {shape.n_layers}-layer model, "
+                       f"T={len(parents)} tree (4,2,2,1,1), over a synthetic {Lc}-slot KV cache: {t:.1f} s")}
 
 
 def main():
@@ -84,6 +100,10 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--layers", type=int, default=0, help="(testing only) fewer layers; invalidates the metric")
+    ap.add_argument("--counter-pass", action="store_true",
+                    help="profiling pass for hardware counters: verify steps only, direct launches (no graphs), "
+                         "then a copy of --copy-mib MiB; prints no metric")
+    ap.add_argument("--copy-mib", type=int, default=1024)
     args = ap.parse_args()
     if args.gpus != 1:
         print(json.dumps({"error": "this build runs on one GPU; --gpus above 1 is not supported",
@@ -118,6 +138,26 @@ def main():
     parents = synth.tree_from_branching(*synth.TREE_7B)
     toks = synth.gen_tree_tokens(parents, shape.vocab, seed=2)
     odd = [l % 2 for l in range(shape.n_layers)]
+
+    if args.counter_pass:
+        m.set_graphs(False)
+        for _ in range(args.warmup + args.steps):
+            m.forward(toks, parents, 0, logits=False)
+            acc, _ = m.accept()
+            m.compact(acc)
+            m.set_committed(Lc)
+        m.sync()
+        m.close()
+        del m
+        nbytes = args.copy_mib << 20
+        src = torch.empty(nbytes // 4, dtype=torch.int32, device="cuda:0").random_()
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            cas.op_copy(dst, src, nbytes)
+        torch.cuda.synchronize()
+        assert torch.equal(src, dst)
+        log(f"[bench] counter pass: {args.warmup + args.steps} verify steps, 3 copies of {nbytes} bytes")
+        return
 
     def step():
         m.forward(toks[:1], [-1], 0, skip=odd, logits=False)
@@ -213,7 +253,7 @@ def main():
         "verify_kernels": kernels_verify,
         "roofline": {"bound": "hbm", "kernel": "gemm_gateup (bf16 MFMA, N=22016 K=4096 T=32, fused SwiGLU)",
                      "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
-                     "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": None,
+                     "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": measured_traffic(),
                      "bytes_per_launch": gu_bytes, "avg_ms": round(v_gu_avg, 5)},
     }
     if args.layers:

@@ -149,8 +149,10 @@ hipEvent_t take_event(cas_ctx* c) {
         c->ev_pool.pop_back();
         return e;
     }
+    // timing-only events: no system-scope fence (cache writeback) at record,
+    // so the bracket measures the launch rather than the fence
     hipEvent_t e = nullptr;
-    if (hipEventCreate(&e) != hipSuccess) return nullptr;
+    if (hipEventCreateWithFlags(&e, hipEventDisableSystemFence) != hipSuccess) return nullptr;
     return e;
 }
 
