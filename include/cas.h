@@ -5,15 +5,15 @@
  * One call, cas_forward, runs a Llama-style decoder over the nodes of a small
  * draft token tree against the KV cache.  The same call serves
  *   - the target model's verification of a whole tree in one pass with tree
- *     attention (Sec. 3.2, "Tree Cascade"; Sec. 2 on speculative decoding), and
+ *     attention (Sec. 4.2, "Tree Cascade"; Sec. 2 on speculative decoding), and
  *   - the "virtual" draft models that a DSIA strategy switches on per call
- *     (Def. 3.1; Sec. 3.1 strategy list): layer sparsity (skip_mask) and
+ *     (Def. 4.1; Sec. 4.1 strategy list): layer sparsity (skip_mask) and
  *     activation quantisation (act_quant: per-token int8 activations against a
  *     per-output-channel int8 copy of the weights, App. C), including the
- *     tree-parallel draft calls over a leaf and its siblings (Sec. 3.2,
+ *     tree-parallel draft calls over a leaf and its siblings (Sec. 4.2,
  *     "Tree-based Parallel Draft Generation").
  * cas_accept_tree performs greedy verification of the tree (lossless decoding,
- * Sec. 4.1: the output equals greedy autoregressive decoding), and
+ * Sec. 5.1: the output equals greedy autoregressive decoding), and
  * cas_kv_compact commits the accepted path into the cache that drafts and
  * target share (self-speculative decoding keeps no separate draft cache, Sec. 2).
  *

@@ -7,10 +7,10 @@
  *
  * What it computes (CAS-Spec, arXiv 2510.26843):
  *   - the target model's forward over the nodes of a draft token tree that is
- *     verified in one pass with tree attention (Sec. 3.2, "Tree Cascade" and
+ *     verified in one pass with tree attention (Sec. 4.2, "Tree Cascade" and
  *     "Tree-based Parallel Draft Generation"; Sec. 2, speculative decoding);
  *   - the same forward as a "virtual" draft model switched on by a DSIA
- *     strategy (Def. 3.1 and the strategy list of Sec. 3.1): layer sparsity
+ *     strategy (Def. 4.1 and the strategy list of Sec. 4.1): layer sparsity
  *     (whole layers skipped per call) and activation quantisation (per-token
  *     int8 activations against an int8 copy of the weights; App. C);
  *   - committing the accepted path of a verified tree into the KV cache that

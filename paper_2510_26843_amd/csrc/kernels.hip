@@ -1,7 +1,7 @@
 // gfx950 (MI355X, CDNA4) kernels of the CAS-Spec token-tree decoder step.
 //
-// Hot path (Sec. 3.2: one target forward verifies a whole draft tree with tree
-// attention; Def. 3.1 / Sec. 3.1: the same forward with layers skipped or
+// Hot path (Sec. 4.2: one target forward verifies a whole draft tree with tree
+// attention; Def. 4.1 / Sec. 4.1: the same forward with layers skipped or
 // int8 activations is a draft model):
 //   k_gemm       weight-streaming linear layer on MFMA (bf16 16x16x32, int8
 //                16x16x64, fp32 16x16x4) with fused epilogues: RoPE + KV

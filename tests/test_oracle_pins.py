@@ -7,9 +7,9 @@ fails at least one of them:
     (torch rms_norm, scaled_dot_product_attention with a causal mask, silu,
     complex-number rotation for RoPE): the textbook model;
   - tree verification equals independent causal forwards along each
-    root-to-node path (the exactness of tree attention, Sec. 3.2);
+    root-to-node path (the exactness of tree attention, Sec. 4.2);
   - greedy speculative decoding equals greedy autoregressive decoding token
-    for token (lossless decoding, Sec. 4.1);
+    for token (lossless decoding, Sec. 5.1);
   - closed forms: skip-all logits, one-key attention, RoPE relative-position
     identity, RMSNorm output scale, exact integer dot products;
   - structural invariants: skip-layer-l equals deleting layer l, GQA equals
