@@ -296,38 +296,42 @@ __global__ void __launch_bounds__(64 * WAVES) k_gemm(const GemmArgs a) {
 }
 
 // Wide variant for tall weight matrices: the four waves of a workgroup own
-// four adjacent 16-row tiles over the whole K range, and the activation
-// fragments of each stage are loaded once per workgroup (each thread one
-// 16-byte piece of a contiguous 4 KB run) into a two-slot LDS ring that all
-// four waves read: four times less activation traffic than one tile per
-// workgroup.  One barrier per stage; register stages as in k_gemm.
-template <int WT, int NT, int UC, int D, int EPI, typename AT>
+// 4*TPW adjacent 16-row tiles (TPW per wave) over the whole K range, and the
+// activation fragments of each stage are loaded once per workgroup (each
+// thread one 16-byte piece of a contiguous 4 KB run) into a two-slot LDS ring
+// that all four waves read: 4*TPW times less activation traffic than one tile
+// per workgroup.  One barrier per stage; register stages as in k_gemm.
+template <int WT, int NT, int UC, int D, int TPW, int EPI, typename AT>
 __global__ void __launch_bounds__(256) k_gemm_wide(const GemmArgs a) {
     using Tr = WTr<WT>;
     using ACC = typename Tr::acc_t;
     constexpr int E = Tr::E;
     constexpr int NB = NT * UC;  // 1 KB activation blocks per stage
     constexpr int LPT = NB / 4;  // 16-byte loads per thread per stage
-    static_assert(NB % 4 == 0 && D % 2 == 0, "stage shape");
+    static_assert(NB % 4 == 0 && D % 2 == 0 && FRAG_U % UC == 0, "stage shape");
     __shared__ __attribute__((aligned(16))) char lds[2][NB * 1024];
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-    const int tile = blockIdx.x * 4 + wave;
+    const int tile0 = (blockIdx.x * 4 + wave) * TPW;
     const int C = a.Kp / (16 * E);
     const int NS = C * (FRAG_U / UC);  // stages over the whole K range
-    const char* wb = (const char*)a.W + ((size_t)tile * C * FRAG_U * 64 + lane) * 16;
+    const char* wb = (const char*)a.W + ((size_t)tile0 * C * FRAG_U * 64 + lane) * 16;
+    const size_t tstride = (size_t)C * FRAG_U * 1024;  // bytes of one tile
     const char* xb = (const char*)a.X + (size_t)threadIdx.x * 16;
-    ACC acc[NT];
+    ACC acc[TPW][NT];
 #pragma unroll
-    for (int j = 0; j < NT; ++j) acc[j] = ACC{0, 0, 0, 0};
-    i32x4 A[D][UC];
+    for (int t = 0; t < TPW; ++t)
+#pragma unroll
+        for (int j = 0; j < NT; ++j) acc[t][j] = ACC{0, 0, 0, 0};
+    i32x4 A[D][TPW][UC];
     i32x4 Bv[D][LPT];
 
 #define CAS_W_LOAD(st, stage)                                                                    \
     do {                                                                                         \
         const size_t q = (size_t)(stage) * UC;                                                   \
-        _Pragma("unroll") for (int u = 0; u < UC; ++u) A[st][u] =                               \
-            __builtin_nontemporal_load((const i32x4*)(wb + (q + u) * 1024));                     \
+        _Pragma("unroll") for (int t = 0; t < TPW; ++t)                                         \
+            _Pragma("unroll") for (int u = 0; u < UC; ++u) A[st][t][u] =                        \
+                __builtin_nontemporal_load((const i32x4*)(wb + t * tstride + (q + u) * 1024));   \
         _Pragma("unroll") for (int p = 0; p < LPT; ++p) Bv[st][p] =                             \
             *(const i32x4*)(xb + ((size_t)(stage) * NB + 4 * p) * 1024);                         \
     } while (0)
@@ -339,7 +343,8 @@ __global__ void __launch_bounds__(256) k_gemm_wide(const GemmArgs a) {
         _Pragma("unroll") for (int u = 0; u < UC; ++u)                                          \
             _Pragma("unroll") for (int j = 0; j < NT; ++j) {                                    \
                 const i32x4 b = *(const i32x4*)(&lds[slot][(u * NT + j) * 1024 + lane * 16]);    \
-                acc[j] = mfma_step<WT>(A[st][u], b, acc[j]);                                     \
+                _Pragma("unroll") for (int t = 0; t < TPW; ++t)                                 \
+                    acc[t][j] = mfma_step<WT>(A[st][t][u], b, acc[t][j]);                        \
             }                                                                                    \
     } while (0)
 
@@ -368,7 +373,8 @@ __global__ void __launch_bounds__(256) k_gemm_wide(const GemmArgs a) {
         if (c + D + s < NS) CAS_W_STAGE(s, s & 1);
 #undef CAS_W_STAGE
 #undef CAS_W_LOAD
-    gemm_epilogue<WT, NT, EPI, AT>(a, acc, tile, a.N / 16 - 1, lane);
+#pragma unroll
+    for (int t = 0; t < TPW; ++t) gemm_epilogue<WT, NT, EPI, AT>(a, acc[t], tile0 + t, a.N / 16 - 1, lane);
 }
 
 // Matrices with at least 8192 rows (a multiple of 64) take the wide variant;
@@ -378,7 +384,14 @@ template <int WT, int NT, int EPI, typename AT>
 static hipError_t gemm_go(const GemmArgs& a, hipStream_t s) {
     constexpr int UC = NT == 2 ? 4 : (NT == 4 ? 2 : 1);
     if (a.N >= 8192 && a.N % 64 == 0) {
-        hipLaunchKernelGGL((k_gemm_wide<WT, NT, UC, 4, EPI, AT>), dim3(a.N / 64), dim3(256), 0, s, a);
+        // two tiles per wave once one tile per wave would need more than 256
+        // workgroups: every workgroup then stays resident on its own CU (a
+        // CU holding two workgroups while others hold one sets the pace)
+        const int tiles = a.N / 16;
+        if (tiles / 4 > 256 && tiles % 8 == 0)
+            hipLaunchKernelGGL((k_gemm_wide<WT, NT, UC, 2, 2, EPI, AT>), dim3(tiles / 8), dim3(256), 0, s, a);
+        else
+            hipLaunchKernelGGL((k_gemm_wide<WT, NT, UC, 4, 1, EPI, AT>), dim3(tiles / 4), dim3(256), 0, s, a);
         return hipGetLastError();
     }
     constexpr int D = NT == 2 ? 2 : 4;
