@@ -295,29 +295,29 @@ __global__ void __launch_bounds__(64 * WAVES) k_gemm(const GemmArgs a) {
     gemm_epilogue<WT, NT, EPI, AT>(a, acc, blockIdx.x, (int)gridDim.x - 1, lane);
 }
 
-// Wide variant for tall weight matrices: the four waves of a workgroup own
-// 4*TPW adjacent 16-row tiles (TPW per wave) over the whole K range, and the
-// activation fragments of each stage are loaded once per workgroup (each
-// thread one 16-byte piece of a contiguous 4 KB run) into a two-slot LDS ring
-// that all four waves read: 4*TPW times less activation traffic than one tile
+// Wide variant for tall weight matrices: the WAVES waves of a workgroup own
+// WAVES*TPW adjacent 16-row tiles (TPW per wave) over the whole K range, and
+// the activation fragments of each stage are loaded once per workgroup (wave
+// w loads the stage's 1 KB blocks w, w + WAVES, ...) into a two-slot LDS ring
+// that all waves read: WAVES*TPW times less activation traffic than one tile
 // per workgroup.  One barrier per stage; register stages as in k_gemm.
-template <int WT, int NT, int UC, int D, int TPW, int EPI, typename AT>
-__global__ void __launch_bounds__(256) k_gemm_wide(const GemmArgs a) {
+template <int WT, int NT, int UC, int D, int WAVES, int TPW, int EPI, typename AT>
+__global__ void __launch_bounds__(64 * WAVES) k_gemm_wide(const GemmArgs a) {
     using Tr = WTr<WT>;
     using ACC = typename Tr::acc_t;
     constexpr int E = Tr::E;
     constexpr int NB = NT * UC;  // 1 KB activation blocks per stage
-    constexpr int LPT = NB / 4;  // 16-byte loads per thread per stage
-    static_assert(NB % 4 == 0 && D % 2 == 0 && FRAG_U % UC == 0, "stage shape");
+    constexpr int LPT = (NB + WAVES - 1) / WAVES;  // 1 KB blocks per wave per stage
+    static_assert(D % 2 == 0 && FRAG_U % UC == 0, "stage shape");
     __shared__ __attribute__((aligned(16))) char lds[2][NB * 1024];
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-    const int tile0 = (blockIdx.x * 4 + wave) * TPW;
+    const int tile0 = (blockIdx.x * WAVES + wave) * TPW;
     const int C = a.Kp / (16 * E);
     const int NS = C * (FRAG_U / UC);  // stages over the whole K range
     const char* wb = (const char*)a.W + ((size_t)tile0 * C * FRAG_U * 64 + lane) * 16;
     const size_t tstride = (size_t)C * FRAG_U * 1024;  // bytes of one tile
-    const char* xb = (const char*)a.X + (size_t)threadIdx.x * 16;
+    const char* xb = (const char*)a.X + (size_t)lane * 16;
     ACC acc[TPW][NT];
 #pragma unroll
     for (int t = 0; t < TPW; ++t)
@@ -332,13 +332,15 @@ __global__ void __launch_bounds__(256) k_gemm_wide(const GemmArgs a) {
         _Pragma("unroll") for (int t = 0; t < TPW; ++t)                                         \
             _Pragma("unroll") for (int u = 0; u < UC; ++u) A[st][t][u] =                        \
                 __builtin_nontemporal_load((const i32x4*)(wb + t * tstride + (q + u) * 1024));   \
+        /* a block index past the stage (WAVES not dividing NB) reloads the last block, */  \
+        /* so every wave issues the same loads; it is not stored */                         \
         _Pragma("unroll") for (int p = 0; p < LPT; ++p) Bv[st][p] =                             \
-            *(const i32x4*)(xb + ((size_t)(stage) * NB + 4 * p) * 1024);                         \
+            *(const i32x4*)(xb + ((size_t)(stage) * NB + min(p * WAVES + wave, NB - 1)) * 1024); \
     } while (0)
 #define CAS_W_STAGE(st, slot)                                                                    \
     do {                                                                                         \
-        _Pragma("unroll") for (int p = 0; p < LPT; ++p)                                         \
-            *(i32x4*)(&lds[slot][4 * p * 1024 + threadIdx.x * 16]) = Bv[st][p];                  \
+        _Pragma("unroll") for (int p = 0; p < LPT; ++p) if (p * WAVES + wave < NB)              \
+            *(i32x4*)(&lds[slot][(p * WAVES + wave) * 1024 + lane * 16]) = Bv[st][p];            \
         __syncthreads();                                                                         \
         _Pragma("unroll") for (int u = 0; u < UC; ++u)                                          \
             _Pragma("unroll") for (int j = 0; j < NT; ++j) {                                    \
@@ -377,21 +379,38 @@ __global__ void __launch_bounds__(256) k_gemm_wide(const GemmArgs a) {
     for (int t = 0; t < TPW; ++t) gemm_epilogue<WT, NT, EPI, AT>(a, acc[t], tile0 + t, a.N / 16 - 1, lane);
 }
 
-// Matrices with at least 8192 rows (a multiple of 64) take the wide variant;
+// Matrices with at least 8192 rows (in tiles: a multiple of 3 or 4) take the wide variant;
 // shorter ones split K across the waves of a 16-row workgroup so that the
 // grid still covers every CU.
 template <int WT, int NT, int EPI, typename AT>
 static hipError_t gemm_go(const GemmArgs& a, hipStream_t s) {
     constexpr int UC = NT == 2 ? 4 : (NT == 4 ? 2 : 1);
-    if (a.N >= 8192 && a.N % 64 == 0) {
-        // two tiles per wave once one tile per wave would need more than 256
-        // workgroups: every workgroup then stays resident on its own CU (a
-        // CU holding two workgroups while others hold one sets the pace)
+    if (a.N >= 8192 && ((a.N / 16) % 4 == 0 || (a.N / 16) % 3 == 0)) {
+        // Every workgroup should stay resident on a CU of its own (a CU that
+        // holds two workgroups while others hold one sets the pace): take the
+        // split of the tiles into equal workgroups of 4x1, 3x1, 4x2 or 3x2
+        // tiles (waves x tiles per wave) with the most workgroups up to 256,
+        // else 4x2.
         const int tiles = a.N / 16;
-        if (tiles / 4 > 256 && tiles % 8 == 0)
-            hipLaunchKernelGGL((k_gemm_wide<WT, NT, UC, 2, 2, EPI, AT>), dim3(tiles / 8), dim3(256), 0, s, a);
+        static const int opt[4][2] = {{4, 1}, {3, 1}, {4, 2}, {3, 2}};
+        int bw = 0, bt = 0, bg = 0;
+        for (const auto& o : opt) {
+            const int per = o[0] * o[1];
+            if (tiles % per == 0 && tiles / per <= 256 && tiles / per > bg) { bw = o[0]; bt = o[1]; bg = tiles / per; }
+        }
+        if (!bg) {
+            if (tiles % 8 == 0) { bw = 4; bt = 2; bg = tiles / 8; }
+            else if (tiles % 4 == 0) { bw = 4; bt = 1; bg = tiles / 4; }
+            else { bw = 3; bt = 1; bg = tiles / 3; }
+        }
+        if (bw == 4 && bt == 1)
+            hipLaunchKernelGGL((k_gemm_wide<WT, NT, UC, 4, 4, 1, EPI, AT>), dim3(bg), dim3(256), 0, s, a);
+        else if (bw == 3 && bt == 1)
+            hipLaunchKernelGGL((k_gemm_wide<WT, NT, UC, 4, 3, 1, EPI, AT>), dim3(bg), dim3(192), 0, s, a);
+        else if (bw == 4)
+            hipLaunchKernelGGL((k_gemm_wide<WT, NT, UC, 2, 4, 2, EPI, AT>), dim3(bg), dim3(256), 0, s, a);
         else
-            hipLaunchKernelGGL((k_gemm_wide<WT, NT, UC, 4, 1, EPI, AT>), dim3(tiles / 4), dim3(256), 0, s, a);
+            hipLaunchKernelGGL((k_gemm_wide<WT, NT, UC, 2, 3, 2, EPI, AT>), dim3(bg), dim3(192), 0, s, a);
         return hipGetLastError();
     }
     constexpr int D = NT == 2 ? 2 : 4;

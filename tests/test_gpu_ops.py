@@ -34,12 +34,13 @@ def _gemm_bound(x64, w64):
     return K * 2.0 ** -23 * (np.abs(x64) @ np.abs(w64).T) + 1e-30
 
 
-# N >= 8192 with N % 64 == 0 takes the four-tile workgroup variant (two tiles
-# per wave from N = 16512 on); 8208 does not
+# N >= 8192 with N/16 a multiple of 3 or 4 takes the multi-tile workgroup
+# variant: 4 waves x 1 tile (8192, 8256), 3 x 1 (8208, 12288), 4 x 2 (16512),
+# 3 x 2 (24480); 8240 and smaller N split K inside a one-tile workgroup
 @pytest.mark.parametrize("N,K,T", [(64, 4096, 32), (48, 688, 5), (32, 256, 1), (16, 1376, 17), (64, 512, 128),
                                    (80, 11008, 64), (32, 128, 100), (8192, 512, 32), (8256, 256, 5),
                                    (8192, 384, 128), (8208, 256, 9), (8320, 128, 1), (16512, 256, 32),
-                                   (16512, 128, 100)])
+                                   (16512, 128, 100), (12288, 256, 32), (24480, 128, 20), (8240, 128, 3)])
 def test_gemm_bf16(N, K, T):
     w = synth.f32_to_bf16_bits(synth.gen_activations(N, K, seed=N + K, edge_rows=False) * 0.02)
     x = synth.f32_to_bf16_bits(synth.gen_activations(T, K, seed=T + 7))
@@ -68,7 +69,8 @@ def test_gemm_f32_and_residual(N, K, T):
 
 
 @pytest.mark.parametrize("N,K,T", [(64, 4096, 32), (48, 688, 5), (16, 13824, 3), (32, 256, 100), (16, 5120, 64),
-                                   (8192, 512, 32), (8256, 256, 1), (8192, 256, 65), (16512, 256, 17)])
+                                   (8192, 512, 32), (8256, 256, 1), (8192, 256, 65), (16512, 256, 17),
+                                   (12288, 128, 5), (24480, 128, 33)])
 def test_gemm_int8_bit_exact(N, K, T):
     rng = np.random.default_rng(N * 7 + K + T)
     qw = rng.integers(-127, 128, (N, K)).astype(np.int8)
