@@ -576,8 +576,10 @@ __device__ __forceinline__ bool anc_bit(uint64_t a0, uint64_t a1, int node) {
 // out of the QK^T MFMA with slots along the row index; the cache puts slots
 // 8g..8g+7 of a tile in lane group g, which is exactly the k-order of the P
 // operand of the PV MFMA, so probabilities never leave registers.  Each wave
-// issues the K and V fragments of both its tiles before any arithmetic.  The
-// four waves merge in LDS and write the split's partial; k_attn_merge then
+// issues its query fragments and then the K and V fragments of its tiles in
+// the order they are consumed, before any arithmetic.  The four waves put
+// their states in LDS (one barrier) and the workgroup writes the split's
+// partial as float4 runs, waves summed in wave order; k_attn_merge then
 // merges the splits in split order (deterministic).  (Merging inside this
 // kernel by its last-arriving workgroup needs device-scope fences that cost
 // more than the separate launch on gfx950.)
@@ -587,6 +589,7 @@ __global__ void __launch_bounds__(256) k_attn_bf16(const AttnArgs a, float scale
     constexpr int DG = HD / 4;    // head_dim span of one lane group
     constexpr int NDT = HD / 16;  // output d tiles
     constexpr int TE = 32 * HD;   // elements per key tile
+    constexpr int RS = HD + 4;    // LDS row stride of the wave states (floats; conflict-free float4 rows)
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int r = lane & 15, g = lane >> 4;
     const int split = blockIdx.x, kvh = blockIdx.y, rc = blockIdx.z;
@@ -595,10 +598,29 @@ __global__ void __launch_bounds__(256) k_attn_bf16(const AttnArgs a, float scale
     const int T = a.T, Tp = (T + 15) & ~15, G = a.H / a.Hkv;
     const int nct = G * Tp / 16;
     const uint16_t* q = (const uint16_t*)a.q;
+
+    // query fragments of the two 16-row column tiles (rows past T read row
+    // T-1 and are zeroed below, so every load is unconditional)
+    bool tv[2];
+    int head[2], t0[2];
+    i32x4 Qf[2][UD];
+    uint64_t an0[2], an1[2];
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+        const int ct = 2 * rc + j;
+        tv[j] = ct < nct;
+        const int hg = tv[j] ? (ct * 16) / Tp : 0;
+        t0[j] = (ct * 16) % Tp;
+        head[j] = kvh * G + hg;
+        const int t = min(t0[j] + r, T - 1);
+#pragma unroll
+        for (int u = 0; u < UD; ++u) Qf[j][u] = *(const i32x4*)(q + ((size_t)t * a.H + head[j]) * HD + g * DG + u * 8);
+        an0[j] = a.anc[2 * t];
+        an1[j] = a.anc[2 * t + 1];
+    }
+    // K and V fragments of this wave's tiles, in the order they are consumed
     const uint16_t* kbase = (const uint16_t*)a.kc + (size_t)kvh * a.ctx_cap * HD + lane * 8;
     const uint16_t* vbase = (const uint16_t*)a.vt + (size_t)kvh * a.ctx_cap * HD + lane * 8;
-
-    // K and V fragments of this wave's tiles first: the longest latency
     const int tile0 = (split * ATT_WAVES + wave) * ATT_TPW;
     i32x4 Kf[ATT_TPW][2][UD], Vf[ATT_TPW][NDT];
 #pragma unroll
@@ -611,26 +633,14 @@ __global__ void __launch_bounds__(256) k_attn_bf16(const AttnArgs a, float scale
 #pragma unroll
         for (int dt = 0; dt < NDT; ++dt) Vf[tt][dt] = *(const i32x4*)(vbase + tb + dt * 512);
     }
-
-    bool tv[2];
-    int head[2], t0[2];
-    i32x4 Qf[2][UD];
-    uint64_t an0[2], an1[2];
     const i32x4 zero = {0, 0, 0, 0};
 #pragma unroll
     for (int j = 0; j < 2; ++j) {
-        const int ct = 2 * rc + j;
-        tv[j] = ct < nct;
-        const int hg = tv[j] ? (ct * 16) / Tp : 0;
-        t0[j] = (ct * 16) % Tp;
-        head[j] = kvh * G + hg;
-        const int t = t0[j] + r;
-        const bool ok = tv[j] && t < T;
+        if (!(tv[j] && t0[j] + r < T)) {
 #pragma unroll
-        for (int u = 0; u < UD; ++u)
-            Qf[j][u] = ok ? *(const i32x4*)(q + ((size_t)t * a.H + head[j]) * HD + g * DG + u * 8) : zero;
-        an0[j] = ok ? a.anc[2 * t] : 0ull;
-        an1[j] = ok ? a.anc[2 * t + 1] : 0ull;
+            for (int u = 0; u < UD; ++u) Qf[j][u] = zero;
+            an0[j] = an1[j] = 0ull;
+        }
     }
 
     float m[2] = {-1e30f, -1e30f}, l[2] = {0.f, 0.f};
@@ -643,7 +653,7 @@ __global__ void __launch_bounds__(256) k_attn_bf16(const AttnArgs a, float scale
 #pragma unroll
     for (int tt = 0; tt < ATT_TPW; ++tt) {
         const int ti = tile0 + tt;
-        if (ti >= n_tiles || !(tv[0] || tv[1])) continue;
+        if (ti >= n_tiles) continue;
         const int tb = ti * 32;
         f32x4 S[2][2];
 #pragma unroll
@@ -696,9 +706,10 @@ __global__ void __launch_bounds__(256) k_attn_bf16(const AttnArgs a, float scale
             for (int j = 0; j < 2; ++j) O[dt][j] = mfma_step<ET_BF16>(Vf[tt][dt], Pf[j], O[dt][j]);
     }
 
-    // ---- merge the four waves in LDS (wave order)
+    // ---- merge the four waves: states to LDS, one barrier, then each
+    // (row, 4 d) of the split is the wave-order sum of the rescaled states
     __shared__ float sm_m[ATT_WAVES][2][16], sm_l[ATT_WAVES][2][16];
-    __shared__ float sm_o[2][HD][16];
+    __shared__ __attribute__((aligned(16))) float sm_o[ATT_WAVES][2][16][RS];
     if (g == 0) {
 #pragma unroll
         for (int j = 0; j < 2; ++j) {
@@ -706,42 +717,33 @@ __global__ void __launch_bounds__(256) k_attn_bf16(const AttnArgs a, float scale
             sm_l[wave][j][r] = l[j];
         }
     }
+#pragma unroll
+    for (int dt = 0; dt < NDT; ++dt)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) *(f32x4*)(&sm_o[wave][j][r][16 * dt + 4 * g]) = O[dt][j];
     __syncthreads();
-    float f[2];
+    constexpr int D4 = HD / 4;
+    for (int idx = threadIdx.x; idx < 2 * 16 * D4; idx += 256) {
+        const int j = idx / (16 * D4), rr = (idx / D4) & 15, d4 = (idx % D4) * 4;
+        const int t = (j ? t0[1] : t0[0]) + rr;
+        if (!(j ? tv[1] : tv[0]) || t >= T) continue;
+        float mw[ATT_WAVES], M = -1e30f;
 #pragma unroll
-    for (int j = 0; j < 2; ++j) {
-        const float M = fmaxf(fmaxf(sm_m[0][j][r], sm_m[1][j][r]), fmaxf(sm_m[2][j][r], sm_m[3][j][r]));
-        f[j] = exp2f(m[j] - M);
-    }
-    for (int w = 0; w < ATT_WAVES; ++w) {
-        if (wave == w) {
-#pragma unroll
-            for (int dt = 0; dt < NDT; ++dt)
-#pragma unroll
-                for (int j = 0; j < 2; ++j)
-#pragma unroll
-                    for (int i = 0; i < 4; ++i) {
-                        float& dst = sm_o[j][16 * dt + 4 * g + i][r];
-                        const float val = O[dt][j][i] * f[j];
-                        dst = (w == 0) ? val : dst + val;
-                    }
+        for (int w = 0; w < ATT_WAVES; ++w) {
+            mw[w] = sm_m[w][j][rr];
+            M = fmaxf(M, mw[w]);
         }
-        __syncthreads();
-    }
-    // ---- this split's partial for every valid (row, d), d fastest (coalesced)
-    for (int idx = threadIdx.x; idx < 2 * 16 * HD; idx += 256) {
-        const int row = idx / HD, d = idx % HD, j = row >> 4, rr = row & 15;
-        const int t = t0[j] + rr;
-        if (!tv[j] || t >= T) continue;
-        const size_t o = ((size_t)split * a.H + head[j]) * T + t;
-        a.part_o[o * HD + d] = sm_o[j][d][rr];
-        if (d == 0) {
-            const float Mj = fmaxf(fmaxf(sm_m[0][j][rr], sm_m[1][j][rr]), fmaxf(sm_m[2][j][rr], sm_m[3][j][rr]));
-            float L = 0.f;
-            for (int w = 0; w < ATT_WAVES; ++w) L += sm_l[w][j][rr] * exp2f(sm_m[w][j][rr] - Mj);
-            a.part_ml[o * 2] = Mj;
-            a.part_ml[o * 2 + 1] = L;
+        f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+        float L = 0.f;
+#pragma unroll
+        for (int w = 0; w < ATT_WAVES; ++w) {
+            const float f = exp2f(mw[w] - M);
+            acc += *(const f32x4*)(&sm_o[w][j][rr][d4]) * f;
+            L += sm_l[w][j][rr] * f;
         }
+        const size_t o = ((size_t)split * a.H + (j ? head[1] : head[0])) * T + t;
+        *(f32x4*)(a.part_o + o * HD + d4) = acc;
+        if (d4 == 0) *(float2*)(a.part_ml + o * 2) = make_float2(M, L);
     }
 }
 
