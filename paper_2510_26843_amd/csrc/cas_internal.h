@@ -101,11 +101,22 @@ struct GemmArgs {
     void* kc;               // key cache of the layer (act type, cache layout)
     void* vt;               // value cache of the layer (act type, cache layout)
     int H, Hkv, hd, ctx_cap;
+    // split-K partial sums (launch_gemm_parts): split k writes its fp32 sums
+    // to out + k * part_stride, [T][ldo]
+    int ksplit;
+    size_t part_stride;
 };
 
 // wtype: element type of W and X; atype: activation type written by the
 // SWIGLU and QKV epilogues (ET_F32 or ET_BF16).
 hipError_t launch_gemm(int wtype, int atype, int epi, const GemmArgs& a, hipStream_t s);
+// Number of K splits for a residual projection of N rows whose partial sums
+// a following RMSNorm adds to the residual stream: 1 = do not split (enough
+// workgroups already, int8 weights, or too few stages).
+int gemm_parts_count(int wtype, int N, int Kp, int T);
+// The split-K form: a.ksplit splits, each writing fp32 sums of its K range to
+// a.out + k * a.part_stride ([T][a.ldo]); bf16 / fp32 weights only.
+hipError_t launch_gemm_parts(int wtype, const GemmArgs& a, hipStream_t s);
 
 struct AttnArgs {
     const void* q;        // [T][H][hd]
@@ -133,8 +144,11 @@ hipError_t launch_kv_convert(int atype, void* kc, void* vt, const void* k_rows, 
 // RMSNorm of rows of the fp32 residual stream h [T][d] with gains g:
 // writes the normalised rows as tiled activations of act type (out) or, with
 // q != NULL, their int8 quantisation (tiled int8 q, scales qs [T]) instead.
-hipError_t launch_rmsnorm(int atype, const float* h, const float* g, int T, int d, float eps,
-                          void* out, int8_t* q, float* qs, hipStream_t s);
+// With nparts > 0 the rows first take the pending split-K sums of the last
+// projection: h += parts[0] + ... + parts[nparts-1] (in that order; part p at
+// parts + p * pstride, [T][d]), stored back to h.
+hipError_t launch_rmsnorm(int atype, float* h, const float* g, int T, int d, float eps, void* out, int8_t* q,
+                          float* qs, const float* parts, int nparts, size_t pstride, hipStream_t s);
 // Per-row int8 quantisation of x [T][K] (act type).  tiled = 1: x is tiled
 // activations and q is written tiled; tiled = 0: both row-major.
 hipError_t launch_quant_rows(int atype, const void* x, int T, int K, int8_t* q, float* qs, int tiled,

@@ -21,6 +21,7 @@
 // contraction only needs A and B to agree on which k sits in which register
 // element, so this k-order is free.
 #include "cas_internal.h"
+#include <algorithm>
 
 #include <hip/hip_runtime.h>
 #include <math.h>
@@ -314,10 +315,13 @@ __global__ void __launch_bounds__(64 * WAVES) k_gemm_wide(const GemmArgs a) {
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int tile0 = (blockIdx.x * WAVES + wave) * TPW;
     const int C = a.Kp / (16 * E);
-    const int NS = C * (FRAG_U / UC);  // stages over the whole K range
-    const char* wb = (const char*)a.W + ((size_t)tile0 * C * FRAG_U * 64 + lane) * 16;
+    // stages of this workgroup: the whole K range, or split gridDim.y ways
+    const int NS_all = C * (FRAG_U / UC);
+    const int s0 = (int)(((long)blockIdx.y * NS_all) / gridDim.y);
+    const int NS = (int)(((long)(blockIdx.y + 1) * NS_all) / gridDim.y) - s0;
+    const char* wb = (const char*)a.W + ((size_t)tile0 * C * FRAG_U * 64 + lane) * 16 + (size_t)s0 * UC * 1024;
     const size_t tstride = (size_t)C * FRAG_U * 1024;  // bytes of one tile
-    const char* xb = (const char*)a.X + (size_t)lane * 16;
+    const char* xb = (const char*)a.X + (size_t)lane * 16 + (size_t)s0 * NB * 1024;
     ACC acc[TPW][NT];
 #pragma unroll
     for (int t = 0; t < TPW; ++t)
@@ -375,8 +379,15 @@ __global__ void __launch_bounds__(64 * WAVES) k_gemm_wide(const GemmArgs a) {
         if (c + D + s < NS) CAS_W_STAGE(s, s & 1);
 #undef CAS_W_STAGE
 #undef CAS_W_LOAD
+    if (gridDim.y == 1) {
 #pragma unroll
-    for (int t = 0; t < TPW; ++t) gemm_epilogue<WT, NT, EPI, AT>(a, acc[t], tile0 + t, a.N / 16 - 1, lane);
+        for (int t = 0; t < TPW; ++t) gemm_epilogue<WT, NT, EPI, AT>(a, acc[t], tile0 + t, a.N / 16 - 1, lane);
+    } else {
+        GemmArgs b = a;
+        b.out = (float*)a.out + blockIdx.y * a.part_stride;
+#pragma unroll
+        for (int t = 0; t < TPW; ++t) gemm_epilogue<WT, NT, EPI, AT>(b, acc[t], tile0 + t, a.N / 16 - 1, lane);
+    }
 }
 
 // Matrices with at least 8192 rows (in tiles: a multiple of 3 or 4) take the wide variant;
@@ -460,6 +471,37 @@ hipError_t launch_gemm(int wtype, int atype, int epi, const GemmArgs& a, hipStre
         }
         break;
     }
+    return hipErrorInvalidValue;
+}
+
+int gemm_parts_count(int wtype, int N, int Kp, int T) {
+    if (wtype == ET_I8 || N % 64 || T < 1 || T > 128) return 1;
+    const int groups = N / 64;  // four 16-row tiles per workgroup
+    if (groups >= 192) return 1;
+    const int NT = col_tiles(T), UC = NT == 2 ? 4 : (NT == 4 ? 2 : 1);
+    const int NS = Kp / chunk_k(wtype) * (FRAG_U / UC);
+    int ks = std::min(8, 256 / groups);
+    ks = std::min(ks, NS / 2);
+    return ks >= 2 ? ks : 1;
+}
+
+template <int WT, typename AT>
+static hipError_t gemm_parts_go(const GemmArgs& a, hipStream_t s) {
+    const dim3 grid(a.N / 64, a.ksplit);
+    switch (col_tiles(a.T)) {
+    case 2: hipLaunchKernelGGL((k_gemm_wide<WT, 2, 4, 4, 4, 1, EPI_STORE, AT>), grid, dim3(256), 0, s, a); break;
+    case 4: hipLaunchKernelGGL((k_gemm_wide<WT, 4, 2, 4, 4, 1, EPI_STORE, AT>), grid, dim3(256), 0, s, a); break;
+    default: hipLaunchKernelGGL((k_gemm_wide<WT, 8, 1, 4, 4, 1, EPI_STORE, AT>), grid, dim3(256), 0, s, a); break;
+    }
+    return hipGetLastError();
+}
+
+hipError_t launch_gemm_parts(int wtype, const GemmArgs& a, hipStream_t s) {
+    if (a.N % 64 || a.Kp % chunk_k(wtype) || a.Kp < chunk_k(wtype) || a.T < 1 || a.T > 128 || a.ksplit < 2 ||
+        a.ksplit > 8 || a.part_stride < (size_t)a.T * a.ldo)
+        return hipErrorInvalidValue;
+    if (wtype == ET_BF16) return gemm_parts_go<ET_BF16, uint16_t>(a, s);
+    if (wtype == ET_F32) return gemm_parts_go<ET_F32, float>(a, s);
     return hipErrorInvalidValue;
 }
 
@@ -564,6 +606,26 @@ int attention_splits(int n_slots) { return (n_slots + ATT_SPLIT - 1) / ATT_SPLIT
 size_t attention_work_bytes(int n_slots, int T, int H, int hd) {
     const size_t S = (size_t)attention_splits(n_slots);
     return S * H * T * (size_t)hd * 4 + S * H * T * 2 * 4 + 256;
+}
+
+// Butterfly max / sum with the lane 16 and lane 32 apart, through the
+// cross-lane swap instructions (no LDS round trip).  Both lanes of a pair get
+// the same operands in the same order, so their results are bit-identical.
+__device__ __forceinline__ float pair_max16(float x) {
+    const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float pair_max32(float x) {
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float pair_sum16(float x) {
+    const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+__device__ __forceinline__ float pair_sum32(float x) {
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
 __device__ __forceinline__ bool anc_bit(uint64_t a0, uint64_t a1, int node) {
@@ -679,8 +741,7 @@ __global__ void __launch_bounds__(256) k_attn_bf16(const AttnArgs a, float scale
                     x[4 * h2 + i] = xv;
                     mt = fmaxf(mt, xv);
                 }
-            mt = fmaxf(mt, __shfl_xor(mt, 16));
-            mt = fmaxf(mt, __shfl_xor(mt, 32));
+            mt = pair_max32(pair_max16(mt));
             const float mn = fmaxf(m[j], mt);
             const float alpha = exp2f(m[j] - mn);
             float ps = 0.f;
@@ -691,8 +752,7 @@ __global__ void __launch_bounds__(256) k_attn_bf16(const AttnArgs a, float scale
                 ps += p;
                 pb[e] = f2bf(p);
             }
-            ps += __shfl_xor(ps, 16);
-            ps += __shfl_xor(ps, 32);
+            ps = pair_sum32(pair_sum16(ps));
             l[j] = l[j] * alpha + ps;
             m[j] = mn;
 #pragma unroll
@@ -921,30 +981,63 @@ __device__ __forceinline__ float q8(float x, float sc) {
 
 // RMSNorm of one row of the residual stream, written as tiled activations
 // (pad columns zero) or, with Q, straight to the row's int8 quantisation.
-// Loads are float4, unconditional (clamped into the row) so they issue back
-// to back; d is a multiple of 16.
-template <typename AT, bool Q>
-__global__ void __launch_bounds__(256) k_rmsnorm(const float* h, const float* gain, int d, float eps,
-                                                 AT* out, int8_t* q, float* qs) {
+// With nparts > 0 the row first takes the pending split-K sums of the last
+// projection (summed in split order, then added to the residual, which is
+// stored back).  NV float4 per thread; loads are unconditional (clamped into
+// the row) so they issue back to back; d is a multiple of 16.
+template <typename AT, bool Q, int NV>
+__global__ void __launch_bounds__(256) k_rmsnorm(float* h, const float* gain, int d, float eps, AT* out,
+                                                 int8_t* q, float* qs, const float* parts, int nparts,
+                                                 size_t pstride) {
     __shared__ float red[4];
-    const int t = blockIdx.x, NT = col_tiles(gridDim.x);
-    const float* x = h + (size_t)t * d;
-    float4 v[NORM_MAXV], gv[NORM_MAXV];
-    float ss = 0.f;
+    const int t = blockIdx.x, NT = col_tiles(gridDim.x), tid = threadIdx.x;
+    float* x = h + (size_t)t * d;
+    float4 v[NV], gv[NV];
 #pragma unroll
-    for (int i = 0; i < NORM_MAXV; ++i) {
-        const int k4 = (threadIdx.x + 256 * i) * 4;
-        const int kc = min(k4, d - 4);
+    for (int i = 0; i < NV; ++i) {
+        const int kc = min((tid + 256 * i) * 4, d - 4);
         v[i] = *(const float4*)(x + kc);
         gv[i] = *(const float4*)(gain + kc);
-        if (k4 >= d) v[i] = make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+    if (nparts > 0) {
+        float4 ps[NV];
+        const float* pr = parts + (size_t)t * d;
+#pragma unroll
+        for (int i = 0; i < NV; ++i) ps[i] = *(const float4*)(pr + min((tid + 256 * i) * 4, d - 4));
+        for (int p = 1; p < nparts; ++p) {
+            float4 pp[NV];
+#pragma unroll
+            for (int i = 0; i < NV; ++i)
+                pp[i] = *(const float4*)(pr + p * pstride + min((tid + 256 * i) * 4, d - 4));
+#pragma unroll
+            for (int i = 0; i < NV; ++i) {
+                ps[i].x += pp[i].x;
+                ps[i].y += pp[i].y;
+                ps[i].z += pp[i].z;
+                ps[i].w += pp[i].w;
+            }
+        }
+#pragma unroll
+        for (int i = 0; i < NV; ++i) {
+            v[i].x += ps[i].x;
+            v[i].y += ps[i].y;
+            v[i].z += ps[i].z;
+            v[i].w += ps[i].w;
+            const int k4 = (tid + 256 * i) * 4;
+            if (k4 < d) *(float4*)(x + k4) = v[i];
+        }
+    }
+    float ss = 0.f;
+#pragma unroll
+    for (int i = 0; i < NV; ++i) {
+        if ((tid + 256 * i) * 4 >= d) v[i] = make_float4(0.f, 0.f, 0.f, 0.f);
         ss += v[i].x * v[i].x + v[i].y * v[i].y + v[i].z * v[i].z + v[i].w * v[i].w;
     }
     ss = block_sum256(ss, red);
     const float inv = 1.0f / sqrtf(ss / (float)d + eps);
     float amax = 0.f;
 #pragma unroll
-    for (int i = 0; i < NORM_MAXV; ++i) {
+    for (int i = 0; i < NV; ++i) {
         v[i].x = Act<AT>::round(v[i].x * inv * gv[i].x);
         v[i].y = Act<AT>::round(v[i].y * inv * gv[i].y);
         v[i].z = Act<AT>::round(v[i].z * inv * gv[i].z);
@@ -955,8 +1048,8 @@ __global__ void __launch_bounds__(256) k_rmsnorm(const float* h, const float* ga
         constexpr int EA = 16 / sizeof(AT);
         const int kpa = (d + 16 * EA - 1) / (16 * EA) * (16 * EA);
 #pragma unroll
-        for (int i = 0; i < NORM_MAXV; ++i) {
-            const int k4 = (threadIdx.x + 256 * i) * 4;
+        for (int i = 0; i < NV; ++i) {
+            const int k4 = (tid + 256 * i) * 4;
             if (k4 < kpa) st4(out, xt_off(t, k4, NT, EA), v[i].x, v[i].y, v[i].z, v[i].w);  // zero past d
         }
     } else {
@@ -965,24 +1058,40 @@ __global__ void __launch_bounds__(256) k_rmsnorm(const float* h, const float* ga
         if (threadIdx.x == 0) qs[t] = sc;
         const int kpq = (d + 255) / 256 * 256;
 #pragma unroll
-        for (int i = 0; i < NORM_MAXV; ++i) {
-            const int k4 = (threadIdx.x + 256 * i) * 4;
+        for (int i = 0; i < NV; ++i) {
+            const int k4 = (tid + 256 * i) * 4;
             if (k4 < kpq) st4q(q, xt_off(t, k4, NT, 16), q8(v[i].x, sc), q8(v[i].y, sc), q8(v[i].z, sc), q8(v[i].w, sc));
         }
     }
 }
 
-hipError_t launch_rmsnorm(int atype, const float* h, const float* g, int T, int d, float eps, void* out,
-                          int8_t* q, float* qs, hipStream_t s) {
-    if (d > 1024 * NORM_MAXV || d % 16) return hipErrorInvalidValue;
-    if (atype == ET_BF16) {
-        if (q) hipLaunchKernelGGL((k_rmsnorm<uint16_t, true>), dim3(T), dim3(256), 0, s, h, g, d, eps, (uint16_t*)out, q, qs);
-        else hipLaunchKernelGGL((k_rmsnorm<uint16_t, false>), dim3(T), dim3(256), 0, s, h, g, d, eps, (uint16_t*)out, q, qs);
-    } else {
-        if (q) hipLaunchKernelGGL((k_rmsnorm<float, true>), dim3(T), dim3(256), 0, s, h, g, d, eps, (float*)out, q, qs);
-        else hipLaunchKernelGGL((k_rmsnorm<float, false>), dim3(T), dim3(256), 0, s, h, g, d, eps, (float*)out, q, qs);
-    }
+template <typename AT, bool Q>
+static hipError_t rmsnorm_go(float* h, const float* g, int T, int d, float eps, AT* out, int8_t* q, float* qs,
+                             const float* parts, int nparts, size_t pstride, hipStream_t s) {
+    // float4 per thread covering the padded row (int8 output pads to 256, bf16 to 128)
+    const int span = (d + 255) / 256 * 256;
+    const int nv = (span + 1023) / 1024;
+#define CAS_NORM(NV) \
+    hipLaunchKernelGGL((k_rmsnorm<AT, Q, NV>), dim3(T), dim3(256), 0, s, h, g, d, eps, out, q, qs, parts, nparts, pstride)
+    if (nv <= 1) CAS_NORM(1);
+    else if (nv <= 2) CAS_NORM(2);
+    else if (nv <= 4) CAS_NORM(4);
+    else if (nv <= 6) CAS_NORM(6);
+    else CAS_NORM(NORM_MAXV);
+#undef CAS_NORM
     return hipGetLastError();
+}
+
+hipError_t launch_rmsnorm(int atype, float* h, const float* g, int T, int d, float eps, void* out, int8_t* q,
+                          float* qs, const float* parts, int nparts, size_t pstride, hipStream_t s) {
+    if (d > 1024 * NORM_MAXV || d % 16 || nparts < 0 || (nparts > 0 && (!parts || pstride < (size_t)T * d)))
+        return hipErrorInvalidValue;
+    if (atype == ET_BF16) {
+        if (q) return rmsnorm_go<uint16_t, true>(h, g, T, d, eps, (uint16_t*)out, q, qs, parts, nparts, pstride, s);
+        return rmsnorm_go<uint16_t, false>(h, g, T, d, eps, (uint16_t*)out, q, qs, parts, nparts, pstride, s);
+    }
+    if (q) return rmsnorm_go<float, true>(h, g, T, d, eps, (float*)out, q, qs, parts, nparts, pstride, s);
+    return rmsnorm_go<float, false>(h, g, T, d, eps, (float*)out, q, qs, parts, nparts, pstride, s);
 }
 
 // Per-row symmetric int8: s = amax / 127, q = clamp(rne(x / s), -127, 127).

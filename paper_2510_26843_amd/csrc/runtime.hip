@@ -91,6 +91,7 @@ struct cas_ctx {
     void* d_sw = nullptr;
     float* d_logits = nullptr;
     float* d_part = nullptr;
+    float* d_gpart = nullptr;  // split-K partial sums of the O / down projections [8][max_tree][d_model]
     size_t part_bytes = 0;
     int* d_gbuf = nullptr;
     int* d_result = nullptr;
@@ -277,6 +278,27 @@ hipError_t enqueue_forward(cas_ctx* c, int T, const uint8_t* skip, int aq) {
     at.part_o = c->d_part;
     at.part_ml = c->d_part + (size_t)S * H * T * hd;
     const int wq = aq ? (int)ET_I8 : et;
+    // split-K sums of the last O / down projection that the next RMSNorm
+    // adds to the residual stream (0: the projection updated it itself)
+    int pend = 0;
+    const size_t pstride = (size_t)T * d;
+    auto norm = [&](const float* gain, void* out, int8_t* qo, float* qso) -> hipError_t {
+        const hipError_t r = launch_rmsnorm(et, c->d_h, gain, T, d, f.rms_eps, out, qo, qso, c->d_gpart, pend,
+                                            pstride, s);
+        pend = 0;
+        return r;
+    };
+    // a residual projection: split-K partial sums when that fills the GPU better
+    auto resid_proj = [&](GemmArgs& g) -> hipError_t {
+        const int ks = aq ? 1 : gemm_parts_count(wq, g.N, g.Kp, T);
+        if (ks <= 1) return launch_gemm(wq, et, EPI_RESID, g, s);
+        g.out = c->d_gpart;
+        g.ksplit = ks;
+        g.part_stride = pstride;
+        const hipError_t r = launch_gemm_parts(wq, g, s);
+        if (r == hipSuccess) pend = ks;
+        return r;
+    };
 
     for (int l = 0; l < f.n_layers; ++l) {
         if (skip && skip[l]) continue;
@@ -284,8 +306,7 @@ hipError_t enqueue_forward(cas_ctx* c, int T, const uint8_t* skip, int aq) {
         void* kc = (char*)c->kc + kv_layer * l;
         void* vt = (char*)c->vt + kv_layer * l;
         // --- attention block
-        RUN(CAS_K_RMSNORM, launch_rmsnorm(et, c->d_h, w.attn_norm, T, d, f.rms_eps, aq ? nullptr : c->d_xn,
-                                          aq ? c->d_xq : nullptr, c->d_xs, s));
+        RUN(CAS_K_RMSNORM, norm(w.attn_norm, aq ? nullptr : c->d_xn, aq ? c->d_xq : nullptr, c->d_xs));
         GemmArgs g{};
         g.T = T;
         g.N = c->qkv_rows;
@@ -320,10 +341,9 @@ hipError_t enqueue_forward(cas_ctx* c, int T, const uint8_t* skip, int aq) {
         go.ws = w.s8[1];
         go.out = c->d_h;
         go.ldo = d;
-        RUN(CAS_K_GEMM_O, launch_gemm(wq, et, EPI_RESID, go, s));
+        RUN(CAS_K_GEMM_O, resid_proj(go));
         // --- FFN block
-        RUN(CAS_K_RMSNORM, launch_rmsnorm(et, c->d_h, w.ffn_norm, T, d, f.rms_eps, aq ? nullptr : c->d_xn,
-                                          aq ? c->d_xq : nullptr, c->d_xs, s));
+        RUN(CAS_K_RMSNORM, norm(w.ffn_norm, aq ? nullptr : c->d_xn, aq ? c->d_xq : nullptr, c->d_xs));
         GemmArgs gu{};
         gu.T = T;
         gu.N = 2 * ffn;
@@ -347,9 +367,9 @@ hipError_t enqueue_forward(cas_ctx* c, int T, const uint8_t* skip, int aq) {
         gd.ws = w.s8[3];
         gd.out = c->d_h;
         gd.ldo = d;
-        RUN(CAS_K_GEMM_DOWN, launch_gemm(wq, et, EPI_RESID, gd, s));
+        RUN(CAS_K_GEMM_DOWN, resid_proj(gd));
     }
-    RUN(CAS_K_RMSNORM, launch_rmsnorm(et, c->d_h, c->final_norm, T, d, f.rms_eps, c->d_xn, nullptr, nullptr, s));
+    RUN(CAS_K_RMSNORM, norm(c->final_norm, c->d_xn, nullptr, nullptr));
     GemmArgs gh{};
     gh.T = T;
     gh.N = f.vocab;
@@ -668,6 +688,7 @@ cas_status cas_create(const cas_config* cfg, int device, void* stream, cas_ctx**
     ALLOC(c->d_logits, T * (size_t)f.vocab * 4);
     c->part_bytes = attention_work_bytes(c->ctx_cap, (int)T, f.n_heads, f.head_dim);
     ALLOC(c->d_part, c->part_bytes);
+    ALLOC(c->d_gpart, sizeof(float) * 8 * (size_t)f.max_tree * f.d_model);
     ALLOC(c->d_gbuf, T * 8 * 3 * 4);  // per row: 8 argmax parts of (index, value, NaN flag)
     ALLOC(c->d_result, (T + 4) * 4);
     ALLOC(c->d_acc, (T + 1) * 4);
