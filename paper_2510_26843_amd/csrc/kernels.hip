@@ -726,7 +726,7 @@ __global__ void __launch_bounds__(256) k_attn_bf16(const AttnArgs a, float scale
 #pragma unroll
                 for (int u = 0; u < UD; ++u) S[h2][j] = mfma_step<ET_BF16>(Kf[tt][h2][u], Qf[j][u], S[h2][j]);
             }
-        i32x4 Pf[2];
+        i32x4 Pf[2], Pl[2];
 #pragma unroll
         for (int j = 0; j < 2; ++j) {
             float x[8];
@@ -745,12 +745,13 @@ __global__ void __launch_bounds__(256) k_attn_bf16(const AttnArgs a, float scale
             const float mn = fmaxf(m[j], mt);
             const float alpha = exp2f(m[j] - mn);
             float ps = 0.f;
-            uint16_t pb[8];
+            uint16_t pb[8], pl[8];
 #pragma unroll
             for (int e = 0; e < 8; ++e) {
                 const float p = exp2f(x[e] - mn);
                 ps += p;
                 pb[e] = f2bf(p);
+                pl[e] = f2bf(p - bf2f(pb[e]));  // exact difference, rounded: p = hi + lo to ~2^-17
             }
             ps = pair_sum32(pair_sum16(ps));
             l[j] = l[j] * alpha + ps;
@@ -759,11 +760,18 @@ __global__ void __launch_bounds__(256) k_attn_bf16(const AttnArgs a, float scale
             for (int dt = 0; dt < NDT; ++dt) O[dt][j] *= alpha;
             Pf[j] = i32x4{(int)(pb[0] | ((uint32_t)pb[1] << 16)), (int)(pb[2] | ((uint32_t)pb[3] << 16)),
                           (int)(pb[4] | ((uint32_t)pb[5] << 16)), (int)(pb[6] | ((uint32_t)pb[7] << 16))};
+            Pl[j] = i32x4{(int)(pl[0] | ((uint32_t)pl[1] << 16)), (int)(pl[2] | ((uint32_t)pl[3] << 16)),
+                          (int)(pl[4] | ((uint32_t)pl[5] << 16)), (int)(pl[6] | ((uint32_t)pl[7] << 16))};
         }
+        // P V with the probabilities as a two-term bf16 sum (hi + lo): the
+        // product carries them to fp32-level accuracy; V is exact in bf16
 #pragma unroll
         for (int dt = 0; dt < NDT; ++dt)
 #pragma unroll
-            for (int j = 0; j < 2; ++j) O[dt][j] = mfma_step<ET_BF16>(Vf[tt][dt], Pf[j], O[dt][j]);
+            for (int j = 0; j < 2; ++j) {
+                O[dt][j] = mfma_step<ET_BF16>(Vf[tt][dt], Pf[j], O[dt][j]);
+                O[dt][j] = mfma_step<ET_BF16>(Vf[tt][dt], Pl[j], O[dt][j]);
+            }
     }
 
     // ---- merge the four waves: states to LDS, one barrier, then each
