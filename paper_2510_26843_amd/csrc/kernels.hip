@@ -489,7 +489,7 @@ template <int WT, typename AT>
 static hipError_t gemm_parts_go(const GemmArgs& a, hipStream_t s) {
     const dim3 grid(a.N / 64, a.ksplit);
     switch (col_tiles(a.T)) {
-    case 2: hipLaunchKernelGGL((k_gemm_wide<WT, 2, 4, 4, 4, 1, EPI_STORE, AT>), grid, dim3(256), 0, s, a); break;
+    case 2: hipLaunchKernelGGL((k_gemm_wide<WT, 2, 4, 2, 4, 1, EPI_STORE, AT>), grid, dim3(256), 0, s, a); break;
     case 4: hipLaunchKernelGGL((k_gemm_wide<WT, 4, 2, 4, 4, 1, EPI_STORE, AT>), grid, dim3(256), 0, s, a); break;
     default: hipLaunchKernelGGL((k_gemm_wide<WT, 8, 1, 4, 4, 1, EPI_STORE, AT>), grid, dim3(256), 0, s, a); break;
     }
