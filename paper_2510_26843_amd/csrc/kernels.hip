@@ -77,6 +77,31 @@ __device__ __forceinline__ float block_max256(float v, float* sh) {
     return fmaxf(fmaxf(sh[0], sh[1]), fmaxf(sh[2], sh[3]));
 }
 
+// Reductions over a workgroup of W waves (sh: W floats of LDS); the wave
+// partials are combined in wave order, so every thread gets the same value.
+template <int W>
+__device__ __forceinline__ float block_sum(float v, float* sh) {
+    v = wave_sum(v);
+    __syncthreads();
+    if ((threadIdx.x & 63) == 0) sh[threadIdx.x >> 6] = v;
+    __syncthreads();
+    float r = sh[0];
+#pragma unroll
+    for (int w = 1; w < W; ++w) r += sh[w];
+    return r;
+}
+template <int W>
+__device__ __forceinline__ float block_max(float v, float* sh) {
+    v = wave_max(v);
+    __syncthreads();
+    if ((threadIdx.x & 63) == 0) sh[threadIdx.x >> 6] = v;
+    __syncthreads();
+    float r = sh[0];
+#pragma unroll
+    for (int w = 1; w < W; ++w) r = fmaxf(r, sh[w]);
+    return r;
+}
+
 // ---------------------------------------------------------------- GEMM
 
 template <int WT> struct WTr;
@@ -976,7 +1001,10 @@ hipError_t launch_kv_convert(int atype, void* kc, void* vt, const void* k_rows, 
 
 // ---------------------------------------------------------------- norms, quantisation
 
-static constexpr int NORM_MAXV = 8;  // float4 per thread: rows up to 8192 elements
+// One workgroup of 16 waves per row: the loads of a row spread over the
+// whole CU (measured faster than 4 waves once split-K partials are folded in).
+static constexpr int NORM_THREADS = 1024;
+static constexpr int NORM_MAXV = 4;  // float4 per thread: rows up to 16384 elements
 
 __device__ __forceinline__ void st4q(int8_t* q, size_t o, float a, float b, float c, float d) {
     const uint32_t v = (uint32_t)(uint8_t)(int8_t)a | ((uint32_t)(uint8_t)(int8_t)b << 8) |
@@ -994,16 +1022,16 @@ __device__ __forceinline__ float q8(float x, float sc) {
 // stored back).  NV float4 per thread; loads are unconditional (clamped into
 // the row) so they issue back to back; d is a multiple of 16.
 template <typename AT, bool Q, int NV>
-__global__ void __launch_bounds__(256) k_rmsnorm(float* h, const float* gain, int d, float eps, AT* out,
+__global__ void __launch_bounds__(NORM_THREADS) k_rmsnorm(float* h, const float* gain, int d, float eps, AT* out,
                                                  int8_t* q, float* qs, const float* parts, int nparts,
                                                  size_t pstride) {
-    __shared__ float red[4];
+    __shared__ float red[NORM_THREADS / 64];
     const int t = blockIdx.x, NT = col_tiles(gridDim.x), tid = threadIdx.x;
     float* x = h + (size_t)t * d;
     float4 v[NV], gv[NV];
 #pragma unroll
     for (int i = 0; i < NV; ++i) {
-        const int kc = min((tid + 256 * i) * 4, d - 4);
+        const int kc = min((tid + NORM_THREADS * i) * 4, d - 4);
         v[i] = *(const float4*)(x + kc);
         gv[i] = *(const float4*)(gain + kc);
     }
@@ -1011,12 +1039,12 @@ __global__ void __launch_bounds__(256) k_rmsnorm(float* h, const float* gain, in
         float4 ps[NV];
         const float* pr = parts + (size_t)t * d;
 #pragma unroll
-        for (int i = 0; i < NV; ++i) ps[i] = *(const float4*)(pr + min((tid + 256 * i) * 4, d - 4));
+        for (int i = 0; i < NV; ++i) ps[i] = *(const float4*)(pr + min((tid + NORM_THREADS * i) * 4, d - 4));
         for (int p = 1; p < nparts; ++p) {
             float4 pp[NV];
 #pragma unroll
             for (int i = 0; i < NV; ++i)
-                pp[i] = *(const float4*)(pr + p * pstride + min((tid + 256 * i) * 4, d - 4));
+                pp[i] = *(const float4*)(pr + p * pstride + min((tid + NORM_THREADS * i) * 4, d - 4));
 #pragma unroll
             for (int i = 0; i < NV; ++i) {
                 ps[i].x += pp[i].x;
@@ -1031,17 +1059,17 @@ __global__ void __launch_bounds__(256) k_rmsnorm(float* h, const float* gain, in
             v[i].y += ps[i].y;
             v[i].z += ps[i].z;
             v[i].w += ps[i].w;
-            const int k4 = (tid + 256 * i) * 4;
+            const int k4 = (tid + NORM_THREADS * i) * 4;
             if (k4 < d) *(float4*)(x + k4) = v[i];
         }
     }
     float ss = 0.f;
 #pragma unroll
     for (int i = 0; i < NV; ++i) {
-        if ((tid + 256 * i) * 4 >= d) v[i] = make_float4(0.f, 0.f, 0.f, 0.f);
+        if ((tid + NORM_THREADS * i) * 4 >= d) v[i] = make_float4(0.f, 0.f, 0.f, 0.f);
         ss += v[i].x * v[i].x + v[i].y * v[i].y + v[i].z * v[i].z + v[i].w * v[i].w;
     }
-    ss = block_sum256(ss, red);
+    ss = block_sum<NORM_THREADS / 64>(ss, red);
     const float inv = 1.0f / sqrtf(ss / (float)d + eps);
     float amax = 0.f;
 #pragma unroll
@@ -1057,17 +1085,17 @@ __global__ void __launch_bounds__(256) k_rmsnorm(float* h, const float* gain, in
         const int kpa = (d + 16 * EA - 1) / (16 * EA) * (16 * EA);
 #pragma unroll
         for (int i = 0; i < NV; ++i) {
-            const int k4 = (tid + 256 * i) * 4;
+            const int k4 = (tid + NORM_THREADS * i) * 4;
             if (k4 < kpa) st4(out, xt_off(t, k4, NT, EA), v[i].x, v[i].y, v[i].z, v[i].w);  // zero past d
         }
     } else {
-        amax = block_max256(amax, red);
+        amax = block_max<NORM_THREADS / 64>(amax, red);
         const float sc = amax / 127.0f;
         if (threadIdx.x == 0) qs[t] = sc;
         const int kpq = (d + 255) / 256 * 256;
 #pragma unroll
         for (int i = 0; i < NV; ++i) {
-            const int k4 = (tid + 256 * i) * 4;
+            const int k4 = (tid + NORM_THREADS * i) * 4;
             if (k4 < kpq) st4q(q, xt_off(t, k4, NT, 16), q8(v[i].x, sc), q8(v[i].y, sc), q8(v[i].z, sc), q8(v[i].w, sc));
         }
     }
@@ -1078,13 +1106,11 @@ static hipError_t rmsnorm_go(float* h, const float* g, int T, int d, float eps, 
                              const float* parts, int nparts, size_t pstride, hipStream_t s) {
     // float4 per thread covering the padded row (int8 output pads to 256, bf16 to 128)
     const int span = (d + 255) / 256 * 256;
-    const int nv = (span + 1023) / 1024;
+    const int nv = (span + 4 * NORM_THREADS - 1) / (4 * NORM_THREADS);
 #define CAS_NORM(NV) \
-    hipLaunchKernelGGL((k_rmsnorm<AT, Q, NV>), dim3(T), dim3(256), 0, s, h, g, d, eps, out, q, qs, parts, nparts, pstride)
+    hipLaunchKernelGGL((k_rmsnorm<AT, Q, NV>), dim3(T), dim3(NORM_THREADS), 0, s, h, g, d, eps, out, q, qs, parts, nparts, pstride)
     if (nv <= 1) CAS_NORM(1);
     else if (nv <= 2) CAS_NORM(2);
-    else if (nv <= 4) CAS_NORM(4);
-    else if (nv <= 6) CAS_NORM(6);
     else CAS_NORM(NORM_MAXV);
 #undef CAS_NORM
     return hipGetLastError();
@@ -1092,7 +1118,7 @@ static hipError_t rmsnorm_go(float* h, const float* g, int T, int d, float eps, 
 
 hipError_t launch_rmsnorm(int atype, float* h, const float* g, int T, int d, float eps, void* out, int8_t* q,
                           float* qs, const float* parts, int nparts, size_t pstride, hipStream_t s) {
-    if (d > 1024 * NORM_MAXV || d % 16 || nparts < 0 || (nparts > 0 && (!parts || pstride < (size_t)T * d)))
+    if (d > 4 * NORM_THREADS * NORM_MAXV || d % 16 || nparts < 0 || (nparts > 0 && (!parts || pstride < (size_t)T * d)))
         return hipErrorInvalidValue;
     if (atype == ET_BF16) {
         if (q) return rmsnorm_go<uint16_t, true>(h, g, T, d, eps, (uint16_t*)out, q, qs, parts, nparts, pstride, s);
