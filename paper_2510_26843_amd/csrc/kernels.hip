@@ -670,7 +670,7 @@ __device__ __forceinline__ bool anc_bit(uint64_t a0, uint64_t a1, int node) {
 // merges the splits in split order (deterministic).  (Merging inside this
 // kernel by its last-arriving workgroup needs device-scope fences that cost
 // more than the separate launch on gfx950.)
-template <int HD>
+template <int HD, int JT>
 __global__ void __launch_bounds__(256) k_attn_bf16(const AttnArgs a, float scale_log2) {
     constexpr int UD = HD / 32;   // k-steps of QK^T over head_dim
     constexpr int DG = HD / 4;    // head_dim span of one lane group
@@ -688,13 +688,13 @@ __global__ void __launch_bounds__(256) k_attn_bf16(const AttnArgs a, float scale
 
     // query fragments of the two 16-row column tiles (rows past T read row
     // T-1 and are zeroed below, so every load is unconditional)
-    bool tv[2];
-    int head[2], t0[2];
-    i32x4 Qf[2][UD];
-    uint64_t an0[2], an1[2];
+    bool tv[JT];
+    int head[JT], t0[JT];
+    i32x4 Qf[JT][UD];
+    uint64_t an0[JT], an1[JT];
 #pragma unroll
-    for (int j = 0; j < 2; ++j) {
-        const int ct = 2 * rc + j;
+    for (int j = 0; j < JT; ++j) {
+        const int ct = JT * rc + j;
         tv[j] = ct < nct;
         const int hg = tv[j] ? (ct * 16) / Tp : 0;
         t0[j] = (ct * 16) % Tp;
@@ -722,7 +722,7 @@ __global__ void __launch_bounds__(256) k_attn_bf16(const AttnArgs a, float scale
     }
     const i32x4 zero = {0, 0, 0, 0};
 #pragma unroll
-    for (int j = 0; j < 2; ++j) {
+    for (int j = 0; j < JT; ++j) {
         if (!(tv[j] && t0[j] + r < T)) {
 #pragma unroll
             for (int u = 0; u < UD; ++u) Qf[j][u] = zero;
@@ -730,30 +730,35 @@ __global__ void __launch_bounds__(256) k_attn_bf16(const AttnArgs a, float scale
         }
     }
 
-    float m[2] = {-1e30f, -1e30f}, l[2] = {0.f, 0.f};
-    f32x4 O[NDT][2];
+    float m[JT], l[JT];
+#pragma unroll
+    for (int j = 0; j < JT; ++j) {
+        m[j] = -1e30f;
+        l[j] = 0.f;
+    }
+    f32x4 O[NDT][JT];
 #pragma unroll
     for (int dt = 0; dt < NDT; ++dt)
 #pragma unroll
-        for (int j = 0; j < 2; ++j) O[dt][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+        for (int j = 0; j < JT; ++j) O[dt][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
 #pragma unroll
     for (int tt = 0; tt < ATT_TPW; ++tt) {
         const int ti = tile0 + tt;
         if (ti >= n_tiles) continue;
         const int tb = ti * 32;
-        f32x4 S[2][2];
+        f32x4 S[2][JT];
 #pragma unroll
         for (int h2 = 0; h2 < 2; ++h2)
 #pragma unroll
-            for (int j = 0; j < 2; ++j) {
+            for (int j = 0; j < JT; ++j) {
                 S[h2][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
                 for (int u = 0; u < UD; ++u) S[h2][j] = mfma_step<ET_BF16>(Kf[tt][h2][u], Qf[j][u], S[h2][j]);
             }
-        i32x4 Pf[2], Pl[2];
+        i32x4 Pf[JT], Pl[JT];
 #pragma unroll
-        for (int j = 0; j < 2; ++j) {
+        for (int j = 0; j < JT; ++j) {
             float x[8];
             float mt = -INFINITY;
 #pragma unroll
@@ -793,7 +798,7 @@ __global__ void __launch_bounds__(256) k_attn_bf16(const AttnArgs a, float scale
 #pragma unroll
         for (int dt = 0; dt < NDT; ++dt)
 #pragma unroll
-            for (int j = 0; j < 2; ++j) {
+            for (int j = 0; j < JT; ++j) {
                 O[dt][j] = mfma_step<ET_BF16>(Vf[tt][dt], Pf[j], O[dt][j]);
                 O[dt][j] = mfma_step<ET_BF16>(Vf[tt][dt], Pl[j], O[dt][j]);
             }
@@ -801,11 +806,11 @@ __global__ void __launch_bounds__(256) k_attn_bf16(const AttnArgs a, float scale
 
     // ---- merge the four waves: states to LDS, one barrier, then each
     // (row, 4 d) of the split is the wave-order sum of the rescaled states
-    __shared__ float sm_m[ATT_WAVES][2][16], sm_l[ATT_WAVES][2][16];
-    __shared__ __attribute__((aligned(16))) float sm_o[ATT_WAVES][2][16][RS];
+    __shared__ float sm_m[ATT_WAVES][JT][16], sm_l[ATT_WAVES][JT][16];
+    __shared__ __attribute__((aligned(16))) float sm_o[ATT_WAVES][JT][16][RS];
     if (g == 0) {
 #pragma unroll
-        for (int j = 0; j < 2; ++j) {
+        for (int j = 0; j < JT; ++j) {
             sm_m[wave][j][r] = m[j];
             sm_l[wave][j][r] = l[j];
         }
@@ -813,13 +818,13 @@ __global__ void __launch_bounds__(256) k_attn_bf16(const AttnArgs a, float scale
 #pragma unroll
     for (int dt = 0; dt < NDT; ++dt)
 #pragma unroll
-        for (int j = 0; j < 2; ++j) *(f32x4*)(&sm_o[wave][j][r][16 * dt + 4 * g]) = O[dt][j];
+        for (int j = 0; j < JT; ++j) *(f32x4*)(&sm_o[wave][j][r][16 * dt + 4 * g]) = O[dt][j];
     __syncthreads();
     constexpr int D4 = HD / 4;
-    for (int idx = threadIdx.x; idx < 2 * 16 * D4; idx += 256) {
+    for (int idx = threadIdx.x; idx < JT * 16 * D4; idx += 256) {
         const int j = idx / (16 * D4), rr = (idx / D4) & 15, d4 = (idx % D4) * 4;
-        const int t = (j ? t0[1] : t0[0]) + rr;
-        if (!(j ? tv[1] : tv[0]) || t >= T) continue;
+        const int t = t0[JT == 1 ? 0 : j] + rr;
+        if (!tv[JT == 1 ? 0 : j] || t >= T) continue;
         float mw[ATT_WAVES], M = -1e30f;
 #pragma unroll
         for (int w = 0; w < ATT_WAVES; ++w) {
@@ -834,7 +839,7 @@ __global__ void __launch_bounds__(256) k_attn_bf16(const AttnArgs a, float scale
             acc += *(const f32x4*)(&sm_o[w][j][rr][d4]) * f;
             L += sm_l[w][j][rr] * f;
         }
-        const size_t o = ((size_t)split * a.H + (j ? head[1] : head[0])) * T + t;
+        const size_t o = ((size_t)split * a.H + head[JT == 1 ? 0 : j]) * T + t;
         *(f32x4*)(a.part_o + o * HD + d4) = acc;
         if (d4 == 0) *(float2*)(a.part_ml + o * 2) = make_float2(M, L);
     }
@@ -949,15 +954,17 @@ hipError_t launch_attention(int atype, const AttnArgs& a, hipStream_t s) {
     }
     const int S = attention_splits(n_slots);
     const int G = a.H / a.Hkv, Tp = (a.T + 15) & ~15;
-    const int nct = G * Tp / 16, nrc = (nct + 1) / 2;
+    // one 16-row query tile per workgroup: twice the workgroups of two tiles,
+    // half the arithmetic on each one's critical path (K/V re-reads hit L2)
+    const int nct = G * Tp / 16, nrc = nct;
     if (a.ctx_cap % 32 || S > ATT_MAX_SPLITS) return hipErrorInvalidValue;
     const float scale_log2 = (1.0f / sqrtf((float)a.hd)) * 1.4426950408889634f;
     const dim3 mg((a.T + 15) / 16, a.H);
     if (a.hd == 128) {
-        hipLaunchKernelGGL(k_attn_bf16<128>, dim3(S, a.Hkv, nrc), dim3(256), 0, s, a, scale_log2);
+        hipLaunchKernelGGL((k_attn_bf16<128, 1>), dim3(S, a.Hkv, nrc), dim3(256), 0, s, a, scale_log2);
         hipLaunchKernelGGL(k_attn_merge<128>, mg, dim3(256), 0, s, a, S);
     } else if (a.hd == 64) {
-        hipLaunchKernelGGL(k_attn_bf16<64>, dim3(S, a.Hkv, nrc), dim3(256), 0, s, a, scale_log2);
+        hipLaunchKernelGGL((k_attn_bf16<64, 1>), dim3(S, a.Hkv, nrc), dim3(256), 0, s, a, scale_log2);
         hipLaunchKernelGGL(k_attn_merge<64>, mg, dim3(256), 0, s, a, S);
     } else {
         return hipErrorInvalidValue;
