@@ -845,59 +845,52 @@ __global__ void __launch_bounds__(256) k_attn_bf16(const AttnArgs a, float scale
     }
 }
 
-// Merge the KV splits of 16 query rows of one head: the split weights
-// exp2(m_s - M) / L of every row are formed once (all (row, split) pairs
-// loaded in parallel), then float4 runs of the partial outputs are summed in
-// split order.
+// Merge the KV splits of 16 query rows of one head.  Each thread owns one
+// (row, 4 d) item and merges the splits in split order with a running max
+// (online softmax), eight splits' (m, l) pairs and partial outputs loaded at
+// a time: a single round of loads for contexts up to 2048 slots.
 template <int HD>
 __global__ void __launch_bounds__(256) k_attn_merge(const AttnArgs a, int S) {
-    __shared__ float sm[16][ATT_MAX_SPLITS], sl[16][ATT_MAX_SPLITS], sw[16][ATT_MAX_SPLITS];
     const int h = blockIdx.y, t0 = blockIdx.x * 16, T = a.T;
-    for (int i = threadIdx.x; i < 16 * S; i += 256) {
-        const int rr = i / S, sp = i % S, t = min(t0 + rr, T - 1);
-        const float* ml = a.part_ml + (((size_t)sp * a.H + h) * T + t) * 2;
-        sm[rr][sp] = ml[0];
-        sl[rr][sp] = ml[1];
-    }
-    __syncthreads();
-    if (threadIdx.x < 16) {
-        const int rr = threadIdx.x;
-        float M = -1e30f;
-        for (int sp = 0; sp < S; ++sp) M = fmaxf(M, sm[rr][sp]);
-        float L = 0.f;
-        for (int sp = 0; sp < S; ++sp) {
-            const float w = exp2f(sm[rr][sp] - M);
-            sw[rr][sp] = w;
-            L += sl[rr][sp] * w;
-        }
-        const float inv = L > 0.f ? 1.f / L : 0.f;
-        for (int sp = 0; sp < S; ++sp) sw[rr][sp] *= inv;
-    }
-    __syncthreads();
     const int NTo = col_tiles(T);
-    const size_t sstride = (size_t)a.H * T * HD;
+    const size_t sstride = (size_t)a.H * T;  // rows between splits
     for (int idx = threadIdx.x; idx < 16 * (HD / 4); idx += 256) {
         const int rr = idx / (HD / 4), d4 = (idx % (HD / 4)) * 4, t = t0 + rr;
         if (t >= T) continue;
-        const float* po = a.part_o + ((size_t)h * T + t) * HD + d4;
-        float4 acc4 = make_float4(0.f, 0.f, 0.f, 0.f);
-        for (int sp = 0; sp < S; ++sp) {
-            const float4 v = *(const float4*)(po + sp * sstride);
-            const float w = sw[rr][sp];
-            acc4.x += v.x * w;
-            acc4.y += v.y * w;
-            acc4.z += v.z * w;
-            acc4.w += v.w * w;
+        const size_t row = (size_t)h * T + t;
+        float M = -1e30f, L = 0.f;
+        f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+        for (int s0 = 0; s0 < S; s0 += 8) {
+            float2 ml[8];
+            f32x4 po[8];
+#pragma unroll
+            for (int k = 0; k < 8; ++k) {
+                const size_t r = row + (size_t)min(s0 + k, S - 1) * sstride;
+                ml[k] = *(const float2*)(a.part_ml + r * 2);
+                po[k] = *(const f32x4*)(a.part_o + r * HD + d4);
+            }
+#pragma unroll
+            for (int k = 0; k < 8; ++k) {
+                if (s0 + k < S) {
+                    const float mn = fmaxf(M, ml[k].x);
+                    const float fo = exp2f(M - mn), fn = exp2f(ml[k].x - mn);
+                    acc = acc * fo + po[k] * fn;
+                    L = L * fo + ml[k].y * fn;
+                    M = mn;
+                }
+            }
         }
-        const int k = h * HD + d4;
+        const float inv = L > 0.f ? 1.f / L : 0.f;
+        acc *= inv;
+        const int kk = h * HD + d4;
         if (a.out_tiled) {
-            st4((uint16_t*)a.out, xt_off(t, k, NTo, 8), acc4.x, acc4.y, acc4.z, acc4.w);
+            st4((uint16_t*)a.out, xt_off(t, kk, NTo, 8), acc[0], acc[1], acc[2], acc[3]);
         } else {
-            uint16_t* o = (uint16_t*)a.out + (size_t)t * a.H * HD + k;
-            o[0] = f2bf(acc4.x);
-            o[1] = f2bf(acc4.y);
-            o[2] = f2bf(acc4.z);
-            o[3] = f2bf(acc4.w);
+            uint16_t* o = (uint16_t*)a.out + (size_t)t * a.H * HD + kk;
+            o[0] = f2bf(acc[0]);
+            o[1] = f2bf(acc[1]);
+            o[2] = f2bf(acc[2]);
+            o[3] = f2bf(acc[3]);
         }
     }
 }
