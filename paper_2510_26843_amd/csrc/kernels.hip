@@ -730,79 +730,73 @@ __global__ void __launch_bounds__(256) k_attn_bf16(const AttnArgs a, float scale
         }
     }
 
-    float m[JT], l[JT];
+    // all of the wave's tiles form one block: scores first, then a single
+    // softmax pass (no running rescale), then P V.  Slots past the context
+    // and masked slots get probability 0; a wave with no visible slot keeps
+    // m = -1e30, l = 0 and contributes nothing to the merge.
+    f32x4 S[ATT_TPW][2][JT];
 #pragma unroll
-    for (int j = 0; j < JT; ++j) {
-        m[j] = -1e30f;
-        l[j] = 0.f;
-    }
-    f32x4 O[NDT][JT];
-#pragma unroll
-    for (int dt = 0; dt < NDT; ++dt)
-#pragma unroll
-        for (int j = 0; j < JT; ++j) O[dt][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-#pragma unroll
-    for (int tt = 0; tt < ATT_TPW; ++tt) {
-        const int ti = tile0 + tt;
-        if (ti >= n_tiles) continue;
-        const int tb = ti * 32;
-        f32x4 S[2][JT];
+    for (int tt = 0; tt < ATT_TPW; ++tt)
 #pragma unroll
         for (int h2 = 0; h2 < 2; ++h2)
 #pragma unroll
             for (int j = 0; j < JT; ++j) {
-                S[h2][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+                S[tt][h2][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-                for (int u = 0; u < UD; ++u) S[h2][j] = mfma_step<ET_BF16>(Kf[tt][h2][u], Qf[j][u], S[h2][j]);
+                for (int u = 0; u < UD; ++u) S[tt][h2][j] = mfma_step<ET_BF16>(Kf[tt][h2][u], Qf[j][u], S[tt][h2][j]);
             }
-        i32x4 Pf[JT], Pl[JT];
+    float m[JT], l[JT];
+    i32x4 Pf[ATT_TPW][JT], Pl[ATT_TPW][JT];
 #pragma unroll
-        for (int j = 0; j < JT; ++j) {
-            float x[8];
-            float mt = -INFINITY;
+    for (int j = 0; j < JT; ++j) {
+        float x[ATT_TPW][8];
+        float mt = -INFINITY;
+#pragma unroll
+        for (int tt = 0; tt < ATT_TPW; ++tt)
 #pragma unroll
             for (int h2 = 0; h2 < 2; ++h2)
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
-                    const int slot = tb + 8 * g + 4 * h2 + i;
+                    const int slot = (tile0 + tt) * 32 + 8 * g + 4 * h2 + i;
                     const bool vis = slot < n_slots && (slot < Lc || anc_bit(an0[j], an1[j], slot - Lc));
-                    const float xv = vis ? S[h2][j][i] * scale_log2 : -INFINITY;
-                    x[4 * h2 + i] = xv;
+                    const float xv = vis ? S[tt][h2][j][i] * scale_log2 : -INFINITY;
+                    x[tt][4 * h2 + i] = xv;
                     mt = fmaxf(mt, xv);
                 }
-            mt = pair_max32(pair_max16(mt));
-            const float mn = fmaxf(m[j], mt);
-            const float alpha = exp2f(m[j] - mn);
-            float ps = 0.f;
+        const float mn = fmaxf(-1e30f, pair_max32(pair_max16(mt)));
+        float ps = 0.f;
+#pragma unroll
+        for (int tt = 0; tt < ATT_TPW; ++tt) {
             uint16_t pb[8], pl[8];
 #pragma unroll
             for (int e = 0; e < 8; ++e) {
-                const float p = exp2f(x[e] - mn);
+                const float p = exp2f(x[tt][e] - mn);
                 ps += p;
                 pb[e] = f2bf(p);
                 pl[e] = f2bf(p - bf2f(pb[e]));  // exact difference, rounded: p = hi + lo to ~2^-17
             }
-            ps = pair_sum32(pair_sum16(ps));
-            l[j] = l[j] * alpha + ps;
-            m[j] = mn;
-#pragma unroll
-            for (int dt = 0; dt < NDT; ++dt) O[dt][j] *= alpha;
-            Pf[j] = i32x4{(int)(pb[0] | ((uint32_t)pb[1] << 16)), (int)(pb[2] | ((uint32_t)pb[3] << 16)),
-                          (int)(pb[4] | ((uint32_t)pb[5] << 16)), (int)(pb[6] | ((uint32_t)pb[7] << 16))};
-            Pl[j] = i32x4{(int)(pl[0] | ((uint32_t)pl[1] << 16)), (int)(pl[2] | ((uint32_t)pl[3] << 16)),
-                          (int)(pl[4] | ((uint32_t)pl[5] << 16)), (int)(pl[6] | ((uint32_t)pl[7] << 16))};
+            Pf[tt][j] = i32x4{(int)(pb[0] | ((uint32_t)pb[1] << 16)), (int)(pb[2] | ((uint32_t)pb[3] << 16)),
+                              (int)(pb[4] | ((uint32_t)pb[5] << 16)), (int)(pb[6] | ((uint32_t)pb[7] << 16))};
+            Pl[tt][j] = i32x4{(int)(pl[0] | ((uint32_t)pl[1] << 16)), (int)(pl[2] | ((uint32_t)pl[3] << 16)),
+                              (int)(pl[4] | ((uint32_t)pl[5] << 16)), (int)(pl[6] | ((uint32_t)pl[7] << 16))};
         }
-        // P V with the probabilities as a two-term bf16 sum (hi + lo): the
-        // product carries them to fp32-level accuracy; V is exact in bf16
-#pragma unroll
-        for (int dt = 0; dt < NDT; ++dt)
-#pragma unroll
-            for (int j = 0; j < JT; ++j) {
-                O[dt][j] = mfma_step<ET_BF16>(Vf[tt][dt], Pf[j], O[dt][j]);
-                O[dt][j] = mfma_step<ET_BF16>(Vf[tt][dt], Pl[j], O[dt][j]);
-            }
+        l[j] = pair_sum32(pair_sum16(ps));
+        m[j] = mn;
     }
+    // P V with the probabilities as a two-term bf16 sum (hi + lo): the
+    // product carries them to fp32-level accuracy; V is exact in bf16
+    f32x4 O[NDT][JT];
+#pragma unroll
+    for (int dt = 0; dt < NDT; ++dt)
+#pragma unroll
+        for (int j = 0; j < JT; ++j) {
+            O[dt][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int tt = 0; tt < ATT_TPW; ++tt) {
+                O[dt][j] = mfma_step<ET_BF16>(Vf[tt][dt], Pf[tt][j], O[dt][j]);
+                O[dt][j] = mfma_step<ET_BF16>(Vf[tt][dt], Pl[tt][j], O[dt][j]);
+            }
+        }
 
     // ---- merge the four waves: states to LDS, one barrier, then each
     // (row, 4 d) of the split is the wave-order sum of the rescaled states
