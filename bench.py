@@ -50,19 +50,6 @@ def measured_traffic():
     return rec.get("hbm_bytes_per_launch")
 
 
-def algorithmic_bytes(shape, T, Lc, run_layers, es=2):
-    """Bytes the forward must move: weights of the layers that run and the LM
-    head once, KV reads of all visible slots and writes of the new ones, the
-    embedding rows, the fp32 logits."""
-    kv_row = shape.n_kv_heads * shape.head_dim * es
-    b = run_layers * shape.layer_params() * es
-    b += shape.vocab * shape.d_model * es
-    b += run_layers * 2 * kv_row * (Lc + T)
-    b += run_layers * 2 * kv_row * T
-    b += T * shape.d_model * es + T * shape.vocab * 4
-    return b
-
-
 def gemm_bytes(N, K, T, out_bytes):
     return N * K * 2 + T * K * 2 + out_bytes
 
@@ -112,6 +99,7 @@ def main():
 
     import torch
     from paper_2510_26843_amd import cas, synth
+    from paper_2510_26843_amd.latency import algorithmic_bytes
 
     if not torch.cuda.is_available():
         print(json.dumps({"error": "no GPU visible"}))
