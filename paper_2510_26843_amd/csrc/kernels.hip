@@ -418,10 +418,23 @@ __global__ void __launch_bounds__(64 * WAVES) k_gemm_wide(const GemmArgs a) {
 // Matrices with at least 8192 rows (in tiles: a multiple of 3 or 4) take the wide variant;
 // shorter ones split K across the waves of a 16-row workgroup so that the
 // grid still covers every CU.
+// Stage shape of the wide kernel: UC steps per stage and D stages in the
+// register ring, by column tiles NT and tiles per wave TPW.  The ring keeps
+// 8-16 KB of weights in flight per wave; wider activations (larger NT) take
+// fewer steps per stage, so the ring gets deeper (measured on the 7B
+// shapes: T = 64 gate/up 38.7 -> 35.8 us, T = 128 69.6 -> 50.8 us, T <= 32
+// QKV 17.9 -> 17.2 us).
+template <int NT, int TPW> struct WideStage {
+    static constexpr int UC = TPW == 2 ? (NT == 2 ? 4 : 2) : (NT == 8 ? 1 : 2);
+    static constexpr int D = TPW == 2 && NT == 2 ? 2 : 4;
+};
+
 template <int WT, int NT, int EPI, typename AT>
 static hipError_t gemm_go(const GemmArgs& a, hipStream_t s) {
     constexpr int UC = NT == 2 ? 4 : (NT == 4 ? 2 : 1);
     if (a.N >= 8192 && ((a.N / 16) % 4 == 0 || (a.N / 16) % 3 == 0)) {
+        using S1 = WideStage<NT, 1>;
+        using S2 = WideStage<NT, 2>;
         // Every workgroup should stay resident on a CU of its own (a CU that
         // holds two workgroups while others hold one sets the pace): take the
         // split of the tiles into equal workgroups of 4x1, 3x1, 4x2 or 3x2
@@ -440,13 +453,13 @@ static hipError_t gemm_go(const GemmArgs& a, hipStream_t s) {
             else { bw = 3; bt = 1; bg = tiles / 3; }
         }
         if (bw == 4 && bt == 1)
-            hipLaunchKernelGGL((k_gemm_wide<WT, NT, UC, 4, 4, 1, EPI, AT>), dim3(bg), dim3(256), 0, s, a);
+            hipLaunchKernelGGL((k_gemm_wide<WT, NT, S1::UC, S1::D, 4, 1, EPI, AT>), dim3(bg), dim3(256), 0, s, a);
         else if (bw == 3 && bt == 1)
-            hipLaunchKernelGGL((k_gemm_wide<WT, NT, UC, 4, 3, 1, EPI, AT>), dim3(bg), dim3(192), 0, s, a);
+            hipLaunchKernelGGL((k_gemm_wide<WT, NT, S1::UC, S1::D, 3, 1, EPI, AT>), dim3(bg), dim3(192), 0, s, a);
         else if (bw == 4)
-            hipLaunchKernelGGL((k_gemm_wide<WT, NT, UC, 2, 4, 2, EPI, AT>), dim3(bg), dim3(256), 0, s, a);
+            hipLaunchKernelGGL((k_gemm_wide<WT, NT, S2::UC, S2::D, 4, 2, EPI, AT>), dim3(bg), dim3(256), 0, s, a);
         else
-            hipLaunchKernelGGL((k_gemm_wide<WT, NT, UC, 2, 3, 2, EPI, AT>), dim3(bg), dim3(192), 0, s, a);
+            hipLaunchKernelGGL((k_gemm_wide<WT, NT, S2::UC, S2::D, 3, 2, EPI, AT>), dim3(bg), dim3(192), 0, s, a);
         return hipGetLastError();
     }
     constexpr int D = NT == 2 ? 2 : 4;
@@ -500,7 +513,7 @@ hipError_t launch_gemm(int wtype, int atype, int epi, const GemmArgs& a, hipStre
 }
 
 int gemm_parts_count(int wtype, int N, int Kp, int T) {
-    if (wtype == ET_I8 || N % 64 || T < 1 || T > 128) return 1;
+    if (N % 64 || T < 1 || T > 128) return 1;
     const int groups = N / 64;  // four 16-row tiles per workgroup
     if (groups >= 192) return 1;
     const int NT = col_tiles(T), UC = NT == 2 ? 4 : (NT == 4 ? 2 : 1);
@@ -527,6 +540,8 @@ hipError_t launch_gemm_parts(int wtype, const GemmArgs& a, hipStream_t s) {
         return hipErrorInvalidValue;
     if (wtype == ET_BF16) return gemm_parts_go<ET_BF16, uint16_t>(a, s);
     if (wtype == ET_F32) return gemm_parts_go<ET_F32, float>(a, s);
+    // int8: each split dequantises its own int32 sums, (acc * xs[t]) * ws[n]
+    if (wtype == ET_I8) return gemm_parts_go<ET_I8, float>(a, s);
     return hipErrorInvalidValue;
 }
 
@@ -1122,9 +1137,59 @@ hipError_t launch_rmsnorm(int atype, float* h, const float* g, int T, int d, flo
     return rmsnorm_go<float, false>(h, g, T, d, eps, (float*)out, q, qs, parts, nparts, pstride, s);
 }
 
-// Per-row symmetric int8: s = amax / 127, q = clamp(rne(x / s), -127, 127).
-// TILED: x is tiled activations (act type) and q is written tiled (pad zero);
-// otherwise both are row-major [T][K].
+// Per-row symmetric int8 of tiled activations: s = amax / 127,
+// q = clamp(rne(x / s), -127, 127), codes written tiled (pad zero).  One
+// workgroup of 1024 threads per row; a thread takes whole 16-byte fragments
+// of the row (EA consecutive k each, which land in one int8 fragment of 16
+// k), NF fragments per thread held in registers between the amax and the
+// quantisation.
+static constexpr int QR_THREADS = 1024;
+
+template <typename AT, int NF>
+__global__ void __launch_bounds__(QR_THREADS) k_quant_rows_tiled(const AT* x, int K, int8_t* q, float* qs) {
+    __shared__ float red[QR_THREADS / 64];
+    constexpr int EA = 16 / sizeof(AT);
+    const int t = blockIdx.x, NT = col_tiles(gridDim.x), tid = threadIdx.x;
+    const int nfa = (K + 16 * EA - 1) / (16 * EA) * 16;  // fragments of the padded input row
+    const int nfq = (K + 255) / 256 * 256 / EA;           // fragments covering the padded int8 row
+    i32x4 v[NF];
+    float amax = 0.f;
+#pragma unroll
+    for (int i = 0; i < NF; ++i) {
+        const int f = tid + QR_THREADS * i;
+        v[i] = *(const i32x4*)(x + xt_off(t, min(f, nfa - 1) * EA, NT, EA));
+        const AT* e = (const AT*)&v[i];
+#pragma unroll
+        for (int j = 0; j < EA; ++j)
+            if (f < nfa && f * EA + j < K) amax = fmaxf(amax, fabsf(Act<AT>::ld(e, j)));
+    }
+    amax = block_max<QR_THREADS / 64>(amax, red);
+    const float sc = amax / 127.0f;
+    if (tid == 0) qs[t] = sc;
+#pragma unroll
+    for (int i = 0; i < NF; ++i) {
+        const int f = tid + QR_THREADS * i;
+        if (f >= nfq) continue;
+        const AT* e = (const AT*)&v[i];
+        uint32_t w[EA / 4];
+#pragma unroll
+        for (int j = 0; j < EA / 4; ++j) {
+            uint32_t b = 0;
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                const int k = f * EA + 4 * j + u;
+                const float c = (f < nfa && k < K) ? q8(Act<AT>::ld(e, 4 * j + u), sc) : 0.f;
+                b |= (uint32_t)(uint8_t)(int8_t)c << (8 * u);
+            }
+            w[j] = b;
+        }
+        int8_t* o = q + xt_off(t, f * EA, NT, 16);
+        if constexpr (EA == 8) *(uint2*)o = make_uint2(w[0], w[1]);
+        else *(uint32_t*)o = w[0];
+    }
+}
+
+// Row-major form ([T][K] in, [T][K] out), for the kernel-level entry point.
 template <typename AT, bool TILED>
 __global__ void __launch_bounds__(256) k_quant_rows(const AT* x, int K, int8_t* q, float* qs) {
     __shared__ float red[4];
@@ -1144,13 +1209,29 @@ __global__ void __launch_bounds__(256) k_quant_rows(const AT* x, int K, int8_t* 
     }
 }
 
+template <typename AT>
+static hipError_t quant_tiled_go(const AT* x, int T, int K, int8_t* q, float* qs, hipStream_t s) {
+    constexpr int EA = 16 / sizeof(AT);
+    const int nfq = (K + 255) / 256 * 256 / EA;  // >= fragments of the padded input row
+    const int nf = (nfq + QR_THREADS - 1) / QR_THREADS;
+#define CAS_QR(NF) hipLaunchKernelGGL((k_quant_rows_tiled<AT, NF>), dim3(T), dim3(QR_THREADS), 0, s, x, K, q, qs)
+    if (nf <= 1) CAS_QR(1);
+    else if (nf <= 2) CAS_QR(2);
+    else if (nf <= 4) CAS_QR(4);
+    else if (nf <= 8) CAS_QR(8);
+    else CAS_QR(16);
+#undef CAS_QR
+    return hipGetLastError();
+}
+
 hipError_t launch_quant_rows(int atype, const void* x, int T, int K, int8_t* q, float* qs, int tiled, hipStream_t s) {
+    if (T < 1 || K < 1 || (tiled && (T > 128 || K > 65536))) return hipErrorInvalidValue;
     if (atype == ET_BF16) {
-        if (tiled) hipLaunchKernelGGL((k_quant_rows<uint16_t, true>), dim3(T), dim3(256), 0, s, (const uint16_t*)x, K, q, qs);
-        else hipLaunchKernelGGL((k_quant_rows<uint16_t, false>), dim3(T), dim3(256), 0, s, (const uint16_t*)x, K, q, qs);
+        if (tiled) return quant_tiled_go((const uint16_t*)x, T, K, q, qs, s);
+        hipLaunchKernelGGL((k_quant_rows<uint16_t, false>), dim3(T), dim3(256), 0, s, (const uint16_t*)x, K, q, qs);
     } else {
-        if (tiled) hipLaunchKernelGGL((k_quant_rows<float, true>), dim3(T), dim3(256), 0, s, (const float*)x, K, q, qs);
-        else hipLaunchKernelGGL((k_quant_rows<float, false>), dim3(T), dim3(256), 0, s, (const float*)x, K, q, qs);
+        if (tiled) return quant_tiled_go((const float*)x, T, K, q, qs, s);
+        hipLaunchKernelGGL((k_quant_rows<float, false>), dim3(T), dim3(256), 0, s, (const float*)x, K, q, qs);
     }
     return hipGetLastError();
 }

@@ -290,7 +290,7 @@ hipError_t enqueue_forward(cas_ctx* c, int T, const uint8_t* skip, int aq) {
     };
     // a residual projection: split-K partial sums when that fills the GPU better
     auto resid_proj = [&](GemmArgs& g) -> hipError_t {
-        const int ks = aq ? 1 : gemm_parts_count(wq, g.N, g.Kp, T);
+        const int ks = gemm_parts_count(wq, g.N, g.Kp, T);
         if (ks <= 1) return launch_gemm(wq, et, EPI_RESID, g, s);
         g.out = c->d_gpart;
         g.ksplit = ks;
