@@ -159,6 +159,11 @@ def _attention_case(H, Hkv, hd, Lc, parents, seed):
     (2, 2, 128, 0, ((), 1)),
     (4, 2, 128, 300, ((2,) * 7, 128)),
     (8, 8, 64, 129, ((4, 4, 4), 20)),
+    # several 16-row query tiles per workgroup sharing one load of K/V
+    # (GQA 4:1, 64 nodes, 9 KV splits: 3 tiles per workgroup, the last
+    # workgroup of each head group with one), and an MHA 128-node tree
+    (32, 8, 128, 2000, ((4, 4, 4, 4), 64)),
+    (8, 8, 128, 3000, ((2,) * 7, 128)),
 ])
 def test_attention_tree_mask(H, Hkv, hd, Lc, tree):
     parents = synth.tree_from_branching(*tree) if tree[0] else [-1]
