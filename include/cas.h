@@ -162,6 +162,20 @@ cas_status cas_accept_tree(cas_ctx* ctx, int32_t greedy, int32_t* accepted,
                            int32_t* n_accepted, int32_t* bonus_token);
 
 /*
+ * Draft candidates of the last forward (verify or draft): for each of its n
+ * rows, the K tokens of highest logit (decreasing logit, lower id on ties;
+ * id -1 and probability 0 past the row's finite entries) and their softmax
+ * probabilities over the whole vocabulary, p = exp(l - max) / sum exp(l_v -
+ * max) in fp32 (Alg. 1: the K candidates y[i, :] of a drafted position;
+ * Sec. 4.2 "Token-Level Information": the normalised probability of a
+ * drafted token).  n must equal the last forward's row count; ids and probs
+ * are host arrays of n*K (row-major); K in [1, 16].  Only n*K pairs cross
+ * PCIe, not the n x vocab logits.  NaN logits give CAS_ERR_DEVICE.
+ * Synchronous.
+ */
+cas_status cas_topk(cas_ctx* ctx, int32_t n, int32_t K, int32_t* ids, float* probs);
+
+/*
  * Commit an accepted root path of the verified round: accepted[j] must be the
  * root for j = 0 and a child of accepted[j-1] otherwise.  Node accepted[j]
  * moves from slot Lc+accepted[j] to slot Lc+j in every layer; then
@@ -187,7 +201,7 @@ typedef enum {
     CAS_K_EMBED = 0, CAS_K_RMSNORM = 1, CAS_K_GEMM_QKV = 2, CAS_K_ATTN = 3,
     CAS_K_GEMM_O = 4, CAS_K_GEMM_GATEUP = 5, CAS_K_GEMM_DOWN = 6,
     CAS_K_GEMM_HEAD = 7, CAS_K_QUANT = 8, CAS_K_ACCEPT = 9, CAS_K_COMPACT = 10,
-    CAS_K_COUNT = 11
+    CAS_K_TOPK = 11, CAS_K_COUNT = 12
 } cas_kclass;
 cas_status cas_profile(cas_ctx* ctx, int32_t enable);
 cas_status cas_profile_read(cas_ctx* ctx, double* ms, int32_t* launches, int32_t reset);

@@ -26,12 +26,12 @@ EPI_STORE, EPI_RESID, EPI_RAW_I32 = 0, 1, 2
 TENSOR = {"embed": 0, "lm_head": 1, "final_norm": 2, "attn_norm": 3, "ffn_norm": 4, "wq": 5, "wk": 6,
           "wv": 7, "wo": 8, "w_gate": 9, "w_up": 10, "w_down": 11}
 KCLASS = ["embed", "rmsnorm", "gemm_qkv", "attn", "gemm_o", "gemm_gateup", "gemm_down", "gemm_head", "quant",
-          "accept", "compact"]
+          "accept", "compact", "topk"]
 
 # every symbol the two headers declare
 EXPORTS = ("cas_create", "cas_destroy", "cas_last_error", "cas_create_error", "cas_load_tensor", "cas_build_int8",
            "cas_prefill", "cas_kv_load", "cas_kv_read", "cas_set_committed", "cas_committed_len", "cas_forward",
-           "cas_logits_device", "cas_accept_tree", "cas_kv_compact", "cas_tree_info", "cas_set_graphs",
+           "cas_logits_device", "cas_accept_tree", "cas_topk", "cas_kv_compact", "cas_tree_info", "cas_set_graphs",
            "cas_profile", "cas_profile_read", "cas_sync", "cas_op_gemm", "cas_op_gemm_work_bytes",
            "cas_op_quant_rows", "cas_op_quant_weight", "cas_op_quant_weight_work_bytes", "cas_op_attention",
            "cas_op_attention_work_bytes", "cas_op_copy")
@@ -75,6 +75,7 @@ def lib():
             "cas_logits_device": ([P, P, P], I),
             "cas_accept_tree": ([P, I, P, P, P], I),
             "cas_kv_compact": ([P, P, I], I),
+            "cas_topk": ([P, I, I, P, P], I),
             "cas_tree_info": ([P, I, P, P], I),
             "cas_set_graphs": ([P, I], I),
             "cas_profile": ([P, I], I),
@@ -223,6 +224,14 @@ class Model:
         b = ctypes.c_int32()
         self._chk(lib().cas_accept_tree(self.h, 1, _p(self._acc), ctypes.byref(n), ctypes.byref(b)))
         return [int(x) for x in self._acc[: n.value]], int(b.value)
+
+    def topk(self, K: int, n: int) -> Tuple[np.ndarray, np.ndarray]:
+        """Top-K token ids and their softmax probabilities for the n rows of
+        the last forward ([n][K] int32 and float32)."""
+        ids = np.zeros((n, K), dtype=np.int32)
+        probs = np.zeros((n, K), dtype=np.float32)
+        self._chk(lib().cas_topk(self.h, int(n), int(K), _p(ids), _p(probs)))
+        return ids, probs
 
     def compact(self, accepted: Sequence[int]) -> None:
         a = np.ascontiguousarray(accepted, dtype=np.int32)

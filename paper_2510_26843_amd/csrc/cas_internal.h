@@ -173,6 +173,10 @@ hipError_t launch_embed(int atype, const void* embed, int d, const int* round_to
 // result: [0] = n_accepted, [1] = bonus token, [2] = NaN flag, [3..] = node ids.
 hipError_t launch_accept(const float* logits, int T, int V, const int* round_tokens, const int* round_parent,
                          int* argmax_buf, int* result, hipStream_t s);
+// Top-K ids (value descending, lower id on ties; -1 past the finite
+// entries) and softmax probabilities of each of n logits rows [n][V]; K in
+// [1, 16]; flag[row] set to 1 when the row holds a NaN (not cleared here).
+hipError_t launch_topk(const float* logits, int n, int V, int K, int* ids, float* probs, int* flag, hipStream_t s);
 // Move accepted slots Lc+acc[j] -> Lc+j in every layer (K and V caches).
 hipError_t launch_compact(int atype, void* kc, void* vt, int L, int Hkv, int hd, int ctx_cap,
                           const StepParams* sp, const int* accepted, int n_acc, hipStream_t s);

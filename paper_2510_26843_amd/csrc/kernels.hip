@@ -340,10 +340,12 @@ __global__ void __launch_bounds__(64 * WAVES) k_gemm_wide(const GemmArgs a) {
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int tile0 = (blockIdx.x * WAVES + wave) * TPW;
     const int C = a.Kp / (16 * E);
-    // stages of this workgroup: the whole K range, or split gridDim.y ways
-    const int NS_all = C * (FRAG_U / UC);
-    const int s0 = (int)(((long)blockIdx.y * NS_all) / gridDim.y);
-    const int NS = (int)(((long)(blockIdx.y + 1) * NS_all) / gridDim.y) - s0;
+    // stages of this workgroup: the whole K range, or split gridDim.y ways at
+    // chunk boundaries, so the K ranges (and every row's summation order) do
+    // not depend on the stage width, which changes with the column tiles
+    const int c0 = (int)(((long)blockIdx.y * C) / gridDim.y);
+    const int c1 = (int)(((long)(blockIdx.y + 1) * C) / gridDim.y);
+    const int s0 = c0 * (FRAG_U / UC), NS = (c1 - c0) * (FRAG_U / UC);
     const char* wb = (const char*)a.W + ((size_t)tile0 * C * FRAG_U * 64 + lane) * 16 + (size_t)s0 * UC * 1024;
     const size_t tstride = (size_t)C * FRAG_U * 1024;  // bytes of one tile
     const char* xb = (const char*)a.X + (size_t)lane * 16 + (size_t)s0 * NB * 1024;
@@ -512,14 +514,16 @@ hipError_t launch_gemm(int wtype, int atype, int epi, const GemmArgs& a, hipStre
     return hipErrorInvalidValue;
 }
 
+// The split count depends on the matrix only, never on T, so a row's sums
+// are the same for every tree size (greedy speculative output then equals
+// greedy decoding bit for bit, not only up to near-ties).
 int gemm_parts_count(int wtype, int N, int Kp, int T) {
     if (N % 64 || T < 1 || T > 128) return 1;
     const int groups = N / 64;  // four 16-row tiles per workgroup
     if (groups >= 192) return 1;
-    const int NT = col_tiles(T), UC = NT == 2 ? 4 : (NT == 4 ? 2 : 1);
-    const int NS = Kp / chunk_k(wtype) * (FRAG_U / UC);
+    const int C = Kp / chunk_k(wtype);
     int ks = std::min(8, 256 / groups);
-    ks = std::min(ks, NS / 2);
+    ks = std::min(ks, C / 2);
     return ks >= 2 ? ks : 1;
 }
 
@@ -1326,6 +1330,120 @@ hipError_t launch_embed(int atype, const void* embed, int d, const int* rtok, co
     else
         hipLaunchKernelGGL(k_embed<float>, dim3(T), dim3(256), 0, s, (const float*)embed, d, rtok, rpar, sp, h,
                            row_pos, row_slot, row_anc);
+    return hipGetLastError();
+}
+
+// ---------------------------------------------------------------- draft top-K
+
+// Top-K tokens of one logits row per workgroup with their softmax
+// probabilities over the whole vocabulary (the K candidates of a drafted
+// position and their normalised probabilities, Alg. 1 and Sec. 4.2
+// "Token-Level Information").  Each of the 1024 threads scans a strided
+// slice of the row keeping its KL best (value descending, index ascending on
+// ties) in a sorted register list, and an online (max, sum of exp) pair.
+// The workgroup then pops the best list head K times (workgroup argmax over
+// the heads, by value then lower index) and combines the (max, sum) pairs:
+// lanes by a fixed butterfly, waves in wave order.  NaN entries are skipped
+// and reported in flag.
+static constexpr int TOPK_THREADS = 1024;
+
+__device__ __forceinline__ bool tk_better(float a, int ia, float b, int ib) {
+    return a > b || (a == b && ia < ib);
+}
+__device__ __forceinline__ void ms_combine(float& m, float& s, float m2, float s2) {
+    const float M = fmaxf(m, m2);
+    s = (m == -INFINITY ? 0.f : s * __expf(m - M)) + (m2 == -INFINITY ? 0.f : s2 * __expf(m2 - M));
+    m = M;
+}
+
+template <int KL>
+__global__ void __launch_bounds__(TOPK_THREADS) k_topk(const float* logits, int V, int K, int* ids, float* probs,
+                                                       int* flag) {
+    __shared__ float sh_v[TOPK_THREADS / 64], sh_m[TOPK_THREADS / 64], sh_s[TOPK_THREADS / 64];
+    __shared__ int sh_i[TOPK_THREADS / 64];
+    const int row = blockIdx.x, tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+    const float* x = logits + (size_t)row * V;
+    float lv[KL];
+    int li[KL];
+#pragma unroll
+    for (int k = 0; k < KL; ++k) { lv[k] = -INFINITY; li[k] = 0x7fffffff; }
+    float m = -INFINITY, s = 0.f;
+    int nan = 0;
+    for (int v = tid; v < V; v += TOPK_THREADS) {
+        const float y = x[v];
+        if (y != y) { nan = 1; continue; }
+        if (y > m) { s = (m == -INFINITY ? 0.f : s * __expf(m - y)) + 1.f; m = y; }
+        else s += __expf(y - m);
+        if (tk_better(y, v, lv[KL - 1], li[KL - 1])) {
+            // insert into the sorted list: shift the worse entries down
+            float cv = y;
+            int ci = v;
+#pragma unroll
+            for (int k = 0; k < KL; ++k) {
+                if (tk_better(cv, ci, lv[k], li[k])) {
+                    const float tv = lv[k];
+                    const int ti = li[k];
+                    lv[k] = cv; li[k] = ci;
+                    cv = tv; ci = ti;
+                }
+            }
+        }
+    }
+    // softmax normaliser of the row
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+        const float m2 = __shfl_xor(m, o), s2 = __shfl_xor(s, o);
+        ms_combine(m, s, m2, s2);
+    }
+    for (int o = 1; o < 64; o <<= 1) nan |= __shfl_xor(nan, o);
+    if (lane == 0) { sh_m[w] = m; sh_s[w] = s; sh_i[w] = nan; }
+    __syncthreads();
+    float M = sh_m[0], S = sh_s[0];
+    nan = sh_i[0];
+    for (int k = 1; k < TOPK_THREADS / 64; ++k) {
+        ms_combine(M, S, sh_m[k], sh_s[k]);
+        nan |= sh_i[k];
+    }
+    __syncthreads();
+    // K rounds of workgroup argmax over the list heads
+    for (int r = 0; r < K; ++r) {
+        float bv = lv[0];
+        int bi = li[0];
+#pragma unroll
+        for (int o = 32; o >= 1; o >>= 1) {
+            const float ov = __shfl_xor(bv, o);
+            const int oi = __shfl_xor(bi, o);
+            if (tk_better(ov, oi, bv, bi)) { bv = ov; bi = oi; }
+        }
+        if (lane == 0) { sh_v[w] = bv; sh_i[w] = bi; }
+        __syncthreads();
+        bv = sh_v[0];
+        bi = sh_i[0];
+        for (int k = 1; k < TOPK_THREADS / 64; ++k)
+            if (tk_better(sh_v[k], sh_i[k], bv, bi)) { bv = sh_v[k]; bi = sh_i[k]; }
+        __syncthreads();
+        if (tid == 0) {
+            const bool ok = bi != 0x7fffffff;  // fewer than K finite entries: id -1, probability 0
+            ids[(size_t)row * K + r] = ok ? bi : -1;
+            probs[(size_t)row * K + r] = ok && S > 0.f ? __expf(bv - M) / S : 0.f;
+        }
+        if (li[0] == bi) {  // the owner pops its head (ids are unique within a row)
+#pragma unroll
+            for (int k = 0; k + 1 < KL; ++k) { lv[k] = lv[k + 1]; li[k] = li[k + 1]; }
+            lv[KL - 1] = -INFINITY;
+            li[KL - 1] = 0x7fffffff;
+        }
+    }
+    if (tid == 0 && nan) flag[row] = 1;
+}
+
+hipError_t launch_topk(const float* logits, int n, int V, int K, int* ids, float* probs, int* flag, hipStream_t s) {
+    if (n < 1 || V < 1 || K < 1 || K > 16) return hipErrorInvalidValue;
+    if (K <= 1) hipLaunchKernelGGL(k_topk<1>, dim3(n), dim3(TOPK_THREADS), 0, s, logits, V, K, ids, probs, flag);
+    else if (K <= 2) hipLaunchKernelGGL(k_topk<2>, dim3(n), dim3(TOPK_THREADS), 0, s, logits, V, K, ids, probs, flag);
+    else if (K <= 4) hipLaunchKernelGGL(k_topk<4>, dim3(n), dim3(TOPK_THREADS), 0, s, logits, V, K, ids, probs, flag);
+    else if (K <= 8) hipLaunchKernelGGL(k_topk<8>, dim3(n), dim3(TOPK_THREADS), 0, s, logits, V, K, ids, probs, flag);
+    else hipLaunchKernelGGL(k_topk<16>, dim3(n), dim3(TOPK_THREADS), 0, s, logits, V, K, ids, probs, flag);
     return hipGetLastError();
 }
 

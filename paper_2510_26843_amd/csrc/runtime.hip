@@ -97,6 +97,8 @@ struct cas_ctx {
     int* d_result = nullptr;
     int* d_acc = nullptr;
     int* h_result = nullptr;  // pinned
+    int* d_topk = nullptr;    // [max_tree][16] ids, [max_tree][16] probabilities, [max_tree] NaN flags
+    int* h_topk = nullptr;    // pinned copy of the same
 
     Stage stage[kStages];
     int stage_i = 0;
@@ -544,6 +546,7 @@ void free_ctx(cas_ctx* c) {
         if (s.host) (void)hipHostFree(s.host);
     }
     if (c->h_result) (void)hipHostFree(c->h_result);
+    if (c->h_topk) (void)hipHostFree(c->h_topk);
     for (void* p : c->allocs) (void)hipFree(p);
     if (c->own_stream && c->stream) (void)hipStreamDestroy(c->stream);
     delete c;
@@ -691,10 +694,13 @@ cas_status cas_create(const cas_config* cfg, int device, void* stream, cas_ctx**
     ALLOC(c->d_gpart, sizeof(float) * 8 * (size_t)f.max_tree * f.d_model);
     ALLOC(c->d_gbuf, T * 8 * 3 * 4);  // per row: 8 argmax parts of (index, value, NaN flag)
     ALLOC(c->d_result, (T + 4) * 4);
+    ALLOC(c->d_topk, T * (16 + 16 + 1) * 4);
     ALLOC(c->d_acc, (T + 1) * 4);
     if (hipMemset(c->d_rtok, 0, T * 4) != hipSuccess || hipMemset(c->d_rpar, 0xff, T * 4) != hipSuccess)
         return cleanup(CAS_ERR_DEVICE, "hipMemset of the round arrays");
     if (hipHostMalloc((void**)&c->h_result, (T + 4) * 4, hipHostMallocDefault) != hipSuccess)
+        return cleanup(CAS_ERR_OOM, "hipHostMalloc");
+    if (hipHostMalloc((void**)&c->h_topk, T * (16 + 16 + 1) * 4, hipHostMallocDefault) != hipSuccess)
         return cleanup(CAS_ERR_OOM, "hipHostMalloc");
     for (auto& s : c->stage) {
         if (hipHostMalloc((void**)&s.host, kStageBytes, hipHostMallocDefault) != hipSuccess)
@@ -906,6 +912,36 @@ cas_status cas_accept_tree(cas_ctx* c, int32_t greedy, int32_t* accepted, int32_
     for (int j = 0; j < na; ++j) accepted[j] = c->h_result[3 + j];
     *n_accepted = na;
     *bonus = c->h_result[1];
+    return CAS_OK;
+}
+
+cas_status cas_topk(cas_ctx* c, int32_t n, int32_t K, int32_t* ids, float* probs) {
+    if (!c) return CAS_ERR_ARG;
+    if (K < 1 || K > 16) return fail(c, CAS_ERR_ARG, "K must be in [1, 16]");
+    if (!ids || !probs) return fail(c, CAS_ERR_ARG, "output pointers must not be NULL");
+    if (c->logits_rows < 1) return fail(c, CAS_ERR_STATE, "cas_topk needs a forward first");
+    if (n != c->logits_rows)
+        return fail(c, CAS_ERR_ARG, "n must equal the last forward's row count " + std::to_string(c->logits_rows));
+    const int cap = c->cfg.max_tree;
+    int* d_ids = c->d_topk;
+    float* d_p = (float*)(c->d_topk + (size_t)cap * 16);
+    int* d_flag = c->d_topk + (size_t)cap * 32;
+    HIPCHK(c, hipMemsetAsync(d_flag, 0, sizeof(int) * (size_t)n, c->stream));
+    hipError_t e = timed(c, CAS_K_TOPK, [&]() -> hipError_t {
+        return launch_topk(c->d_logits, n, c->cfg.vocab, K, d_ids, d_p, d_flag, c->stream);
+    });
+    if (e != hipSuccess) return hip_fail(c, e, "top-K launch");
+    int* h_ids = c->h_topk;
+    float* h_p = (float*)(c->h_topk + (size_t)cap * 16);
+    int* h_flag = c->h_topk + (size_t)cap * 32;
+    HIPCHK(c, hipMemcpyAsync(h_ids, d_ids, sizeof(int) * (size_t)n * K, hipMemcpyDeviceToHost, c->stream));
+    HIPCHK(c, hipMemcpyAsync(h_p, d_p, sizeof(float) * (size_t)n * K, hipMemcpyDeviceToHost, c->stream));
+    HIPCHK(c, hipMemcpyAsync(h_flag, d_flag, sizeof(int) * (size_t)n, hipMemcpyDeviceToHost, c->stream));
+    HIPCHK(c, hipStreamSynchronize(c->stream));
+    for (int i = 0; i < n; ++i)
+        if (h_flag[i]) return fail(c, CAS_ERR_DEVICE, "NaN in the logits of row " + std::to_string(i));
+    memcpy(ids, h_ids, sizeof(int) * (size_t)n * K);
+    memcpy(probs, h_p, sizeof(float) * (size_t)n * K);
     return CAS_OK;
 }
 

@@ -312,3 +312,27 @@ def test_validation_errors_leave_state_unchanged(weights):
     g.compact(path)
     assert g.committed == 40 + len(path)
     g.close()
+
+
+@pytest.mark.parametrize("name", ["tiny", "mha_small"])
+def test_root_row_is_bit_identical_for_every_tree_size(weights, name):
+    """The verify kernels reduce every row in an order that does not depend on
+    how many rows the call has: split-K ranges are chunk-aligned and the split
+    count depends on the matrix only; the attention of the root sees the same
+    slots.  So the root's logits are the same bits for T = 1 (plain greedy
+    decoding) and for trees of 2, 4 and 8 column tiles, which makes greedy
+    speculative output equal greedy decoding exactly.  The MHA shape has
+    down-projection chunks (22) that its split count (8) does not divide."""
+    shape = {"tiny": TINY, "mha_small": MHA}[name]
+    g = cas.Model(shape, max_ctx=512)
+    g.load_weights(weights[name])
+    prompt = [int(x) for x in synth.gen_prompt(shape.vocab, 50, seed=5)]
+    g.prefill(prompt[:-1])
+    rows = []
+    for T in (1, 7, 33, 70):
+        parents = synth.balanced_tree(T)
+        toks = synth.gen_tree_tokens(parents, shape.vocab, seed=T, root_token=prompt[-1])
+        rows.append(g.forward(toks, parents, 0)[0].copy())
+    for r in rows[1:]:
+        assert np.array_equal(r.view(np.uint32), rows[0].view(np.uint32))
+    g.close()
