@@ -173,16 +173,18 @@ def pld_propose(seq: Sequence[int], k: int, n_max: int = 3, n_min: int = 1) -> T
     recent earlier occurrence of the last n tokens of seq; propose the (up
     to k) tokens that followed it.  Returns (tokens, n); ([], 0) when no
     n-gram recurs.  The match length n is the draft's token-level
-    confidence (Sec. 4.2)."""
-    L = len(seq)
-    s = list(seq)
+    confidence (Sec. 4.2).  The search is vectorised over start positions."""
+    a = np.asarray(seq, dtype=np.int64)
+    L = a.shape[0]
     for n in range(min(n_max, L - 1), n_min - 1, -1):
-        tail = s[L - n:]
-        for start in range(L - n - 1, -1, -1):
-            if s[start:start + n] == tail:
-                nxt = s[start + n:start + n + k]
-                if nxt:
-                    return nxt, n
+        S = L - n  # candidate starts 0 .. L-n-1 (the last n tokens themselves excluded)
+        hit = np.ones(S, dtype=bool)
+        for j in range(n):
+            hit &= a[j:j + S] == a[L - n + j]
+        idx = np.flatnonzero(hit)
+        if idx.size:
+            start = int(idx[-1])
+            return [int(x) for x in a[start + n:start + n + k]], n
     return [], 0
 
 
@@ -373,6 +375,7 @@ def build_tree(backend, root_token: int, context: Sequence[int], configs: Sequen
                n_layers: int, stats: Optional[Dict] = None) -> DraftTree:
     """Alg. 1: grow the draft tree of one round (readings R1-R6 above)."""
     tree = DraftTree(root_token)
+    ctx = np.asarray(context, dtype=np.int64)
     by_name = {c.name: c for c in configs}
     a_n, c_n = est.alpha(bottom.name), cost[bottom.name]
     M = params.max_tree
@@ -386,7 +389,7 @@ def build_tree(backend, root_token: int, context: Sequence[int], configs: Sequen
         lookup: List[int] = []
         for c in configs:
             if c.pld:
-                seq = list(context) + [tree.nodes[i].token for i in tree.path(leaf)]
+                seq = np.concatenate([ctx, np.array([tree.nodes[i].token for i in tree.path(leaf)], dtype=np.int64)])
                 lookup, _ = pld_propose(seq, params.k_max, params.pld_n_max)
                 if lookup:
                     cands[c.name] = (est.alpha(c.name), cost[c.name])
@@ -458,11 +461,14 @@ def cas_decode_dytc(backend, prompt: Sequence[int], n_new: int, configs: Sequenc
     the acceptance estimates take the round's first-token outcomes.  The
     output equals greedy autoregressive decoding (Sec. 5.1)."""
     backend.reset(prompt)
-    seq = list(prompt)
+    # the sequence so far, kept in one buffer (the context prompt lookup scans)
+    seq = np.empty(len(prompt) + n_new + params.max_tree + 1, dtype=np.int64)
+    seq[:len(prompt)] = prompt
+    n_seq = len(prompt)
     out: List[int] = []
     root = int(prompt[-1])
     while len(out) < n_new:
-        tree = build_tree(backend, root, seq[:-1], configs, bottom, est, cost, params, n_layers, stats)
+        tree = build_tree(backend, root, seq[:n_seq - 1], configs, bottom, est, cost, params, n_layers, stats)
         order = tree.ordering()
         rid = {node: j for j, node in enumerate(order)}
         toks = [tree.nodes[i].token for i in order]
@@ -476,7 +482,8 @@ def cas_decode_dytc(backend, prompt: Sequence[int], n_new: int, configs: Sequenc
         est.end_step()
         new = [tree.nodes[order[j]].token for j in path_ids[1:]] + [int(bonus)]
         out.extend(new)
-        seq.extend(new)
+        seq[n_seq:n_seq + len(new)] = new
+        n_seq += len(new)
         root = int(bonus)
         if stats is not None:
             stats.setdefault("accepted", []).append(len(path_ids) - 1)
