@@ -64,6 +64,7 @@ typedef struct {
     int n_nodes;                      /* nodes of the current tree round */
     int verified;                     /* the last forward covered the whole round at full depth */
     int *parent, *depth, *token;      /* per node of the round */
+    int attn_sink, attn_window;       /* efficient-attention draft (window 0: all committed slots) */
 } om_model;
 
 /* ------------------------------------------------------------------ numerics */
@@ -324,6 +325,17 @@ int om_set_committed(om_model *m, int Lc) {
 }
 int om_committed(const om_model *m) { return m->Lc; }
 
+/* Efficient attention as a DSIA strategy (Sec. 4.1, StreamingLLM-style): the
+ * forwards that follow see, of the committed slots, only the first `sink`
+ * and the last `window` ones (window 0: all of them).  Such a forward is a
+ * draft, never a verify. */
+int om_set_window(om_model *m, int sink, int window) {
+    if (sink < 0 || window < 0) return -1;
+    m->attn_sink = window > 0 ? sink : 0;
+    m->attn_window = window;
+    return 0;
+}
+
 /*
  * Forward over n new tree nodes (ids node_offset .. node_offset+n-1 of the
  * current round).  node_offset 0 starts a new round; otherwise the call
@@ -363,7 +375,7 @@ int om_forward(om_model *m, const int32_t *tokens, const int32_t *parents, int n
         m->depth[node] = parents[i] < 0 ? 0 : m->depth[parents[i]] + 1;
     }
     m->n_nodes = node_offset + n;
-    m->verified = (node_offset == 0 && full && !act_quant);
+    m->verified = (node_offset == 0 && full && !act_quant && m->attn_window == 0);
 
     uint8_t *run = (uint8_t *)calloc((size_t)n, 1);
     for (int i = n - 1; i >= 0; i--) {
@@ -431,20 +443,30 @@ int om_forward(om_model *m, const int32_t *tokens, const int32_t *parents, int n
         for (int i = 0; i < n; i++) {
             if (!run[i]) continue;
             int node = node_offset + i;
-            /* visible keys: all committed slots, then ancestors-or-self by increasing id */
+            /* visible keys: the committed slots (all, or the sink and the
+               recent window), then ancestors-or-self by increasing id */
             int na = 0;
             for (int a = node; a >= 0; a = m->parent[a]) anc[na++] = a;
-            int nk = m->Lc + na;
+            int c_lo = m->Lc, c_hi = m->Lc;   /* committed slots [0, c_lo) and [c_hi, Lc) */
+            if (m->attn_window > 0) {
+                c_lo = m->attn_sink < m->Lc ? m->attn_sink : m->Lc;
+                c_hi = m->Lc - m->attn_window;
+                if (c_hi < c_lo) c_hi = c_lo;
+            }
+            int nc = c_lo + (m->Lc - c_hi);
+            int nk = nc + na;
             #pragma omp parallel for schedule(static)
             for (int hh = 0; hh < H; hh++) {
                 int kvh = hh / G;
                 const double **kl = (const double **)malloc(sizeof(double *) * (size_t)nk);
                 const double **vl = (const double **)malloc(sizeof(double *) * (size_t)nk);
-                for (int s = 0; s < m->Lc; s++) { kl[s] = kslot(m, l, kvh, s); vl[s] = vslot(m, l, kvh, s); }
+                int c = 0;
+                for (int s = 0; s < c_lo; s++, c++) { kl[c] = kslot(m, l, kvh, s); vl[c] = vslot(m, l, kvh, s); }
+                for (int s = c_hi; s < m->Lc; s++, c++) { kl[c] = kslot(m, l, kvh, s); vl[c] = vslot(m, l, kvh, s); }
                 for (int j = 0; j < na; j++) {
                     int a = anc[na - 1 - j];
-                    kl[m->Lc + j] = kslot(m, l, kvh, m->Lc + a);
-                    vl[m->Lc + j] = vslot(m, l, kvh, m->Lc + a);
+                    kl[nc + j] = kslot(m, l, kvh, m->Lc + a);
+                    vl[nc + j] = vslot(m, l, kvh, m->Lc + a);
                 }
                 om_attend(q + (size_t)i * qd + (size_t)hh * hd, kl, vl, nk, hd, ao + (size_t)i * qd + (size_t)hh * hd);
                 free(kl); free(vl);

@@ -61,6 +61,8 @@ def lib():
         L.om_committed.restype = I
         L.om_forward.argtypes = [P, P, P, I, I, P, I, P, P]
         L.om_forward.restype = I
+        L.om_set_window.argtypes = [P, I, I]
+        L.om_set_window.restype = I
         L.om_compact.argtypes = [P, P, I]
         L.om_compact.restype = I
         L.om_round_bf16.argtypes = [D]
@@ -246,7 +248,19 @@ class OracleModel:
     # the step ----------------------------------------------------------------
     def forward(self, tokens: Sequence[int], parents: Sequence[int], node_offset: int = 0,
                 skip: Optional[Sequence[int]] = None, act_quant: bool = False,
-                need: Optional[Sequence[bool]] = None) -> np.ndarray:
+                need: Optional[Sequence[bool]] = None,
+                attn_window: Optional[Tuple[int, int]] = None) -> np.ndarray:
+        """attn_window = (sink, window): efficient-attention draft that sees
+        only the first sink and the last window committed slots."""
+        sink, win = attn_window if attn_window else (0, 0)
+        if lib().om_set_window(self.h, int(sink), int(win)):
+            raise ValueError("bad attention window")
+        try:
+            return self._forward(tokens, parents, node_offset, skip, act_quant, need)
+        finally:
+            lib().om_set_window(self.h, 0, 0)
+
+    def _forward(self, tokens, parents, node_offset, skip, act_quant, need) -> np.ndarray:
         toks = np.ascontiguousarray(tokens, dtype=np.int32)
         par = np.ascontiguousarray(parents, dtype=np.int32)
         n = toks.shape[0]

@@ -61,9 +61,10 @@ def _rope_complex(x, pos, theta):
     return torch.cat([z.real, z.imag], dim=-1)
 
 
-def textbook_logits(shape, w, tokens, round_bf16=False):
+def textbook_logits(shape, w, tokens, round_bf16=False, mask=None):
     """Causal decoder over `tokens` from library routines, float64.  With
-    round_bf16 the storage points round through torch's bfloat16 cast."""
+    round_bf16 the storage points round through torch's bfloat16 cast; mask
+    ([S][S] bool, True = visible) replaces the causal mask."""
     bf16 = shape.dtype == "bf16"
     rb = (lambda t: t.to(torch.float32).to(torch.bfloat16).to(torch.float64)) if round_bf16 else (lambda t: t)
     S = len(tokens)
@@ -78,8 +79,13 @@ def textbook_logits(shape, w, tokens, round_bf16=False):
         q = rb(_rope_complex(q, pos, shape.rope_theta))
         k = rb(_rope_complex(k, pos, shape.rope_theta))
         v = rb(v)
-        o = F.scaled_dot_product_attention(q.transpose(0, 1)[None], k.transpose(0, 1)[None],
-                                           v.transpose(0, 1)[None], is_causal=True, enable_gqa=True)
+        if mask is None:
+            o = F.scaled_dot_product_attention(q.transpose(0, 1)[None], k.transpose(0, 1)[None],
+                                               v.transpose(0, 1)[None], is_causal=True, enable_gqa=True)
+        else:
+            o = F.scaled_dot_product_attention(q.transpose(0, 1)[None], k.transpose(0, 1)[None],
+                                               v.transpose(0, 1)[None], attn_mask=torch.as_tensor(mask),
+                                               enable_gqa=True)
         o = rb(o[0].transpose(0, 1).reshape(S, H * hd))
         x = x + o @ _w64(lw["wo"], bf16).T
         xn = rb(F.rms_norm(x, (shape.d_model,), weight=torch.from_numpy(lw["ffn_norm"]).double(), eps=shape.rms_eps))
@@ -111,6 +117,37 @@ def test_chain_equals_textbook_bf16_gqa(small):
     err = np.abs(got - ref).max() / np.abs(ref).max()
     assert err < 2e-3, err
     assert err < err0 / 4
+
+
+@pytest.mark.parametrize("sink,win", [(4, 8), (0, 5), (3, 100), (30, 4)])
+def test_attention_window_equals_masked_textbook(tiny, sink, win):
+    """Efficient-attention draft (StreamingLLM-style): after a 24-token
+    prefix is committed with full attention, a 6-token chain that sees only
+    the first `sink` and the last `win` committed slots (plus its own chain)
+    equals the textbook decoder under that explicit mask.  A sink or window
+    covering the prefix gives plain causal attention."""
+    P, C = 24, 6
+    toks = synth.gen_prompt(TINY.vocab, P + C, seed=13)
+    m = O.OracleModel(TINY, tiny, max_ctx=64)
+    m.prefill(list(toks[:P]))
+    got = m.forward(toks[P:], synth.chain_parents(C), attn_window=(sink, win))
+    S = P + C
+    mask = np.tril(np.ones((S, S), dtype=bool))
+    lo = min(sink, P)
+    hi = max(lo, P - win)
+    for i in range(P, S):
+        mask[i, :P] = False
+        mask[i, :lo] = True
+        mask[i, hi:P] = True
+    ref = textbook_logits(TINY, tiny, toks, mask=mask)[P:]
+    err = np.abs(got - ref).max() / np.abs(ref).max()
+    assert err < 1e-12, err
+    if lo == P or hi == lo:
+        full = textbook_logits(TINY, tiny, toks)[P:]
+        assert np.abs(full - ref).max() / np.abs(full).max() < 1e-12
+    else:
+        full = m.forward(toks[P:], synth.chain_parents(C))
+        assert np.abs(full - got).max() > 1e-6  # the window changes the result
 
 
 # ---------------------------------------------------------------- tree exactness
