@@ -151,6 +151,37 @@ cas_status cas_forward(cas_ctx* ctx, const int32_t* tokens, const int32_t* tree_
 cas_status cas_logits_device(const cas_ctx* ctx, const float** dptr, int32_t* n);
 
 /*
+ * Options of a draft forward.  A DSIA draft model (Def. 4.1) is the target
+ * with one or more of these strategies switched on for the call (Sec. 4.1):
+ *   skip_mask    layer sparsity: NULL or n_layers bytes, 1 = skip that layer
+ *                (a suffix of skipped layers is early exit)
+ *   act_quant    activation quantisation: 0, or 1 = per-token int8
+ *                activations (needs cas_build_int8)
+ *   attn_sink,   efficient attention (StreamingLLM-style): attn_window > 0
+ *   attn_window  limits the committed slots each row attends to to the first
+ *                attn_sink and the last attn_window ones (tree ancestors stay
+ *                visible); the kernels then read only those key tiles.
+ *                attn_window = 0 keeps every committed slot (attn_sink is
+ *                ignored).
+ */
+typedef struct {
+    const uint8_t* skip_mask;
+    int32_t act_quant;
+    int32_t attn_sink;
+    int32_t attn_window;
+} cas_draft_opts;
+
+/*
+ * cas_forward with draft options (NULL opts: a plain forward, as
+ * cas_forward with no skip mask and act_quant 0).  Same arguments, limits,
+ * errors and synchronisation as cas_forward; negative attn_sink or
+ * attn_window give CAS_ERR_ARG.  A call with attn_window > 0 is never a
+ * verify call.
+ */
+cas_status cas_forward_draft(cas_ctx* ctx, const int32_t* tokens, const int32_t* tree_parent, int32_t n,
+                             int32_t node_offset, const cas_draft_opts* opts, float* logits_host);
+
+/*
  * Greedy verification of the tree of the last verify call: g[i] is the
  * argmax of node i's logits (lowest index on ties).  From the root, move to
  * the child (lowest id first) whose token equals g of the current node, while

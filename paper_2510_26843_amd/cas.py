@@ -31,7 +31,7 @@ KCLASS = ["embed", "rmsnorm", "gemm_qkv", "attn", "gemm_o", "gemm_gateup", "gemm
 # every symbol the two headers declare
 EXPORTS = ("cas_create", "cas_destroy", "cas_last_error", "cas_create_error", "cas_load_tensor", "cas_build_int8",
            "cas_prefill", "cas_kv_load", "cas_kv_read", "cas_set_committed", "cas_committed_len", "cas_forward",
-           "cas_logits_device", "cas_accept_tree", "cas_topk", "cas_kv_compact", "cas_tree_info", "cas_set_graphs",
+           "cas_logits_device", "cas_forward_draft", "cas_accept_tree", "cas_topk", "cas_kv_compact", "cas_tree_info", "cas_set_graphs",
            "cas_profile", "cas_profile_read", "cas_sync", "cas_op_gemm", "cas_op_gemm_work_bytes",
            "cas_op_quant_rows", "cas_op_quant_weight", "cas_op_quant_weight_work_bytes", "cas_op_attention",
            "cas_op_attention_work_bytes", "cas_op_copy")
@@ -42,6 +42,11 @@ class CasError(RuntimeError):
         name = STATUS_NAMES[status] if 0 <= status < len(STATUS_NAMES) else str(status)
         super().__init__(f"{name}: {msg}")
         self.status = status
+
+
+class DraftOpts(ctypes.Structure):
+    _fields_ = [("skip_mask", ctypes.c_void_p), ("act_quant", ctypes.c_int32), ("attn_sink", ctypes.c_int32),
+                ("attn_window", ctypes.c_int32)]
 
 
 class Config(ctypes.Structure):
@@ -75,6 +80,7 @@ def lib():
             "cas_logits_device": ([P, P, P], I),
             "cas_accept_tree": ([P, I, P, P, P], I),
             "cas_kv_compact": ([P, P, I], I),
+            "cas_forward_draft": ([P, P, P, I, I, P, P], I),
             "cas_topk": ([P, I, I, P, P], I),
             "cas_tree_info": ([P, I, P, P], I),
             "cas_set_graphs": ([P, I], I),
@@ -197,7 +203,8 @@ class Model:
     # the step -------------------------------------------------------------------
     def forward(self, tokens: Sequence[int], parents: Sequence[int], node_offset: int = 0,
                 skip: Optional[Sequence[int]] = None, act_quant: bool = False,
-                logits: bool = True) -> Optional[np.ndarray]:
+                logits: bool = True, attn_window: Optional[Tuple[int, int]] = None) -> Optional[np.ndarray]:
+        """attn_window = (sink, window): efficient-attention draft."""
         t = np.ascontiguousarray(tokens, dtype=np.int32)
         p = np.ascontiguousarray(parents, dtype=np.int32)
         n = t.shape[0]
@@ -209,8 +216,14 @@ class Model:
             if sk.shape[0] != self.shape.n_layers:
                 raise ValueError("skip mask length")
         out = np.empty((n, self.shape.vocab), dtype=np.float32) if logits else None
-        self._chk(lib().cas_forward(self.h, _p(t), _p(p), n, int(node_offset), None if sk is None else _p(sk),
-                                    1 if act_quant else 0, None if out is None else _p(out)))
+        if attn_window:
+            o = DraftOpts(None if sk is None else _p(sk), 1 if act_quant else 0, int(attn_window[0]),
+                          int(attn_window[1]))
+            self._chk(lib().cas_forward_draft(self.h, _p(t), _p(p), n, int(node_offset), ctypes.byref(o),
+                                              None if out is None else _p(out)))
+        else:
+            self._chk(lib().cas_forward(self.h, _p(t), _p(p), n, int(node_offset), None if sk is None else _p(sk),
+                                        1 if act_quant else 0, None if out is None else _p(out)))
         return out
 
     def logits_device(self) -> Tuple[int, int]:

@@ -130,9 +130,16 @@ struct AttnArgs {
     float* part_o;        // [splits][H][T][hd]
     float* part_ml;       // [splits][H][T][2]
     int T, H, Hkv, hd, ctx_cap;
+    // efficient attention (win_len > 0): of the committed slots only
+    // [0, win_sink) and [Lc - win_len, Lc) are visible; the grid covers only
+    // the key tiles that hold them
+    int win_sink, win_len;
 };
 size_t attention_work_bytes(int n_slots, int T, int H, int hd);
 int attention_splits(int n_slots);
+// KV splits of a forward whose committed slots are limited to a sink and a
+// window (win_len 0: all of them)
+int attention_splits_win(int Lc, int n_tree, int win_sink, int win_len);
 // atype: ET_BF16 (MFMA path, then the merge of the KV splits) or ET_F32
 // (plain path, ctx_cap <= 4096)
 hipError_t launch_attention(int atype, const AttnArgs& a, hipStream_t s);

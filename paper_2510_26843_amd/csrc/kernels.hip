@@ -647,6 +647,35 @@ static constexpr int ATT_SPLIT = ATT_WAVES * ATT_TPW * 32;
 static constexpr int ATT_MAX_SPLITS = 64;  // contexts up to 16384 slots
 
 int attention_splits(int n_slots) { return (n_slots + ATT_SPLIT - 1) / ATT_SPLIT; }
+
+// Key tiles of a windowed forward: the tiles holding the sink slots, then the
+// tiles from the window's first slot to the last tree slot.  Logical tile lt
+// is physical tile lt (lt < st) or lt - st + pt0.  Without a window every
+// committed slot is visible (csink = wstart = Lc) and the map is the identity.
+struct AttnWindow {
+    int csink, wstart, st, pt0, n_log;
+    __host__ __device__ AttnWindow(int Lc, int n_tree, int win_sink, int win_len) {
+        const int n_tiles = (Lc + n_tree + 31) >> 5;
+        if (win_len > 0) {
+            csink = win_sink < Lc ? win_sink : Lc;
+            wstart = Lc - win_len > csink ? Lc - win_len : csink;
+            st = (csink + 31) >> 5;
+            pt0 = (wstart >> 5) > st ? (wstart >> 5) : st;
+            n_log = st + (n_tiles - pt0);
+        } else {
+            csink = wstart = Lc;
+            st = n_tiles;
+            pt0 = 0;
+            n_log = n_tiles;
+        }
+    }
+    __host__ __device__ int phys(int lt) const { return lt < st ? lt : lt - st + pt0; }
+};
+
+int attention_splits_win(int Lc, int n_tree, int win_sink, int win_len) {
+    const AttnWindow w(Lc, n_tree, win_sink, win_len);
+    return (w.n_log * 32 + ATT_SPLIT - 1) / ATT_SPLIT;
+}
 size_t attention_work_bytes(int n_slots, int T, int H, int hd) {
     const size_t S = (size_t)attention_splits(n_slots);
     return S * H * T * (size_t)hd * 4 + S * H * T * 2 * 4 + 256;
@@ -701,6 +730,7 @@ __global__ void __launch_bounds__(256) k_attn_bf16(const AttnArgs a, float scale
     const int split = blockIdx.x, kvh = blockIdx.y, rc = blockIdx.z;
     const int Lc = a.sp->Lc, n_tree = a.sp->n_tree, n_slots = Lc + n_tree;
     const int n_tiles = (n_slots + 31) >> 5;
+    const AttnWindow win(Lc, n_tree, a.win_sink, a.win_len);
     const int T = a.T, Tp = (T + 15) & ~15, G = a.H / a.Hkv;
     const int nct = G * Tp / 16;
     const uint16_t* q = (const uint16_t*)a.q;
@@ -727,11 +757,15 @@ __global__ void __launch_bounds__(256) k_attn_bf16(const AttnArgs a, float scale
     // K and V fragments of this wave's tiles, in the order they are consumed
     const uint16_t* kbase = (const uint16_t*)a.kc + (size_t)kvh * a.ctx_cap * HD + lane * 8;
     const uint16_t* vbase = (const uint16_t*)a.vt + (size_t)kvh * a.ctx_cap * HD + lane * 8;
-    const int tile0 = (split * ATT_WAVES + wave) * TPW;
+    const int tile0 = (split * ATT_WAVES + wave) * TPW;  // logical key tiles of this wave
+    int ptile[TPW];
+    bool live[TPW];
     i32x4 Kf[TPW][2][UD], Vf[TPW][NDT];
 #pragma unroll
     for (int tt = 0; tt < TPW; ++tt) {
-        const size_t tb = (size_t)min(tile0 + tt, n_tiles - 1) * TE;
+        live[tt] = tile0 + tt < win.n_log;
+        ptile[tt] = live[tt] ? win.phys(tile0 + tt) : n_tiles - 1;
+        const size_t tb = (size_t)ptile[tt] * TE;
 #pragma unroll
         for (int h2 = 0; h2 < 2; ++h2)
 #pragma unroll
@@ -776,8 +810,10 @@ __global__ void __launch_bounds__(256) k_attn_bf16(const AttnArgs a, float scale
             for (int h2 = 0; h2 < 2; ++h2)
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
-                    const int slot = (tile0 + tt) * 32 + 8 * g + 4 * h2 + i;
-                    const bool vis = slot < n_slots && (slot < Lc || anc_bit(an0[j], an1[j], slot - Lc));
+                    const int slot = ptile[tt] * 32 + 8 * g + 4 * h2 + i;
+                    const bool vis = live[tt] && slot < n_slots &&
+                                     (slot < Lc ? (slot < win.csink || slot >= win.wstart)
+                                                : anc_bit(an0[j], an1[j], slot - Lc));
                     const float xv = vis ? S[tt][h2][j][i] * scale_log2 : -INFINITY;
                     x[tt][4 * h2 + i] = xv;
                     mt = fmaxf(mt, xv);
@@ -916,13 +952,14 @@ __global__ void __launch_bounds__(256) k_attn_f32(const AttnArgs a, float scale)
     const int t = blockIdx.x, h = blockIdx.y, hd = a.hd;
     const int G = a.H / a.Hkv, kvh = h / G;
     const int Lc = a.sp->Lc, n_slots = Lc + a.sp->n_tree;
+    const AttnWindow win(Lc, a.sp->n_tree, a.win_sink, a.win_len);
     const uint64_t a0 = a.anc[2 * t], a1 = a.anc[2 * t + 1];
     const float* q = (const float*)a.q + ((size_t)t * a.H + h) * hd;
     const float* kb = (const float*)a.kc + (size_t)kvh * a.ctx_cap * hd;
     const float* vb = (const float*)a.vt + (size_t)kvh * hd * a.ctx_cap;
     float mx = -INFINITY;
     for (int s = threadIdx.x; s < n_slots; s += 256) {
-        const bool vis = s < Lc || anc_bit(a0, a1, s - Lc);
+        const bool vis = s < Lc ? (s < win.csink || s >= win.wstart) : anc_bit(a0, a1, s - Lc);
         float v = -INFINITY;
         if (vis) {
             float d = 0.f;
@@ -958,7 +995,7 @@ hipError_t launch_attention(int atype, const AttnArgs& a, hipStream_t s) {
         hipLaunchKernelGGL(k_attn_f32, dim3(a.T, a.H), dim3(256), (size_t)a.ctx_cap * 4, s, a, scale);
         return hipGetLastError();
     }
-    const int S = attention_splits(n_slots);
+    const int S = attention_splits_win(a.Lc_host, a.n_tree_host, a.win_sink, a.win_len);
     const int G = a.H / a.Hkv, Tp = (a.T + 15) & ~15;
     // one 16-row query tile per workgroup: twice the workgroups of two tiles,
     // half the arithmetic on each one's critical path (K/V re-reads hit L2)

@@ -105,6 +105,7 @@ struct cas_ctx {
 
     bool graphs = true;
     std::map<std::string, hipGraphExec_t> gcache;
+    int win_sink = 0, win_len = 0;  // attention window of the forward being enqueued (0: none)
 
     bool prof = false;
     std::vector<ProfRec> prec;
@@ -276,7 +277,9 @@ hipError_t enqueue_forward(cas_ctx* c, int T, const uint8_t* skip, int aq) {
     // splits for the attention grid come from the host copy of the state
     at.Lc_host = c->Lc;
     at.n_tree_host = c->n_nodes;  // already the post-call node count
-    const int S = attention_splits(at.Lc_host + at.n_tree_host);
+    at.win_sink = c->win_sink;
+    at.win_len = c->win_len;
+    const int S = attention_splits_win(at.Lc_host, at.n_tree_host, at.win_sink, at.win_len);
     at.part_o = c->d_part;
     at.part_ml = c->d_part + (size_t)S * H * T * hd;
     const int wq = aq ? (int)ET_I8 : et;
@@ -386,7 +389,8 @@ hipError_t enqueue_forward(cas_ctx* c, int T, const uint8_t* skip, int aq) {
 }
 
 std::string graph_key(const cas_ctx* c, int T, const uint8_t* skip, int aq, int S) {
-    std::string k = std::to_string(T) + ":" + std::to_string(aq) + ":" + std::to_string(S) + ":";
+    std::string k = std::to_string(T) + ":" + std::to_string(aq) + ":" + std::to_string(S) + ":" +
+                    std::to_string(c->win_sink) + ":" + std::to_string(c->win_len) + ":";
     for (int l = 0; l < c->cfg.n_layers; ++l) k.push_back(skip && skip[l] ? '1' : '0');
     return k;
 }
@@ -403,9 +407,12 @@ cas_status check_ready(cas_ctx* c, const uint8_t* skip) {
 }
 
 cas_status do_forward(cas_ctx* c, const int32_t* tokens, const int32_t* parent, int n, int node_offset,
-                      const uint8_t* skip, int aq, float* logits_host, bool allow_graph = true) {
+                      const uint8_t* skip, int aq, float* logits_host, bool allow_graph = true, int win_sink = 0,
+                      int win_len = 0) {
     const cas_config& f = c->cfg;
     if (!tokens || !parent) return fail(c, CAS_ERR_ARG, "tokens and tree_parent must not be NULL");
+    if (win_sink < 0 || win_len < 0) return fail(c, CAS_ERR_ARG, "attn_sink and attn_window must be >= 0");
+    if (win_len == 0) win_sink = 0;
     if (n < 1) return fail(c, CAS_ERR_ARG, "n must be >= 1");
     if (node_offset < 0) return fail(c, CAS_ERR_ARG, "node_offset must be >= 0");
     if (aq != 0 && aq != 1) return fail(c, CAS_ERR_ARG, "act_quant must be 0 or 1");
@@ -450,7 +457,9 @@ cas_status do_forward(cas_ctx* c, const int32_t* tokens, const int32_t* parent, 
     // round state (the launch sequence reads the post-call node count)
     const int old_nodes = c->n_nodes;
     c->n_nodes = node_offset + n;
-    const int S = attention_splits(c->Lc + c->n_nodes);
+    c->win_sink = win_sink;
+    c->win_len = win_len;
+    const int S = attention_splits_win(c->Lc, c->n_nodes, win_sink, win_len);
     hipError_t e;
     if (c->graphs && !c->prof && allow_graph) {
         const std::string key = graph_key(c, n, skip, aq, S);
@@ -489,7 +498,7 @@ cas_status do_forward(cas_ctx* c, const int32_t* tokens, const int32_t* parent, 
         c->parent[node_offset + i] = parent[i];
         c->token[node_offset + i] = tokens[i];
     }
-    c->verified_n = (node_offset == 0 && !any_skip && !aq) ? n : 0;
+    c->verified_n = (node_offset == 0 && !any_skip && !aq && win_len == 0) ? n : 0;
     c->logits_rows = n;
     if (logits_host) {
         HIPCHK(c, hipMemcpyAsync(logits_host, c->d_logits, sizeof(float) * (size_t)n * f.vocab, hipMemcpyDeviceToHost,
@@ -803,6 +812,14 @@ cas_status cas_forward(cas_ctx* c, const int32_t* tokens, const int32_t* parent,
                        const uint8_t* skip, int32_t aq, float* logits_host) {
     if (!c) return CAS_ERR_ARG;
     return do_forward(c, tokens, parent, n, node_offset, skip, aq, logits_host);
+}
+
+cas_status cas_forward_draft(cas_ctx* c, const int32_t* tokens, const int32_t* parent, int32_t n,
+                             int32_t node_offset, const cas_draft_opts* o, float* logits_host) {
+    if (!c) return CAS_ERR_ARG;
+    if (!o) return do_forward(c, tokens, parent, n, node_offset, nullptr, 0, logits_host);
+    return do_forward(c, tokens, parent, n, node_offset, o->skip_mask, o->act_quant, logits_host, true, o->attn_sink,
+                      o->attn_window);
 }
 
 cas_status cas_prefill(cas_ctx* c, const int32_t* tokens, int32_t n) {

@@ -237,12 +237,13 @@ class LatencyModel:
 @dataclasses.dataclass
 class DraftConfig:
     """A draft model: a DSIA variant of the target (skip mask over the
-    layers, optional int8 activations) or prompt lookup (skip is None and
-    pld is True)."""
+    layers, optional int8 activations, optional sink + window attention) or
+    prompt lookup (skip is None and pld is True)."""
     name: str
     skip: Optional[Tuple[int, ...]] = None
     act_quant: bool = False
     pld: bool = False
+    window: Optional[Tuple[int, int]] = None  # efficient attention: (sink, window) committed slots
 
     def run_layers(self, n_layers: int) -> frozenset:
         if self.pld:
@@ -342,7 +343,7 @@ class LibraryBackend:
 
     def draft(self, tokens, parents, node_offset: int, cfg: DraftConfig, K: int):
         self.m.forward(tokens, parents, node_offset, skip=list(cfg.skip) if cfg.skip else None,
-                       act_quant=cfg.act_quant, logits=False)
+                       act_quant=cfg.act_quant, logits=False, attn_window=cfg.window)
         return self.m.topk(K, len(tokens))
 
     def verify(self, tokens, parents) -> Tuple[List[int], int]:

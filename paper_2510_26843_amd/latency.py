@@ -22,7 +22,7 @@ import json
 import statistics
 import sys
 import time
-from typing import Dict, List, Optional, Sequence
+from typing import Dict, List, Optional, Sequence, Tuple
 
 import numpy as np
 
@@ -44,11 +44,26 @@ def skip_mask(n_layers: int, rule: str) -> Optional[List[int]]:
     return [1 if l in ids else 0 for l in range(n_layers)]
 
 
-def algorithmic_bytes(shape, T: int, Lc: int, run_layers: int, int8: bool = False) -> int:
+def parse_draft(spec: str, n_layers: int):
+    """A draft configuration from '<skip rule>[+int8][@sink:window]'."""
+    window = None
+    if "@" in spec:
+        spec, w = spec.split("@")
+        sink, win = w.split(":")
+        window = (int(sink), int(win))
+    aq = spec.endswith("+int8")
+    return skip_mask(n_layers, spec.split("+")[0]), aq, window
+
+
+def algorithmic_bytes(shape, T: int, Lc: int, run_layers: int, int8: bool = False,
+                      window: Optional[Tuple[int, int]] = None) -> int:
     """Bytes one forward must move: the weights of the layers that run (bf16
     or fp32, or int8 codes plus fp32 per-channel scales) and the LM head
-    once, the KV reads of all visible slots and the writes of the new ones,
+    once, the KV reads of all visible slots (only the sink and the window
+    of the committed ones under a window) and the writes of the new ones,
     the embedding rows and the fp32 logits."""
+    if window and window[1] > 0:
+        Lc = min(Lc, window[0] + window[1])
     es = 2 if shape.dtype == "bf16" else 4
     kv_row = shape.n_kv_heads * shape.head_dim * es
     if int8:
@@ -78,17 +93,18 @@ def tree_for(T: int) -> List[int]:
     return balanced_tree(T)
 
 
-def time_forward(model, toks, parents, skip, aq: bool, reps: int, warmup: int = 3) -> Dict[str, float]:
+def time_forward(model, toks, parents, skip, aq: bool, reps: int, warmup: int = 3,
+                 window: Optional[Tuple[int, int]] = None) -> Dict[str, float]:
     """Wall time per forward over `reps` back-to-back calls (logits stay on
     the device), median of three such batches."""
     for _ in range(warmup):
-        model.forward(toks, parents, 0, skip=skip, act_quant=aq, logits=False)
+        model.forward(toks, parents, 0, skip=skip, act_quant=aq, logits=False, attn_window=window)
     model.sync()
     runs = []
     for _ in range(3):
         t0 = time.perf_counter()
         for _ in range(reps):
-            model.forward(toks, parents, 0, skip=skip, act_quant=aq, logits=False)
+            model.forward(toks, parents, 0, skip=skip, act_quant=aq, logits=False, attn_window=window)
         model.sync()
         runs.append((time.perf_counter() - t0) / reps * 1e3)
     return {"ms": statistics.median(runs), "ms_min": min(runs), "ms_max": max(runs)}
@@ -101,8 +117,7 @@ def sweep(model, shape, Ts: Sequence[int], ctxs: Sequence[int], drafts: Sequence
     every T as well (tree-parallel drafting runs drafts over several rows)."""
     from .synth import gen_tree_tokens
     out = []
-    configs = [("verify", None, False)] + [
-        (d, skip_mask(shape.n_layers, d.split("+")[0]), d.endswith("+int8")) for d in drafts]
+    configs = [("verify", None, False, None)] + [(d,) + parse_draft(d, shape.n_layers) for d in drafts]
     for ctx in ctxs:
         for T in Ts:
             parents = tree_for(T)
@@ -110,12 +125,13 @@ def sweep(model, shape, Ts: Sequence[int], ctxs: Sequence[int], drafts: Sequence
             depth = [0] * T
             for i, p in enumerate(parents):
                 depth[i] = 0 if p < 0 else depth[p] + 1
-            for name, skip, aq in configs:
+            for name, skip, aq, window in configs:
                 model.set_committed(ctx)
                 run = shape.n_layers - (sum(skip) if skip else 0)
-                r = time_forward(model, toks, parents, skip, aq, reps)
-                b = algorithmic_bytes(shape, T, ctx, run, int8=aq)
-                fl = algorithmic_flops(shape, T, ctx, run, float(np.mean(depth)))
+                r = time_forward(model, toks, parents, skip, aq, reps, window=window)
+                b = algorithmic_bytes(shape, T, ctx, run, int8=aq, window=window)
+                ctx_vis = min(ctx, window[0] + window[1]) if window and window[1] > 0 else ctx
+                fl = algorithmic_flops(shape, T, ctx_vis, run, float(np.mean(depth)))
                 rec = {"config": name, "T": T, "ctx": ctx, "run_layers": run, "act_int8": aq,
                        "ms": round(r["ms"], 4), "ms_min": round(r["ms_min"], 4), "ms_max": round(r["ms_max"], 4),
                        "tokens_per_s": round(T / (r["ms"] * 1e-3), 1), "bytes": b,
@@ -145,7 +161,9 @@ def main(argv=None) -> None:
     ap.add_argument("--shape", default="llama2_7b")
     ap.add_argument("--T", default="1,8,16,32,64,128")
     ap.add_argument("--ctx", default="512,2048,8192")
-    ap.add_argument("--drafts", default="", help="comma-free list separated by ';', e.g. 'odd;q3;odd+int8'")
+    ap.add_argument("--drafts", default="",
+                    help="draft configurations separated by ';', e.g. 'odd;q3;odd+int8;odd@4:1024' "
+                         "(skip rule, +int8 activations, @sink:window attention)")
     ap.add_argument("--reps", type=int, default=20)
     ap.add_argument("--out", default="")
     ap.add_argument("--md", default="")

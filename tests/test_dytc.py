@@ -275,7 +275,7 @@ class OracleBackend:
 
     def draft(self, tokens, parents, node_offset, cfg, K):
         lg = self.m.forward(tokens, parents, node_offset, skip=list(cfg.skip) if cfg.skip else None,
-                            act_quant=cfg.act_quant)
+                            act_quant=cfg.act_quant, attn_window=cfg.window)
         ids = np.stack([np.argsort(-r, kind="stable")[:K] for r in lg]).astype(np.int32)
         e = np.exp(lg - lg.max(axis=1, keepdims=True))
         p = e / e.sum(axis=1, keepdims=True)

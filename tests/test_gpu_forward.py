@@ -336,3 +336,47 @@ def test_root_row_is_bit_identical_for_every_tree_size(weights, name):
     for r in rows[1:]:
         assert np.array_equal(r.view(np.uint32), rows[0].view(np.uint32))
     g.close()
+
+
+@pytest.mark.parametrize("name,sink,win,tol", [("tiny", 4, 16, 1e-4), ("mha_small", 4, 64, 2e-2),
+                                               ("gqa_small", 0, 40, 2e-2), ("mha_small", 40, 33, 2e-2)])
+def test_attention_window_draft_parity(weights, name, sink, win, tol):
+    """Efficient-attention draft: each row sees the first `sink` and the last
+    `win` committed slots plus its ancestors; the kernels visit only those
+    key tiles.  Against the oracle with the same window, over a 32-node tree
+    after a 300-token prefix (130 for the fp32 model)."""
+    shape = {"tiny": TINY, "gqa_small": GQA, "mha_small": MHA}[name]
+    plen = 130 if name == "tiny" else 300
+    prompt = [int(x) for x in synth.gen_prompt(shape.vocab, plen, seed=21)]
+    g, o = _pair(shape, weights[name], prompt, max_ctx=512)
+    parents = synth.tree_from_branching(*synth.TREE_7B)
+    toks = synth.gen_tree_tokens(parents, shape.vocab, seed=22)
+    skip = [l % 2 for l in range(shape.n_layers)] if name == "gqa_small" else None
+    got = g.forward(toks, parents, 0, skip=skip, attn_window=(sink, win))
+    ref = o.forward(toks, parents, 0, skip=skip, attn_window=(sink, win))
+    err = _row_err(got, ref)
+    assert err < tol, err
+    full = o.forward(toks, parents, 0, skip=skip)
+    assert _row_err(full, ref) > 10 * err  # the window matters at this size
+    # a windowed forward is a draft: no acceptance may follow it
+    with pytest.raises(cas.CasError, match="CAS_ERR_STATE"):
+        g.accept()
+    g.close()
+
+
+def test_attention_window_covering_the_prefix_is_exact(weights):
+    shape = MHA
+    prompt = [int(x) for x in synth.gen_prompt(shape.vocab, 200, seed=23)]
+    g = cas.Model(shape, max_ctx=512)
+    g.load_weights(weights["mha_small"])
+    g.prefill(prompt)
+    parents = synth.tree_from_branching(*synth.TREE_7B)
+    toks = synth.gen_tree_tokens(parents, shape.vocab, seed=24)
+    a = g.forward(toks, parents, 0)
+    b = g.forward(toks, parents, 0, attn_window=(0, 200))
+    c = g.forward(toks, parents, 0, attn_window=(300, 1))
+    assert np.array_equal(a.view(np.uint32), b.view(np.uint32))
+    assert np.array_equal(a.view(np.uint32), c.view(np.uint32))
+    with pytest.raises(cas.CasError, match="CAS_ERR_ARG"):
+        g.forward(toks, parents, 0, attn_window=(0, -1))
+    g.close()
