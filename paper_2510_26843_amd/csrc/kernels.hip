@@ -126,10 +126,46 @@ __device__ __forceinline__ typename WTr<WT>::acc_t mfma_step(i32x4 a, i32x4 b, t
     }
 }
 
+// Per-lane operands of the QKV epilogue of one weight tile, loaded at kernel
+// start so that they sit in registers when the weight stream ends: each
+// row's KV slot and, for q and k rows, the RoPE cos/sin of the lane's two
+// rotation pairs at the row's position.  Loads are unconditional (indices
+// clamped into their arrays).
+template <int NT>
+struct QkvPre {
+    int slot[NT];
+    float cs[NT][2], sn[NT][2];
+    __device__ __forceinline__ void load(const GemmArgs& a, int tile, int lane) {
+        const int r = lane & 15, g = lane >> 4, nb = tile * 16 + 4 * g;
+        const int hd = a.hd, qrows = a.H * hd, krows = a.Hkv * hd, half = hd / 2;
+        const bool rot = nb < qrows + krows;
+        const int p0 = ((nb - (nb < qrows ? 0 : qrows)) % hd) / 2;
+#pragma unroll
+        for (int j = 0; j < NT; ++j) {
+            const int t = min(16 * j + r, a.T - 1);
+            slot[j] = a.row_slot[t];
+            const int pos = a.row_pos[t];
+#pragma unroll
+            for (int p = 0; p < 2; ++p) {
+                const size_t idx = rot ? (size_t)pos * half + p0 + p : 0;
+                cs[j][p] = a.rope_cos[idx];
+                sn[j][p] = a.rope_sin[idx];
+            }
+        }
+    }
+};
+
+// Two consecutive activation values (4-byte aligned for bf16, 8 for fp32).
+__device__ __forceinline__ void st2(uint16_t* p, size_t o, float x, float y) {
+    *(uint32_t*)(p + o) = (uint32_t)f2bf(x) | ((uint32_t)f2bf(y) << 16);
+}
+__device__ __forceinline__ void st2(float* p, size_t o, float x, float y) { *(float2*)(p + o) = make_float2(x, y); }
+
 // Epilogue of one 16-row weight tile: lane holds y[n = 16*tile + 4g + i][t = 16j + r].
+// qp: the tile's preloaded QKV operands (EPI_QKV only).
 template <int WT, int NT, int EPI, typename AT>
 __device__ __forceinline__ void gemm_epilogue(const GemmArgs& a, const typename WTr<WT>::acc_t (&acc)[NT], int tile,
-                                              int last_tile, int lane) {
+                                              int last_tile, int lane, const QkvPre<NT>& qp) {
     const int r = lane & 15, g = lane >> 4, T = a.T;
     const int nb = tile * 16 + 4 * g;
 #pragma unroll
@@ -172,29 +208,29 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs& a, const typename 
             }
         } else if constexpr (EPI == EPI_QKV) {
             const int hd = a.hd, qrows = a.H * hd, krows = a.Hkv * hd;
-            const int slot = a.row_slot[t];
+            const int slot = qp.slot[j];
             if (nb < qrows + krows) {
                 const bool isq = nb < qrows;
                 const int rel = nb - (isq ? 0 : qrows);
                 const int head = rel / hd, p0 = (rel % hd) / 2, half = hd / 2;
-                const int pos = a.row_pos[t];
+                float lo[2], hi[2];
 #pragma unroll
                 for (int p = 0; p < 2; ++p) {
-                    const int pp = p0 + p;
-                    const float cs = a.rope_cos[(size_t)pos * half + pp];
-                    const float sn = a.rope_sin[(size_t)pos * half + pp];
+                    const float cs = qp.cs[j][p], sn = qp.sn[j][p];
                     const float x0 = v[2 * p], x1 = v[2 * p + 1];
-                    const float lo = x0 * cs - x1 * sn, hi = x0 * sn + x1 * cs;
-                    if (isq) {
-                        AT* o = (AT*)a.out + ((size_t)t * a.H + head) * hd;
-                        Act<AT>::st(o, pp, lo);
-                        Act<AT>::st(o, pp + half, hi);
-                    } else {
-                        constexpr int ET = sizeof(AT) == 2 ? ET_BF16 : ET_F32;
-                        AT* o = (AT*)a.kc + (size_t)head * a.ctx_cap * hd;
-                        Act<AT>::st(o, kv_k_off(ET, slot, pp, hd, a.ctx_cap), lo);
-                        Act<AT>::st(o, kv_k_off(ET, slot, pp + half, hd, a.ctx_cap), hi);
-                    }
+                    lo[p] = x0 * cs - x1 * sn;
+                    hi[p] = x0 * sn + x1 * cs;
+                }
+                // the pairs p0, p0 + 1 (p0 even) are adjacent in q and in both K layouts
+                if (isq) {
+                    AT* o = (AT*)a.out + ((size_t)t * a.H + head) * hd;
+                    st2(o, p0, lo[0], lo[1]);
+                    st2(o, p0 + half, hi[0], hi[1]);
+                } else {
+                    constexpr int ET = sizeof(AT) == 2 ? ET_BF16 : ET_F32;
+                    AT* o = (AT*)a.kc + (size_t)head * a.ctx_cap * hd;
+                    st2(o, kv_k_off(ET, slot, p0, hd, a.ctx_cap), lo[0], lo[1]);
+                    st2(o, kv_k_off(ET, slot, p0 + half, hd, a.ctx_cap), hi[0], hi[1]);
                 }
             } else {
                 constexpr int ET = sizeof(AT) == 2 ? ET_BF16 : ET_F32;
@@ -254,6 +290,8 @@ __global__ void __launch_bounds__(64 * WAVES) k_gemm(const GemmArgs a) {
 
     i32x4 A[D][UC];
     i32x4 B[D][NT][UC];
+    QkvPre<NT> qp;
+    if constexpr (EPI == EPI_QKV) qp.load(a, tile, lane);
 
 #define CAS_GEMM_LOAD(st, stage)                                                                 \
     do {                                                                                         \
@@ -318,7 +356,7 @@ __global__ void __launch_bounds__(64 * WAVES) k_gemm(const GemmArgs a) {
                 for (int i = 0; i < 4; ++i) acc[j][i] += red[w - 1][j][i][lane];
     }
 
-    gemm_epilogue<WT, NT, EPI, AT>(a, acc, blockIdx.x, (int)gridDim.x - 1, lane);
+    gemm_epilogue<WT, NT, EPI, AT>(a, acc, blockIdx.x, (int)gridDim.x - 1, lane, qp);
 }
 
 // Wide variant for tall weight matrices: the WAVES waves of a workgroup own
@@ -356,6 +394,11 @@ __global__ void __launch_bounds__(64 * WAVES) k_gemm_wide(const GemmArgs a) {
         for (int j = 0; j < NT; ++j) acc[t][j] = ACC{0, 0, 0, 0};
     i32x4 A[D][TPW][UC];
     i32x4 Bv[D][LPT];
+    QkvPre<NT> qp[TPW];
+    if constexpr (EPI == EPI_QKV) {
+#pragma unroll
+        for (int t = 0; t < TPW; ++t) qp[t].load(a, tile0 + t, lane);
+    }
 
 #define CAS_W_LOAD(st, stage)                                                                    \
     do {                                                                                         \
@@ -408,12 +451,12 @@ __global__ void __launch_bounds__(64 * WAVES) k_gemm_wide(const GemmArgs a) {
 #undef CAS_W_LOAD
     if (gridDim.y == 1) {
 #pragma unroll
-        for (int t = 0; t < TPW; ++t) gemm_epilogue<WT, NT, EPI, AT>(a, acc[t], tile0 + t, a.N / 16 - 1, lane);
+        for (int t = 0; t < TPW; ++t) gemm_epilogue<WT, NT, EPI, AT>(a, acc[t], tile0 + t, a.N / 16 - 1, lane, qp[t]);
     } else {
         GemmArgs b = a;
         b.out = (float*)a.out + blockIdx.y * a.part_stride;
 #pragma unroll
-        for (int t = 0; t < TPW; ++t) gemm_epilogue<WT, NT, EPI, AT>(b, acc[t], tile0 + t, a.N / 16 - 1, lane);
+        for (int t = 0; t < TPW; ++t) gemm_epilogue<WT, NT, EPI, AT>(b, acc[t], tile0 + t, a.N / 16 - 1, lane, qp[t]);
     }
 }
 
