@@ -1040,19 +1040,28 @@ hipError_t launch_attention(int atype, const AttnArgs& a, hipStream_t s) {
     }
     const int S = attention_splits_win(a.Lc_host, a.n_tree_host, a.win_sink, a.win_len);
     const int G = a.H / a.Hkv, Tp = (a.T + 15) & ~15;
-    // one 16-row query tile per workgroup: twice the workgroups of two tiles,
-    // half the arithmetic on each one's critical path (K/V re-reads hit L2)
-    const int nct = G * Tp / 16, nrc = nct;
+    // 16-row query tiles per workgroup: one (the most workgroups, the
+    // shortest critical path: the 7B 32-node tree at context 1024) unless
+    // the grid of (split, kv head, query tile) units is large and every query
+    // head has its own K/V.  Then two tiles share each K/V load, which halves
+    // the per-CU key traffic (13B 64 nodes at 2048: 32.6 -> 28.7 us per layer;
+    // 7B 128 nodes at 8192: 181 -> 112 us).  Grouped-query models gained
+    // nothing from it (8B 64 nodes at 4096: 35.1 -> 35.8 us).
+    const int nct = G * Tp / 16;
+    const int JT = (G == 1 && S * a.Hkv * nct >= 1024) ? 2 : 1;
+    const int nrc = (nct + JT - 1) / JT;
     if (a.ctx_cap % 32 || S > ATT_MAX_SPLITS) return hipErrorInvalidValue;
     const float scale_log2 = (1.0f / sqrtf((float)a.hd)) * 1.4426950408889634f;
     // the merge: 4 query rows per workgroup, i.e. many small workgroups
     // (7B layer: attention + merge 12.1 us against 14.2 with 16 rows)
     const dim3 mg((a.T + 3) / 4, a.H);
     if (a.hd == 128) {
-        hipLaunchKernelGGL((k_attn_bf16<128, 1>), dim3(S, a.Hkv, nrc), dim3(256), 0, s, a, scale_log2);
+        if (JT == 2) hipLaunchKernelGGL((k_attn_bf16<128, 2>), dim3(S, a.Hkv, nrc), dim3(256), 0, s, a, scale_log2);
+        else hipLaunchKernelGGL((k_attn_bf16<128, 1>), dim3(S, a.Hkv, nrc), dim3(256), 0, s, a, scale_log2);
         hipLaunchKernelGGL((k_attn_merge<128, 4>), mg, dim3(128), 0, s, a, S);
     } else if (a.hd == 64) {
-        hipLaunchKernelGGL((k_attn_bf16<64, 1>), dim3(S, a.Hkv, nrc), dim3(256), 0, s, a, scale_log2);
+        if (JT == 2) hipLaunchKernelGGL((k_attn_bf16<64, 2>), dim3(S, a.Hkv, nrc), dim3(256), 0, s, a, scale_log2);
+        else hipLaunchKernelGGL((k_attn_bf16<64, 1>), dim3(S, a.Hkv, nrc), dim3(256), 0, s, a, scale_log2);
         hipLaunchKernelGGL((k_attn_merge<64, 4>), mg, dim3(64), 0, s, a, S);
     } else {
         return hipErrorInvalidValue;

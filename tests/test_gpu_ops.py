@@ -164,6 +164,11 @@ def _attention_case(H, Hkv, hd, Lc, parents, seed):
     # workgroup of each head group with one), and an MHA 128-node tree
     (32, 8, 128, 2000, ((4, 4, 4, 4), 64)),
     (8, 8, 128, 3000, ((2,) * 7, 128)),
+    # two query tiles per workgroup (large grids of MHA heads): an even and an
+    # odd tile count (the last workgroup of each head then has one tile)
+    (16, 16, 128, 3000, ((2,) * 7, 128)),
+    (16, 16, 128, 7000, ((2,) * 7, 40)),
+    (32, 32, 64, 2500, ((2,) * 7, 64)),
 ])
 def test_attention_tree_mask(H, Hkv, hd, Lc, tree):
     parents = synth.tree_from_branching(*tree) if tree[0] else [-1]
