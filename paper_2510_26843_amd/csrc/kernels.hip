@@ -748,6 +748,96 @@ __device__ __forceinline__ bool anc_bit(uint64_t a0, uint64_t a1, int node) {
     return node < 64 ? ((a0 >> node) & 1ull) : ((a1 >> (node - 64)) & 1ull);
 }
 
+// Softmax state of one part (NTL key tiles) for the rows of a 16-row query
+// tile, in two steps: attn_part_max gives the scores of visible slots
+// scaled to log2 units and their maximum m (at least -1e30, so an empty part
+// gives exp2 weights of 0); attn_part_probs gives the probabilities as bf16
+// hi + lo pairs in the P-operand order and their sum l.  Both attention
+// kernels use these and the merge helpers below with FP contraction off, so
+// they round every row the same way.
+// Bits e in [lo, hi) of an 8-bit mask.
+__device__ __forceinline__ uint32_t bits8(int lo, int hi) {
+    lo = max(lo, 0);
+    hi = min(hi, 8);
+    return lo < hi ? (0xffu >> (8 - (hi - lo))) << lo : 0u;
+}
+// Visibility of the 8 slots base .. base + 7 for one query row: committed
+// slots in [0, csink) or [wstart, Lc), tree slots whose node is an
+// ancestor-or-self (bit of the row's 128-bit mask), nothing at or past
+// n_slots.  Shifts and range masks instead of a test per slot.
+__device__ __forceinline__ uint32_t attn_vis8(int base, int Lc, int n_slots, const AttnWindow& win, uint64_t an0,
+                                              uint64_t an1) {
+    const uint32_t c = bits8(-base, win.csink - base) | bits8(win.wstart - base, Lc - base);
+    const int n0 = base - Lc;  // tree node of bit 0 (negative: bit -n0 holds node 0)
+    uint32_t t = 0;
+    if (n0 >= 64 && n0 < 128) t = (uint32_t)(an1 >> (n0 - 64));
+    else if (n0 > 0 && n0 < 64) t = (uint32_t)((an0 >> n0) | (an1 << (64 - n0)));
+    else if (n0 == 0) t = (uint32_t)an0;
+    else if (n0 > -8 && n0 < 0) t = (uint32_t)(an0 << (-n0));
+    return c | (t & bits8(Lc - base, n_slots - base));
+}
+template <int NTL>
+__device__ __forceinline__ void attn_part_scores(const f32x4 (&S)[NTL][2], const int* ptile, const bool* live, int g,
+                                                 int Lc, int n_slots, const AttnWindow& win, uint64_t an0,
+                                                 uint64_t an1, float scale_log2, float (&x)[NTL][8]) {
+#pragma clang fp contract(off)
+#pragma unroll
+    for (int tt = 0; tt < NTL; ++tt) {
+        const uint32_t vm = live[tt] ? attn_vis8(ptile[tt] * 32 + 8 * g, Lc, n_slots, win, an0, an1) : 0u;
+        if (__all(vm == 0xffu)) {  // a tile every lane sees whole (all committed tiles without a window)
+#pragma unroll
+            for (int h2 = 0; h2 < 2; ++h2)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) x[tt][4 * h2 + i] = S[tt][h2][i] * scale_log2;
+        } else {
+#pragma unroll
+            for (int h2 = 0; h2 < 2; ++h2)
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+                    x[tt][4 * h2 + i] = (vm >> (4 * h2 + i)) & 1u ? S[tt][h2][i] * scale_log2 : -INFINITY;
+        }
+    }
+}
+template <int NTL>
+__device__ __forceinline__ float attn_part_max(const float (&x)[NTL][8]) {
+    float mt = -INFINITY;
+#pragma unroll
+    for (int tt = 0; tt < NTL; ++tt)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) mt = fmaxf(mt, x[tt][e]);
+    return fmaxf(-1e30f, pair_max32(pair_max16(mt)));
+}
+template <int NTL>
+__device__ __forceinline__ float attn_part_probs(const float (&x)[NTL][8], float mn, i32x4 (&Pf)[NTL],
+                                                 i32x4 (&Pl)[NTL]) {
+#pragma clang fp contract(off)
+    float ps = 0.f;
+#pragma unroll
+    for (int tt = 0; tt < NTL; ++tt) {
+        uint16_t pb[8], pl[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+            const float p = __builtin_amdgcn_exp2f(x[tt][e] - mn);
+            ps += p;
+            pb[e] = f2bf(p);
+            pl[e] = f2bf(p - bf2f(pb[e]));  // exact difference, rounded: p = hi + lo to ~2^-17
+        }
+        Pf[tt] = i32x4{(int)(pb[0] | ((uint32_t)pb[1] << 16)), (int)(pb[2] | ((uint32_t)pb[3] << 16)),
+                       (int)(pb[4] | ((uint32_t)pb[5] << 16)), (int)(pb[6] | ((uint32_t)pb[7] << 16))};
+        Pl[tt] = i32x4{(int)(pl[0] | ((uint32_t)pl[1] << 16)), (int)(pl[2] | ((uint32_t)pl[3] << 16)),
+                       (int)(pl[4] | ((uint32_t)pl[5] << 16)), (int)(pl[6] | ((uint32_t)pl[7] << 16))};
+    }
+    return pair_sum32(pair_sum16(ps));
+}
+
+// The in-order merge of part states under the common maximum M: weight
+// exp2(m - M) of a part, then acc = fma(weight, o, acc), L = fma(weight, l, L).
+__device__ __forceinline__ float attn_merge_weight(float m, float M) { return exp2f(m - M); }
+__device__ __forceinline__ void attn_merge_o(f32x4& acc, const f32x4 o, float f) {
+    acc = f32x4{fmaf(o[0], f, acc[0]), fmaf(o[1], f, acc[1]), fmaf(o[2], f, acc[2]), fmaf(o[3], f, acc[3])};
+}
+__device__ __forceinline__ void attn_merge_l(float& L, float l, float f) { L = fmaf(l, f, L); }
+
 // Workgroup = (split of KV slots, kv head, chunk of 32 query rows).  The query
 // rows of a kv head are its G query heads x T tokens (each head padded to a
 // multiple of 16 rows), so GQA groups share every K/V fragment.  Scores come
@@ -830,56 +920,25 @@ __global__ void __launch_bounds__(256) k_attn_bf16(const AttnArgs a, float scale
     // softmax pass (no running rescale), then P V.  Slots past the context
     // and masked slots get probability 0; a wave with no visible slot keeps
     // m = -1e30, l = 0 and contributes nothing to the merge.
-    f32x4 S[TPW][2][JT];
+    f32x4 S[JT][TPW][2];
 #pragma unroll
     for (int tt = 0; tt < TPW; ++tt)
 #pragma unroll
         for (int h2 = 0; h2 < 2; ++h2)
 #pragma unroll
             for (int j = 0; j < JT; ++j) {
-                S[tt][h2][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+                S[j][tt][h2] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-                for (int u = 0; u < UD; ++u) S[tt][h2][j] = mfma_step<ET_BF16>(Kf[tt][h2][u], Qf[j][u], S[tt][h2][j]);
+                for (int u = 0; u < UD; ++u) S[j][tt][h2] = mfma_step<ET_BF16>(Kf[tt][h2][u], Qf[j][u], S[j][tt][h2]);
             }
     float m[JT], l[JT];
-    i32x4 Pf[TPW][JT], Pl[TPW][JT];
+    i32x4 Pf[JT][TPW], Pl[JT][TPW];
 #pragma unroll
     for (int j = 0; j < JT; ++j) {
         float x[TPW][8];
-        float mt = -INFINITY;
-#pragma unroll
-        for (int tt = 0; tt < TPW; ++tt)
-#pragma unroll
-            for (int h2 = 0; h2 < 2; ++h2)
-#pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    const int slot = ptile[tt] * 32 + 8 * g + 4 * h2 + i;
-                    const bool vis = live[tt] && slot < n_slots &&
-                                     (slot < Lc ? (slot < win.csink || slot >= win.wstart)
-                                                : anc_bit(an0[j], an1[j], slot - Lc));
-                    const float xv = vis ? S[tt][h2][j][i] * scale_log2 : -INFINITY;
-                    x[tt][4 * h2 + i] = xv;
-                    mt = fmaxf(mt, xv);
-                }
-        const float mn = fmaxf(-1e30f, pair_max32(pair_max16(mt)));
-        float ps = 0.f;
-#pragma unroll
-        for (int tt = 0; tt < TPW; ++tt) {
-            uint16_t pb[8], pl[8];
-#pragma unroll
-            for (int e = 0; e < 8; ++e) {
-                const float p = exp2f(x[tt][e] - mn);
-                ps += p;
-                pb[e] = f2bf(p);
-                pl[e] = f2bf(p - bf2f(pb[e]));  // exact difference, rounded: p = hi + lo to ~2^-17
-            }
-            Pf[tt][j] = i32x4{(int)(pb[0] | ((uint32_t)pb[1] << 16)), (int)(pb[2] | ((uint32_t)pb[3] << 16)),
-                              (int)(pb[4] | ((uint32_t)pb[5] << 16)), (int)(pb[6] | ((uint32_t)pb[7] << 16))};
-            Pl[tt][j] = i32x4{(int)(pl[0] | ((uint32_t)pl[1] << 16)), (int)(pl[2] | ((uint32_t)pl[3] << 16)),
-                              (int)(pl[4] | ((uint32_t)pl[5] << 16)), (int)(pl[6] | ((uint32_t)pl[7] << 16))};
-        }
-        l[j] = pair_sum32(pair_sum16(ps));
-        m[j] = mn;
+        attn_part_scores<TPW>(S[j], ptile, live, g, Lc, n_slots, win, an0[j], an1[j], scale_log2, x);
+        m[j] = attn_part_max<TPW>(x);
+        l[j] = attn_part_probs<TPW>(x, m[j], Pf[j], Pl[j]);
     }
     // P V with the probabilities as a two-term bf16 sum (hi + lo): the
     // product carries them to fp32-level accuracy; V is exact in bf16
@@ -891,8 +950,8 @@ __global__ void __launch_bounds__(256) k_attn_bf16(const AttnArgs a, float scale
             O[dt][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
             for (int tt = 0; tt < TPW; ++tt) {
-                O[dt][j] = mfma_step<ET_BF16>(Vf[tt][dt], Pf[tt][j], O[dt][j]);
-                O[dt][j] = mfma_step<ET_BF16>(Vf[tt][dt], Pl[tt][j], O[dt][j]);
+                O[dt][j] = mfma_step<ET_BF16>(Vf[tt][dt], Pf[j][tt], O[dt][j]);
+                O[dt][j] = mfma_step<ET_BF16>(Vf[tt][dt], Pl[j][tt], O[dt][j]);
             }
         }
 
@@ -913,7 +972,7 @@ __global__ void __launch_bounds__(256) k_attn_bf16(const AttnArgs a, float scale
         for (int j = 0; j < JT; ++j) *(f32x4*)(&sm_o[wave][j][r][16 * dt + 4 * g]) = O[dt][j];
     __syncthreads();
     constexpr int D4 = HD / 4;
-    for (int idx = threadIdx.x; idx < JT * 16 * D4; idx += 256) {
+    for (int idx = threadIdx.x; idx < JT * 16 * D4; idx += 64 * ATT_WAVES) {
         const int j = idx / (16 * D4), rr = (idx / D4) & 15, d4 = (idx % D4) * 4;
         const int t = t0[JT == 1 ? 0 : j] + rr;
         if (!tv[JT == 1 ? 0 : j] || t >= T) continue;
@@ -927,13 +986,139 @@ __global__ void __launch_bounds__(256) k_attn_bf16(const AttnArgs a, float scale
         float L = 0.f;
 #pragma unroll
         for (int w = 0; w < ATT_WAVES; ++w) {
-            const float f = exp2f(mw[w] - M);
-            acc += *(const f32x4*)(&sm_o[w][j][rr][d4]) * f;
-            L += sm_l[w][j][rr] * f;
+            const float f = attn_merge_weight(mw[w], M);
+            attn_merge_o(acc, *(const f32x4*)(&sm_o[w][j][rr][d4]), f);
+            attn_merge_l(L, sm_l[w][j][rr], f);
         }
         const size_t o = ((size_t)split * a.H + head[JT == 1 ? 0 : j]) * T + t;
         *(f32x4*)(a.part_o + o * HD + d4) = acc;
         if (d4 == 0) *(float2*)(a.part_ml + o * 2) = make_float2(M, L);
+    }
+}
+
+// Workgroup = (split of KV slots, kv head, QT query tiles of 16 rows): each
+// wave owns one query tile and the split's K and V pass once through LDS for
+// all of them, so a K/V byte leaves L2 once per QT tiles instead of once per
+// tile (grouped-query heads and large trees have many tiles per kv head).
+// Each wave computes, for its rows, the same four part states (two key tiles
+// each) as k_attn_bf16's four waves, with the same helpers, and merges them in
+// part order in registers: the partials are the same bits either way, so the
+// choice between the two kernels never changes a row's result.
+template <int HD, int QT>
+__global__ void __launch_bounds__(64 * QT, 2) k_attn_rows(const AttnArgs a, float scale_log2) {
+    constexpr int UD = HD / 32, DG = HD / 4, NDT = HD / 16, TE = 32 * HD;
+    constexpr int NP = ATT_WAVES;        // part states per split
+    constexpr int NTS = NP * ATT_TPW;    // key tiles per split
+    constexpr int KF = 2 * UD;           // 1 KB fragments per K tile (V: NDT)
+    constexpr int FS = NTS * KF;         // fragments per split, K and V alike
+    constexpr int LPT = FS / QT;         // fragments each wave stages
+    static_assert(KF == NDT && FS % QT == 0, "K and V tiles must stage alike");
+    __shared__ i32x4 kv[FS * 64];        // the split's K, then its V (64 KB for head_dim 128)
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int r = lane & 15, g = lane >> 4;
+    const int split = blockIdx.x, kvh = blockIdx.y;
+    const int Lc = a.sp->Lc, n_tree = a.sp->n_tree, n_slots = Lc + n_tree;
+    const int n_tiles = (n_slots + 31) >> 5;
+    const AttnWindow win(Lc, n_tree, a.win_sink, a.win_len);
+    const int T = a.T, Tp = (T + 15) & ~15, G = a.H / a.Hkv;
+    const int nct = G * Tp / 16;
+    const int ct = QT * blockIdx.z + wave;
+    const bool tv = ct < nct;
+    const int hg = tv ? (ct * 16) / Tp : 0, t0 = (ct * 16) % Tp, head = kvh * G + hg;
+    const uint16_t* q = (const uint16_t*)a.q;
+
+    i32x4 Qf[UD];
+    {
+        const int t = min(t0 + r, T - 1);
+#pragma unroll
+        for (int u = 0; u < UD; ++u) Qf[u] = *(const i32x4*)(q + ((size_t)t * a.H + head) * HD + g * DG + u * 8);
+    }
+    int ptile[NTS];
+    bool live[NTS];
+#pragma unroll
+    for (int tt = 0; tt < NTS; ++tt) {
+        live[tt] = split * NTS + tt < win.n_log;
+        ptile[tt] = live[tt] ? win.phys(split * NTS + tt) : n_tiles - 1;
+    }
+    // stage: every wave loads LPT of the split's K fragments and LPT of its V
+    // fragments (1 KB each, one per lane-wide load); K goes to LDS first
+    const uint16_t* kbase = (const uint16_t*)a.kc + (size_t)kvh * a.ctx_cap * HD + lane * 8;
+    const uint16_t* vbase = (const uint16_t*)a.vt + (size_t)kvh * a.ctx_cap * HD + lane * 8;
+    i32x4 Ks[LPT], Vs[LPT];
+#pragma unroll
+    for (int i = 0; i < LPT; ++i) {
+        const int f = wave * LPT + i;
+        Ks[i] = *(const i32x4*)(kbase + (size_t)ptile[f / KF] * TE + (f % KF) * 512);
+    }
+#pragma unroll
+    for (int i = 0; i < LPT; ++i) {
+        const int f = wave * LPT + i;
+        Vs[i] = *(const i32x4*)(vbase + (size_t)ptile[f / NDT] * TE + (f % NDT) * 512);
+    }
+    uint64_t an0 = a.anc[2 * min(t0 + r, T - 1)], an1 = a.anc[2 * min(t0 + r, T - 1) + 1];
+    if (!(tv && t0 + r < T)) {
+#pragma unroll
+        for (int u = 0; u < UD; ++u) Qf[u] = i32x4{0, 0, 0, 0};
+        an0 = an1 = 0ull;
+    }
+#pragma unroll
+    for (int i = 0; i < LPT; ++i) kv[(wave * LPT + i) * 64 + lane] = Ks[i];
+    __syncthreads();
+
+    f32x4 S[NP][ATT_TPW][2];
+#pragma unroll
+    for (int tt = 0; tt < NTS; ++tt)
+#pragma unroll
+        for (int h2 = 0; h2 < 2; ++h2) {
+            f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int u = 0; u < UD; ++u) acc = mfma_step<ET_BF16>(kv[(tt * KF + h2 * UD + u) * 64 + lane], Qf[u], acc);
+            S[tt / ATT_TPW][tt % ATT_TPW][h2] = acc;
+        }
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < LPT; ++i) kv[(wave * LPT + i) * 64 + lane] = Vs[i];
+    __syncthreads();
+
+    // the parts' scaled, masked scores and maxima first (the merge weights
+    // need the maximum over parts), then part by part: probabilities, P V,
+    // and the merge step
+    float x[NP][ATT_TPW][8], m[NP], M = -1e30f;
+#pragma unroll
+    for (int p = 0; p < NP; ++p) {
+        attn_part_scores<ATT_TPW>(S[p], &ptile[p * ATT_TPW], &live[p * ATT_TPW], g, Lc, n_slots, win, an0, an1,
+                                  scale_log2, x[p]);
+        m[p] = attn_part_max<ATT_TPW>(x[p]);
+        M = fmaxf(M, m[p]);
+    }
+    f32x4 acc[NDT];
+    float L = 0.f;
+#pragma unroll
+    for (int dt = 0; dt < NDT; ++dt) acc[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int p = 0; p < NP; ++p) {
+        i32x4 Pf[ATT_TPW], Pl[ATT_TPW];
+        const float lp = attn_part_probs<ATT_TPW>(x[p], m[p], Pf, Pl);
+        const float f = attn_merge_weight(m[p], M);
+#pragma unroll
+        for (int dt = 0; dt < NDT; ++dt) {
+            f32x4 o = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int tt = 0; tt < ATT_TPW; ++tt) {
+                const i32x4 v = kv[((p * ATT_TPW + tt) * NDT + dt) * 64 + lane];
+                o = mfma_step<ET_BF16>(v, Pf[tt], o);
+                o = mfma_step<ET_BF16>(v, Pl[tt], o);
+            }
+            attn_merge_o(acc[dt], o, f);
+        }
+        attn_merge_l(L, lp, f);
+    }
+    const int t = t0 + r;
+    if (tv && t < T) {
+        const size_t o = ((size_t)split * a.H + head) * T + t;
+#pragma unroll
+        for (int dt = 0; dt < NDT; ++dt) *(f32x4*)(a.part_o + o * HD + 16 * dt + 4 * g) = acc[dt];
+        if (g == 0) *(float2*)(a.part_ml + o * 2) = make_float2(M, L);
     }
 }
 
@@ -1040,27 +1225,35 @@ hipError_t launch_attention(int atype, const AttnArgs& a, hipStream_t s) {
     }
     const int S = attention_splits_win(a.Lc_host, a.n_tree_host, a.win_sink, a.win_len);
     const int G = a.H / a.Hkv, Tp = (a.T + 15) & ~15;
-    // 16-row query tiles per workgroup: one (the most workgroups, the
-    // shortest critical path: the 7B 32-node tree at context 1024) unless
-    // the grid of (split, kv head, query tile) units is large and every query
-    // head has its own K/V.  Then two tiles share each K/V load, which halves
-    // the per-CU key traffic (13B 64 nodes at 2048: 32.6 -> 28.7 us per layer;
-    // 7B 128 nodes at 8192: 181 -> 112 us).  Grouped-query models gained
-    // nothing from it (8B 64 nodes at 4096: 35.1 -> 35.8 us).
-    const int nct = G * Tp / 16;
-    const int JT = (G == 1 && S * a.Hkv * nct >= 1024) ? 2 : 1;
-    const int nrc = (nct + JT - 1) / JT;
+    const int nct = G * Tp / 16;  // 16-row query tiles per kv head
     if (a.ctx_cap % 32 || S > ATT_MAX_SPLITS) return hipErrorInvalidValue;
     const float scale_log2 = (1.0f / sqrtf((float)a.hd)) * 1.4426950408889634f;
     // the merge: 4 query rows per workgroup, i.e. many small workgroups
     // (7B layer: attention + merge 12.1 us against 14.2 with 16 rows)
     const dim3 mg((a.T + 3) / 4, a.H);
+    // Four or more query tiles per kv head, each head with at least 32 rows:
+    // four tiles per workgroup share one pass of the split's K/V through LDS
+    // (k_attn_rows; per layer, 8B 64 nodes at 4096: 27.7 -> 23.3 us, 13B 64
+    // nodes at 2048: 22.7 -> 19.3 us, 7B 128 nodes at 8192: 112 -> 65 us).
+    // A single-token call of a grouped-query model has four tiles of one row
+    // each and keeps the larger grid of k_attn_bf16 (8B one node at 4096:
+    // 3.80 ms per forward against 3.91 with k_attn_rows).  Both kernels give
+    // the same bits for a row.  Otherwise the split's
+    // key tiles spread over four waves (k_attn_bf16), one 16-row tile per
+    // workgroup unless the grid of (split, kv head, tile) units is large; then
+    // two tiles share each K/V load (7B 32 nodes at 8192: fewer, longer
+    // workgroups halve the per-CU key traffic).
+    const bool rows = nct >= 4 && Tp >= 32;
+    const int JT = (G == 1 && S * a.Hkv * nct >= 1024) ? 2 : 1;
+    const int nrc = (nct + JT - 1) / JT;
     if (a.hd == 128) {
-        if (JT == 2) hipLaunchKernelGGL((k_attn_bf16<128, 2>), dim3(S, a.Hkv, nrc), dim3(256), 0, s, a, scale_log2);
+        if (rows) hipLaunchKernelGGL((k_attn_rows<128, 4>), dim3(S, a.Hkv, (nct + 3) / 4), dim3(256), 0, s, a, scale_log2);
+        else if (JT == 2) hipLaunchKernelGGL((k_attn_bf16<128, 2>), dim3(S, a.Hkv, nrc), dim3(256), 0, s, a, scale_log2);
         else hipLaunchKernelGGL((k_attn_bf16<128, 1>), dim3(S, a.Hkv, nrc), dim3(256), 0, s, a, scale_log2);
         hipLaunchKernelGGL((k_attn_merge<128, 4>), mg, dim3(128), 0, s, a, S);
     } else if (a.hd == 64) {
-        if (JT == 2) hipLaunchKernelGGL((k_attn_bf16<64, 2>), dim3(S, a.Hkv, nrc), dim3(256), 0, s, a, scale_log2);
+        if (rows) hipLaunchKernelGGL((k_attn_rows<64, 4>), dim3(S, a.Hkv, (nct + 3) / 4), dim3(256), 0, s, a, scale_log2);
+        else if (JT == 2) hipLaunchKernelGGL((k_attn_bf16<64, 2>), dim3(S, a.Hkv, nrc), dim3(256), 0, s, a, scale_log2);
         else hipLaunchKernelGGL((k_attn_bf16<64, 1>), dim3(S, a.Hkv, nrc), dim3(256), 0, s, a, scale_log2);
         hipLaunchKernelGGL((k_attn_merge<64, 4>), mg, dim3(64), 0, s, a, S);
     } else {

@@ -314,16 +314,19 @@ def test_validation_errors_leave_state_unchanged(weights):
     g.close()
 
 
-@pytest.mark.parametrize("name", ["tiny", "mha_small"])
+@pytest.mark.parametrize("name", ["tiny", "mha_small", "gqa_small"])
 def test_root_row_is_bit_identical_for_every_tree_size(weights, name):
     """The verify kernels reduce every row in an order that does not depend on
     how many rows the call has: split-K ranges are chunk-aligned and the split
     count depends on the matrix only; the attention of the root sees the same
-    slots.  So the root's logits are the same bits for T = 1 (plain greedy
-    decoding) and for trees of 2, 4 and 8 column tiles, which makes greedy
-    speculative output equal greedy decoding exactly.  The MHA shape has
-    down-projection chunks (22) that its split count (8) does not divide."""
-    shape = {"tiny": TINY, "mha_small": MHA}[name]
+    slots, reduced in the same parts and order whichever attention kernel the
+    call's query-tile count selects (the MHA shape at T = 70 has five tiles per
+    kv head, the other sizes fewer).  So the root's logits are the same bits
+    for T = 1 (plain greedy decoding) and for trees of 2, 4 and 8 column
+    tiles, which makes greedy speculative output equal greedy decoding
+    exactly.  The MHA shape has down-projection chunks (22) that its split
+    count (8) does not divide."""
+    shape = {"tiny": TINY, "mha_small": MHA, "gqa_small": GQA}[name]
     g = cas.Model(shape, max_ctx=512)
     g.load_weights(weights[name])
     prompt = [int(x) for x in synth.gen_prompt(shape.vocab, 50, seed=5)]
