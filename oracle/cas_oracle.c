@@ -34,7 +34,10 @@
  *   - int8 activations: per row s = amax/127 (fp32), q = clamp(rne(x/s),
  *     -127, 127), exact integer dot products, y = (fp32(acc) * s) * s_w[n] in
  *     fp32; weights: per output channel, the same rule.  Zero rows give s = 0
- *     and q = 0.  The LM head, attention and KV cache keep full precision.
+ *     and q = 0.  The LM head, attention and KV cache keep full precision;
+ *   - int4 activations against int4 weights (the W4A4 form of activation
+ *     quantisation the paper names, Sec. 4.1 and App. C): the same rules with
+ *     7 in place of 127, codes in [-7, 7].
  */
 #include <math.h>
 #include <stdint.h>
@@ -51,6 +54,8 @@ typedef struct {
     const float *attn_norm, *ffn_norm;
     const int8_t *q8[W_COUNT];        /* int8 copy (per output channel) */
     const float *s8[W_COUNT];
+    const int8_t *q4[W_COUNT];        /* int4 copy: codes in [-7, 7], one per byte */
+    const float *s4[W_COUNT];
 } om_layer;
 
 typedef struct {
@@ -110,26 +115,30 @@ static void linear_f64(const om_model *m, const void *w, int out, int in,
     }
 }
 
-/* Per-row symmetric int8 quantisation (fp32 arithmetic, see header). */
-void om_quant_row(const float *x, int n, int8_t *q, float *scale) {
+/* Per-row symmetric quantisation to codes in [-qmax, qmax] (qmax 127: int8,
+ * 7: int4), fp32 arithmetic, see header. */
+void om_quant_row_q(const float *x, int n, int qmax, int8_t *q, float *scale) {
+    const float qm = (float)qmax;
     float amax = 0.0f;
     for (int k = 0; k < n; k++) {
         float a = fabsf(x[k]);
         if (a > amax) amax = a;
     }
-    float s = amax / 127.0f;
+    float s = amax / qm;
     *scale = s;
     for (int k = 0; k < n; k++) {
         if (s == 0.0f) { q[k] = 0; continue; }
         float r = rintf(x[k] / s);
-        if (r > 127.0f) r = 127.0f;
-        if (r < -127.0f) r = -127.0f;
+        if (r > qm) r = qm;
+        if (r < -qm) r = -qm;
         q[k] = (int8_t)r;
     }
 }
+void om_quant_row(const float *x, int n, int8_t *q, float *scale) { om_quant_row_q(x, n, 127, q, scale); }
 
-/* Per-output-channel int8 copy of a weight matrix [out][in] (bf16 bits or float). */
-void om_quant_weight(const void *w, int bf16, int out, int in, int8_t *q, float *scale) {
+/* Per-output-channel copy of a weight matrix [out][in] (bf16 bits or float),
+ * codes in [-qmax, qmax]. */
+void om_quant_weight_q(const void *w, int bf16, int out, int in, int qmax, int8_t *q, float *scale) {
     #pragma omp parallel
     {
         float *row = (float *)malloc(sizeof(float) * (size_t)in);
@@ -140,10 +149,13 @@ void om_quant_weight(const void *w, int bf16, int out, int in, int8_t *q, float 
                 row[k] = bf16 ? (float)bf16_bits_to_double(((const uint16_t *)w)[idx])
                               : ((const float *)w)[idx];
             }
-            om_quant_row(row, in, q + (size_t)o * in, scale + o);
+            om_quant_row_q(row, in, qmax, q + (size_t)o * in, scale + o);
         }
         free(row);
     }
+}
+void om_quant_weight(const void *w, int bf16, int out, int in, int8_t *q, float *scale) {
+    om_quant_weight_q(w, bf16, out, in, 127, q, scale);
 }
 
 /* Exact integer dot product (int64), reported as int32 (|acc| < 2^31 is checked). */
@@ -155,8 +167,9 @@ int om_dot_i8(const int8_t *a, const int8_t *b, int n, int32_t *out) {
     return 0;
 }
 
-/* int8 activation path of one linear layer for the rows with run[r] set. */
-static int linear_i8(const int8_t *wq, const float *ws, int out, int in,
+/* Quantised-activation path of one linear layer (codes in [-qmax, qmax]
+ * against the matching weight copy) for the rows with run[r] set. */
+static int linear_iq(const int8_t *wq, const float *ws, int qmax, int out, int in,
                      const double *x, int xstride, double *y, int ystride,
                      int nrows, const uint8_t *run) {
     int8_t *qx = (int8_t *)malloc((size_t)nrows * in);
@@ -166,7 +179,7 @@ static int linear_i8(const int8_t *wq, const float *ws, int out, int in,
     for (int r = 0; r < nrows; r++) {
         if (!run[r]) continue;
         for (int k = 0; k < in; k++) row[k] = (float)x[(size_t)r * xstride + k];
-        om_quant_row(row, in, qx + (size_t)r * in, sx + r);
+        om_quant_row_q(row, in, qmax, qx + (size_t)r * in, sx + r);
     }
     free(row);
     #pragma omp parallel for schedule(static) reduction(|:bad)
@@ -270,6 +283,9 @@ void om_set_layer(om_model *m, int l, const void *const *w, const float *attn_no
     m->layers[l].ffn_norm = ffn_norm;
 }
 
+void om_set_layer_i4(om_model *m, int l, const int8_t *const *q, const float *const *s) {
+    for (int i = 0; i < W_COUNT; i++) { m->layers[l].q4[i] = q[i]; m->layers[l].s4[i] = s[i]; }
+}
 void om_set_layer_i8(om_model *m, int l, const int8_t *const *q, const float *const *s) {
     for (int i = 0; i < W_COUNT; i++) { m->layers[l].q8[i] = q[i]; m->layers[l].s8[i] = s[i]; }
 }
@@ -340,7 +356,8 @@ int om_set_window(om_model *m, int sink, int window) {
  * Forward over n new tree nodes (ids node_offset .. node_offset+n-1 of the
  * current round).  node_offset 0 starts a new round; otherwise the call
  * appends to the round.  parents are node ids (root: -1, only node 0).
- * skip: per-layer 0/1 (NULL = none).  act_quant: int8 activations.
+ * skip: per-layer 0/1 (NULL = none).  act_quant: 0, 1 = int8 activations
+ * against the int8 copy, 2 = int4 activations against the int4 copy.
  * need: rows whose logits are wanted (NULL = all); their ancestors inside the
  * call are computed too, other rows are left out (their KV is not written).
  * logits: [n][V] doubles (rows not computed are untouched).
@@ -348,7 +365,7 @@ int om_set_window(om_model *m, int sink, int window) {
  */
 int om_forward(om_model *m, const int32_t *tokens, const int32_t *parents, int node_offset, int n,
                const uint8_t *skip, int act_quant, const uint8_t *need, double *logits) {
-    if (n <= 0 || node_offset < 0) return -1;
+    if (n <= 0 || node_offset < 0 || act_quant < 0 || act_quant > 2) return -1;
     if (node_offset != 0 && node_offset != m->n_nodes) return -1;
     if (m->Lc + node_offset + n > m->max_ctx) return -1;
     for (int i = 0; i < n; i++) {
@@ -360,7 +377,8 @@ int om_forward(om_model *m, const int32_t *tokens, const int32_t *parents, int n
     if (act_quant) {
         for (int l = 0; l < m->L; l++) {
             if (skip && skip[l]) continue;
-            for (int w = 0; w < W_COUNT; w++) if (!m->layers[l].q8[w]) return -1;
+            for (int w = 0; w < W_COUNT; w++)
+                if (!(act_quant == 1 ? m->layers[l].q8[w] : m->layers[l].q4[w])) return -1;
         }
     }
     const int d = m->d, H = m->H, Hkv = m->Hkv, hd = m->hd, ffn = m->ffn, G = H / Hkv;
@@ -405,7 +423,9 @@ int om_forward(om_model *m, const int32_t *tokens, const int32_t *parents, int n
 #define LINEAR(widx, out, in, X, xs, Y, ys)                                                     \
     do {                                                                                        \
         if (act_quant) {                                                                        \
-            if (linear_i8(lay->q8[widx], lay->s8[widx], out, in, X, xs, Y, ys, n, run)) rc = -2; \
+            if (act_quant == 1 ? linear_iq(lay->q8[widx], lay->s8[widx], 127, out, in, X, xs, Y, ys, n, run) \
+                               : linear_iq(lay->q4[widx], lay->s4[widx], 7, out, in, X, xs, Y, ys, n, run))   \
+                rc = -2;                                                                        \
         } else {                                                                                \
             linear_f64(m, lay->w[widx], out, in, X, xs, Y, ys, n, run);                          \
         }                                                                                       \

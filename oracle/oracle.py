@@ -49,6 +49,7 @@ def lib():
         L.om_set_global.argtypes = [P, P, P, P]
         L.om_set_layer.argtypes = [P, I, P, P, P]
         L.om_set_layer_i8.argtypes = [P, I, P, P]
+        L.om_set_layer_i4.argtypes = [P, I, P, P]
         L.om_set_threads.argtypes = [I]
         L.om_threads.restype = I
         L.om_set_kv.argtypes = [P, I, I, P, P]
@@ -69,6 +70,8 @@ def lib():
         L.om_round_bf16.restype = D
         L.om_quant_row.argtypes = [P, I, P, P]
         L.om_quant_weight.argtypes = [P, I, I, I, P, P]
+        L.om_quant_row_q.argtypes = [P, I, I, P, P]
+        L.om_quant_weight_q.argtypes = [P, I, I, I, I, P, P]
         L.om_dot_i8.argtypes = [P, P, I, P]
         L.om_dot_i8.restype = I
         L.om_rmsnorm_row.argtypes = [P, P, I, D, P]
@@ -98,24 +101,26 @@ def round_bf16(x: float) -> float:
     return float(lib().om_round_bf16(float(x)))
 
 
-def quant_rows(x: np.ndarray) -> Tuple[np.ndarray, np.ndarray]:
-    """Per-row symmetric int8 quantisation of float32 rows -> (int8 q, float32 scale)."""
+def quant_rows(x: np.ndarray, qmax: int = 127) -> Tuple[np.ndarray, np.ndarray]:
+    """Per-row symmetric quantisation of float32 rows to codes in [-qmax, qmax]
+    (127: int8, 7: int4) -> (int8 q, float32 scale)."""
     x = np.ascontiguousarray(x, dtype=np.float32)
     rows, cols = x.shape
     q = np.zeros((rows, cols), dtype=np.int8)
     s = np.zeros(rows, dtype=np.float32)
     for r in range(rows):
-        lib().om_quant_row(_ptr(x[r]), cols, _ptr(q[r]), s[r:].ctypes.data)
+        lib().om_quant_row_q(_ptr(x[r]), cols, int(qmax), _ptr(q[r]), s[r:].ctypes.data)
     return q, s
 
 
-def quant_weight(w: np.ndarray, bf16: bool) -> Tuple[np.ndarray, np.ndarray]:
-    """Per-output-channel int8 copy of W[out][in] (uint16 bf16 bits or float32)."""
+def quant_weight(w: np.ndarray, bf16: bool, qmax: int = 127) -> Tuple[np.ndarray, np.ndarray]:
+    """Per-output-channel copy of W[out][in] (uint16 bf16 bits or float32),
+    codes in [-qmax, qmax]."""
     w = np.ascontiguousarray(w)
     out, inn = w.shape
     q = np.zeros((out, inn), dtype=np.int8)
     s = np.zeros(out, dtype=np.float32)
-    lib().om_quant_weight(_ptr(w), 1 if bf16 else 0, out, inn, _ptr(q), _ptr(s))
+    lib().om_quant_weight_q(_ptr(w), 1 if bf16 else 0, out, inn, int(qmax), _ptr(q), _ptr(s))
     return q, s
 
 
@@ -175,7 +180,7 @@ def matmul_rows(x: np.ndarray, w: np.ndarray, bf16: bool) -> np.ndarray:
 class OracleModel:
     """A decoder with its own fp64 KV cache, mirroring the tree-forward API."""
 
-    def __init__(self, shape, weights: Dict, max_ctx: int, int8: bool = False):
+    def __init__(self, shape, weights: Dict, max_ctx: int, int8: bool = False, int4: bool = False):
         self.shape = shape
         self.bf16 = shape.dtype == "bf16"
         self.max_ctx = int(max_ctx)
@@ -200,16 +205,19 @@ class OracleModel:
             fn_ = self._hold(np.asarray(lw["ffn_norm"], dtype=np.float32))
             L.om_set_layer(self.h, l, ctypes.cast(ptrs, ctypes.c_void_p), _ptr(an), _ptr(fn_))
             self._layers_set[l] = True
-            if int8:
+            for on, qmax, setter in ((int8, 127, L.om_set_layer_i8), (int4, 7, L.om_set_layer_i4)):
+                if not on:
+                    continue
                 qs, ss = [], []
                 for n in W_ORDER:
-                    q, s = quant_weight(lw[n], self.bf16)
+                    q, s = quant_weight(lw[n], self.bf16, qmax)
                     qs.append(self._hold(q))
                     ss.append(self._hold(s))
                 qp = (ctypes.c_void_p * 7)(*[_ptr(a) for a in qs])
                 sp = (ctypes.c_void_p * 7)(*[_ptr(a) for a in ss])
-                L.om_set_layer_i8(self.h, l, ctypes.cast(qp, ctypes.c_void_p), ctypes.cast(sp, ctypes.c_void_p))
+                setter(self.h, l, ctypes.cast(qp, ctypes.c_void_p), ctypes.cast(sp, ctypes.c_void_p))
         self.int8 = bool(int8)
+        self.int4 = bool(int4)
 
     def _hold(self, a: np.ndarray) -> np.ndarray:
         a = np.ascontiguousarray(a)
@@ -247,11 +255,13 @@ class OracleModel:
 
     # the step ----------------------------------------------------------------
     def forward(self, tokens: Sequence[int], parents: Sequence[int], node_offset: int = 0,
-                skip: Optional[Sequence[int]] = None, act_quant: bool = False,
+                skip: Optional[Sequence[int]] = None, act_quant: int = 0,
                 need: Optional[Sequence[bool]] = None,
                 attn_window: Optional[Tuple[int, int]] = None) -> np.ndarray:
-        """attn_window = (sink, window): efficient-attention draft that sees
-        only the first sink and the last window committed slots."""
+        """act_quant: 0, 1 (or True) = int8 activations against the int8 copy,
+        2 = int4 activations against the int4 copy.  attn_window = (sink,
+        window): efficient-attention draft that sees only the first sink and
+        the last window committed slots."""
         sink, win = attn_window if attn_window else (0, 0)
         if lib().om_set_window(self.h, int(sink), int(win)):
             raise ValueError("bad attention window")
@@ -274,7 +284,7 @@ class OracleModel:
         need_a = None if need is None else np.ascontiguousarray([1 if x else 0 for x in need], dtype=np.uint8)
         logits = np.zeros((n, self.shape.vocab), dtype=np.float64)
         rc = lib().om_forward(self.h, _ptr(toks), _ptr(par), int(node_offset), n,
-                              None if skip_a is None else _ptr(skip_a), 1 if act_quant else 0,
+                              None if skip_a is None else _ptr(skip_a), int(act_quant),
                               None if need_a is None else _ptr(need_a), _ptr(logits))
         if rc == -2:
             raise OverflowError("int8 accumulator overflow")

@@ -61,11 +61,27 @@ def _rope_complex(x, pos, theta):
     return torch.cat([z.real, z.imag], dim=-1)
 
 
-def textbook_logits(shape, w, tokens, round_bf16=False, mask=None):
+def _qlin(x, w, bf16, qmax):
+    """x @ W^T as a quantised linear layer: per-row codes of x and
+    per-output-channel codes of W (the oracle's pinned quantisers), an exact
+    int64 product, then (fp32(acc) * s_x) * s_w in float32."""
+    xq, sx = O.quant_rows(x.numpy().astype(np.float32), qmax)
+    wq, sw = O.quant_weight(w, bf16, qmax)
+    acc = xq.astype(np.int64) @ wq.astype(np.int64).T
+    y = (acc.astype(np.float32) * sx[:, None]) * sw[None, :]
+    return torch.from_numpy(y.astype(np.float64))
+
+
+def textbook_logits(shape, w, tokens, round_bf16=False, mask=None, qmax=None):
     """Causal decoder over `tokens` from library routines, float64.  With
     round_bf16 the storage points round through torch's bfloat16 cast; mask
-    ([S][S] bool, True = visible) replaces the causal mask."""
+    ([S][S] bool, True = visible) replaces the causal mask; qmax (127 or 7)
+    makes the seven projections of every layer quantised linear layers."""
     bf16 = shape.dtype == "bf16"
+    if qmax is None:
+        mm = lambda x, a: x @ _w64(a, bf16).T
+    else:
+        mm = lambda x, a: _qlin(x, a, bf16, qmax)
     rb = (lambda t: t.to(torch.float32).to(torch.bfloat16).to(torch.float64)) if round_bf16 else (lambda t: t)
     S = len(tokens)
     H, Hkv, hd = shape.n_heads, shape.n_kv_heads, shape.head_dim
@@ -73,9 +89,9 @@ def textbook_logits(shape, w, tokens, round_bf16=False, mask=None):
     x = _w64(w["embed"], bf16)[torch.as_tensor(np.asarray(tokens, dtype=np.int64))]
     for lw in w["layers"]:
         xn = rb(F.rms_norm(x, (shape.d_model,), weight=torch.from_numpy(lw["attn_norm"]).double(), eps=shape.rms_eps))
-        q = (xn @ _w64(lw["wq"], bf16).T).view(S, H, hd)
-        k = (xn @ _w64(lw["wk"], bf16).T).view(S, Hkv, hd)
-        v = (xn @ _w64(lw["wv"], bf16).T).view(S, Hkv, hd)
+        q = mm(xn, lw["wq"]).view(S, H, hd)
+        k = mm(xn, lw["wk"]).view(S, Hkv, hd)
+        v = mm(xn, lw["wv"]).view(S, Hkv, hd)
         q = rb(_rope_complex(q, pos, shape.rope_theta))
         k = rb(_rope_complex(k, pos, shape.rope_theta))
         v = rb(v)
@@ -87,10 +103,10 @@ def textbook_logits(shape, w, tokens, round_bf16=False, mask=None):
                                                v.transpose(0, 1)[None], attn_mask=torch.as_tensor(mask),
                                                enable_gqa=True)
         o = rb(o[0].transpose(0, 1).reshape(S, H * hd))
-        x = x + o @ _w64(lw["wo"], bf16).T
+        x = x + mm(o, lw["wo"])
         xn = rb(F.rms_norm(x, (shape.d_model,), weight=torch.from_numpy(lw["ffn_norm"]).double(), eps=shape.rms_eps))
-        s = rb(F.silu(xn @ _w64(lw["w_gate"], bf16).T) * (xn @ _w64(lw["w_up"], bf16).T))
-        x = x + s @ _w64(lw["w_down"], bf16).T
+        s = rb(F.silu(mm(xn, lw["w_gate"])) * mm(xn, lw["w_up"]))
+        x = x + mm(s, lw["w_down"])
     xn = rb(F.rms_norm(x, (shape.d_model,), weight=torch.from_numpy(w["final_norm"]).double(), eps=shape.rms_eps))
     return (xn @ _w64(w["lm_head"], bf16).T).numpy()
 
@@ -339,6 +355,85 @@ def test_int8_draft_approximates_full(tiny):
     q8 = m.forward(toks, parents, act_quant=True)
     err = np.abs(full - q8).max() / np.abs(full).max()
     assert 0 < err < 0.1, err
+
+
+# ---------------------------------------------------------------- int4 (W4A4)
+
+def test_quant_rows_int4_properties():
+    x = synth.gen_activations(64, 688, seed=13)
+    x[5] = 0.0
+    q, s = O.quant_rows(x, 7)
+    for r in range(x.shape[0]):
+        amax = np.abs(x[r]).max()
+        if amax == 0:
+            assert s[r] == 0 and not q[r].any()
+            continue
+        assert s[r] == np.float32(amax) / np.float32(7.0)
+        assert np.abs(q[r]).max() == 7
+        i = np.argmax(np.abs(x[r]))
+        assert q[r][i] == np.sign(x[r][i]) * 7
+        err = np.abs(x[r].astype(np.float64) - q[r].astype(np.float64) * np.float64(s[r]))
+        assert (err <= 0.5 * np.float64(s[r]) * (1 + 1e-6)).all()
+
+
+def test_quant_int4_worked_example():
+    """amax 3.5 gives the scale 0.5 exactly; x / s = 7, -3.5, 0.5, 0, -7, 2.5,
+    1.5 round half to even: 7, -4, 0, 0, -7, 2, 2."""
+    x = np.array([[3.5, -1.75, 0.25, 0.0, -3.5, 1.25, 0.75]], dtype=np.float32)
+    q, s = O.quant_rows(x, 7)
+    assert s[0] == np.float32(0.5)
+    assert q[0].tolist() == [7, -4, 0, 0, -7, 2, 2]
+
+
+@pytest.mark.parametrize("bf16", [False, True])
+def test_quant_weight_int4_recovers_representable_rows(bf16):
+    """Rows that are a power-of-two scale 2^-e times integer codes in [-7, 7]
+    (each row with a +-7) quantise back to exactly those codes, with the scale
+    amax / 7 = 2^-e."""
+    rng = np.random.default_rng(14)
+    codes = rng.integers(-7, 8, (48, 200))
+    codes[np.arange(48), rng.integers(0, 200, 48)] = rng.choice([-7, 7], 48)
+    scale = 2.0 ** -rng.integers(3, 9, 48)
+    w = (codes * scale[:, None]).astype(np.float32)
+    arr = synth.f32_to_bf16_bits(w) if bf16 else w
+    q, s = O.quant_weight(arr, bf16, 7)
+    assert np.array_equal(q.astype(np.int64), codes)
+    assert np.array_equal(s.astype(np.float64), scale)
+
+
+@pytest.mark.parametrize("which,qmax", [("tiny", 127), ("tiny", 7), ("small", 127), ("small", 7)])
+def test_quantised_forward_equals_textbook(which, qmax, tiny, small):
+    """The oracle's act_quant forward (1: W8A8, 2: W4A4) over a chain equals the
+    textbook decoder whose seven projections per layer are quantised linear
+    layers (codes of the rounded inputs and of the weights, exact integer
+    products, fp32 dequantisation); the LM head stays full precision."""
+    shape, w = (TINY, tiny) if which == "tiny" else (SMALL_BF16, small)
+    bf16 = shape.dtype == "bf16"
+    toks = [int(t) for t in synth.gen_prompt(shape.vocab, 9, seed=15)]
+    m = O.OracleModel(shape, w, max_ctx=32, int8=qmax == 127, int4=qmax == 7)
+    got = m.forward(toks, list(range(-1, len(toks) - 1)), act_quant=1 if qmax == 127 else 2)
+    ref = textbook_logits(shape, w, toks, round_bf16=bf16, qmax=qmax)
+    err = np.abs(got - ref).max() / np.abs(ref).max()
+    assert err < 1e-9, err
+
+
+def test_int4_draft_is_coarser_than_int8(tiny):
+    """Both quantised drafts approximate the same model, int4 less closely."""
+    parents = synth.tree_from_branching((3, 2, 1), 15)
+    toks = synth.gen_tree_tokens(parents, TINY.vocab, seed=24)
+    m = O.OracleModel(TINY, tiny, max_ctx=64, int8=True, int4=True)
+    full = m.forward(toks, parents)
+    e8 = np.abs(full - m.forward(toks, parents, act_quant=1)).max() / np.abs(full).max()
+    e4 = np.abs(full - m.forward(toks, parents, act_quant=2)).max() / np.abs(full).max()
+    assert 0 < e8 < e4 < 1.0, (e8, e4)
+
+
+def test_int4_forward_needs_its_copy(tiny):
+    m = O.OracleModel(TINY, tiny, max_ctx=32, int8=True)
+    with pytest.raises(ValueError):
+        m.forward([1, 2], [-1, 0], act_quant=2)
+    with pytest.raises(ValueError):
+        m.forward([1, 2], [-1, 0], act_quant=3)
 
 
 # ---------------------------------------------------------------- acceptance, compaction, losslessness
