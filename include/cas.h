@@ -9,7 +9,8 @@
  *   - the "virtual" draft models that a DSIA strategy switches on per call
  *     (Def. 4.1; Sec. 4.1 strategy list): layer sparsity (skip_mask) and
  *     activation quantisation (act_quant: per-token int8 activations against a
- *     per-output-channel int8 copy of the weights, App. C), including the
+ *     per-output-channel int8 copy of the weights, or the W4A4 form with int4
+ *     codes on both sides, App. C), including the
  *     tree-parallel draft calls over a leaf and its siblings (Sec. 4.2,
  *     "Tree-based Parallel Draft Generation").
  * cas_accept_tree performs greedy verification of the tree (lossless decoding,
@@ -104,6 +105,13 @@ cas_status cas_load_tensor(cas_ctx* ctx, int32_t tensor, int32_t layer, const vo
  * Required before act_quant calls (App. C, activation quantisation). */
 cas_status cas_build_int8(cas_ctx* ctx);
 
+/* Build the per-output-channel int4 copy of the same projections (the W4A4
+ * form of activation quantisation, Sec. 4.1 and App. C): s[n] = max_k
+ * |W[n][k]| / 7 (fp32), q = clamp(round-half-even(W/s), +-7), stored as 4-bit
+ * codes (half the bytes of the int8 copy).  Required before act_quant = 2
+ * calls.  Loading any tensor invalidates both copies. */
+cas_status cas_build_int4(cas_ctx* ctx);
+
 /* Commit n tokens as a causal sequence after the committed prefix (prefill),
  * in chunks of at most max_tree.  Leaves no round open. */
 cas_status cas_prefill(cas_ctx* ctx, const int32_t* tokens, int32_t n);
@@ -133,9 +141,12 @@ cas_status cas_committed_len(const cas_ctx* ctx, int32_t* n);
  *   skip_mask       NULL (full depth) or n_layers bytes, 1 = skip that layer
  *                   (layer sparsity); a skipped layer is the identity on the
  *                   residual stream and writes no KV
- *   act_quant       0, or 1 = int8 activations for every linear layer of the
- *                   non-skipped layers (needs cas_build_int8); the LM head,
- *                   attention and KV cache keep the model's precision
+ *   act_quant       0; 1 = int8 activations for every linear layer of the
+ *                   non-skipped layers (needs cas_build_int8); 2 = int4
+ *                   activations against the int4 copy (W4A4, needs
+ *                   cas_build_int4).  Codes are per token: s = amax / 127 or
+ *                   / 7.  The LM head, attention and KV cache keep the
+ *                   model's precision
  *   logits_host     NULL keeps logits on the device; else [n][vocab] float32
  *                   copied out (synchronous)
  * Limits: node_offset + n <= max_tree, Lc + node_offset + n <= max_ctx.
@@ -155,8 +166,9 @@ cas_status cas_logits_device(const cas_ctx* ctx, const float** dptr, int32_t* n)
  * with one or more of these strategies switched on for the call (Sec. 4.1):
  *   skip_mask    layer sparsity: NULL or n_layers bytes, 1 = skip that layer
  *                (a suffix of skipped layers is early exit)
- *   act_quant    activation quantisation: 0, or 1 = per-token int8
- *                activations (needs cas_build_int8)
+ *   act_quant    activation quantisation: 0; 1 = per-token int8
+ *                activations (needs cas_build_int8); 2 = W4A4 (needs
+ *                cas_build_int4)
  *   attn_sink,   efficient attention (StreamingLLM-style): attn_window > 0
  *   attn_window  limits the committed slots each row attends to to the first
  *                attn_sink and the last attn_window ones (tree ancestors stay

@@ -18,26 +18,29 @@
 extern "C" {
 #endif
 
-typedef enum { CAS_W_F32 = 0, CAS_W_BF16 = 1, CAS_W_I8 = 2 } cas_wtype;
+typedef enum { CAS_W_F32 = 0, CAS_W_BF16 = 1, CAS_W_I8 = 2, CAS_W_I4 = 3 } cas_wtype;
 typedef enum {
     CAS_EPI_STORE = 0,   /* out[t*ldo + n] = y (float32) */
     CAS_EPI_RESID = 1,   /* out[t*ldo + n] += y (float32 residual stream) */
-    CAS_EPI_RAW_I32 = 2  /* out[t*ldo + n] = integer accumulator (int32; int8 only) */
+    CAS_EPI_RAW_I32 = 2  /* out[t*ldo + n] = integer accumulator (int32; int8 and int4 only) */
 } cas_epi;
 
 /*
  * Linear layer y[t][n] = sum_k X[t][k] W[n][k] for t < T, n < N (the weight
  * streaming GEMM of every projection and the LM head).
- *   W: [N][K] row-major, element type wtype (float32, bf16 bits, int8)
- *   X: [T][K] row-major, same element type as W
- *   xs, ws: for CAS_W_I8 the per-row activation scales [T] and per-output
- *           channel weight scales [N]; y = (float(acc) * xs[t]) * ws[n]
+ *   W: [N][K] row-major, element type wtype (float32, bf16 bits, int8; for
+ *      CAS_W_I4 int8 codes in [-7, 7], which the library packs to 4 bits)
+ *   X: [T][K] row-major, same element type as W (int8 codes for CAS_W_I4)
+ *   xs, ws: for CAS_W_I8 / CAS_W_I4 the per-row activation scales [T] and
+ *           per-output channel weight scales [N]; y = (float(acc) * xs[t]) * ws[n]
  *           (ignored for the other types; unused with CAS_EPI_RAW_I32)
  *   work: device scratch of at least cas_op_gemm_work_bytes(...) bytes; the
  *         operands are first rearranged there into the fragment-tiled layout
  *         the kernel streams (the layout the library keeps its weights in)
  * Limits: N multiple of 16, K multiple of 16, 1 <= T <= 128.
- * Accumulation: fp32 (float32, bf16 inputs), exact int32 (int8 inputs).
+ * Accumulation: fp32 (float32, bf16 inputs), exact int32 (int8 and int4
+ * inputs; the W4A4 form of activation quantisation, Sec. 4.1 and App. C, runs
+ * its int4 codes on the int8 MFMA).
  */
 size_t cas_op_gemm_work_bytes(int32_t wtype, int32_t N, int32_t K, int32_t T);
 cas_status cas_op_gemm(int32_t wtype, const void* W, const void* X, int32_t N, int32_t K, int32_t T,
@@ -52,6 +55,10 @@ cas_status cas_op_gemm(int32_t wtype, const void* W, const void* X, int32_t N, i
  */
 cas_status cas_op_quant_rows(int32_t atype, const void* x, int32_t T, int32_t K,
                              int8_t* q, float* s, void* stream);
+/* The same rule with codes in [-qmax, qmax]: qmax 127 (int8, as above) or 7
+ * (int4 codes of the W4A4 draft, one per int8 byte): s[t] = amax / qmax. */
+cas_status cas_op_quant_rows_q(int32_t atype, const void* x, int32_t T, int32_t K, int32_t qmax,
+                               int8_t* q, float* s, void* stream);
 
 /* Per-output-channel int8 copy of W [N][K] (same rule, one row per output
  * channel), through the library's tiled weight layout: q [N][K] row-major,
@@ -60,6 +67,12 @@ cas_status cas_op_quant_rows(int32_t atype, const void* x, int32_t T, int32_t K,
 size_t cas_op_quant_weight_work_bytes(int32_t wtype, int32_t N, int32_t K);
 cas_status cas_op_quant_weight(int32_t wtype, const void* W, int32_t N, int32_t K,
                                int8_t* q, float* s, void* work, size_t work_bytes, void* stream);
+/* Per-output-channel int4 copy of W (s[n] = amax / 7, codes in [-7, 7]),
+ * through the library's tiled weights and its packed 4-bit layout, returned
+ * unpacked: q [N][K] row-major int8 codes, s [N].  Same arguments, limits and
+ * work size as cas_op_quant_weight. */
+cas_status cas_op_quant_weight_i4(int32_t wtype, const void* W, int32_t N, int32_t K,
+                                  int8_t* q, float* s, void* work, size_t work_bytes, void* stream);
 
 /*
  * Tree-masked attention of one layer (bf16 storage, fp32 softmax):

@@ -21,7 +21,7 @@ OK, ERR_ARG, ERR_TREE, ERR_CAPACITY, ERR_UNSUPPORTED, ERR_OOM, ERR_DEVICE, ERR_S
 STATUS_NAMES = ["CAS_OK", "CAS_ERR_ARG", "CAS_ERR_TREE", "CAS_ERR_CAPACITY", "CAS_ERR_UNSUPPORTED",
                 "CAS_ERR_OOM", "CAS_ERR_DEVICE", "CAS_ERR_STATE"]
 F32, BF16 = 0, 1
-W_F32, W_BF16, W_I8 = 0, 1, 2
+W_F32, W_BF16, W_I8, W_I4 = 0, 1, 2, 3
 EPI_STORE, EPI_RESID, EPI_RAW_I32 = 0, 1, 2
 TENSOR = {"embed": 0, "lm_head": 1, "final_norm": 2, "attn_norm": 3, "ffn_norm": 4, "wq": 5, "wk": 6,
           "wv": 7, "wo": 8, "w_gate": 9, "w_up": 10, "w_down": 11}
@@ -30,10 +30,12 @@ KCLASS = ["embed", "rmsnorm", "gemm_qkv", "attn", "gemm_o", "gemm_gateup", "gemm
 
 # every symbol the two headers declare
 EXPORTS = ("cas_create", "cas_destroy", "cas_last_error", "cas_create_error", "cas_load_tensor", "cas_build_int8",
+           "cas_build_int4",
            "cas_prefill", "cas_kv_load", "cas_kv_read", "cas_set_committed", "cas_committed_len", "cas_forward",
            "cas_logits_device", "cas_forward_draft", "cas_accept_tree", "cas_topk", "cas_kv_compact", "cas_tree_info", "cas_set_graphs",
            "cas_profile", "cas_profile_read", "cas_sync", "cas_op_gemm", "cas_op_gemm_work_bytes",
-           "cas_op_quant_rows", "cas_op_quant_weight", "cas_op_quant_weight_work_bytes", "cas_op_attention",
+           "cas_op_quant_rows", "cas_op_quant_rows_q", "cas_op_quant_weight", "cas_op_quant_weight_i4",
+           "cas_op_quant_weight_work_bytes", "cas_op_attention",
            "cas_op_attention_work_bytes", "cas_op_copy")
 
 
@@ -71,6 +73,7 @@ def lib():
             "cas_create_error": ([], ctypes.c_char_p),
             "cas_load_tensor": ([P, I, I, P, Z], I),
             "cas_build_int8": ([P], I),
+            "cas_build_int4": ([P], I),
             "cas_prefill": ([P, P, I], I),
             "cas_kv_load": ([P, I, P, P, I], I),
             "cas_kv_read": ([P, I, P, P, I], I),
@@ -90,7 +93,9 @@ def lib():
             "cas_op_gemm": ([I, P, P, I, I, I, P, P, I, P, I, P, Z, P], I),
             "cas_op_gemm_work_bytes": ([I, I, I, I], Z),
             "cas_op_quant_rows": ([I, P, I, I, P, P, P], I),
+            "cas_op_quant_rows_q": ([I, P, I, I, I, P, P, P], I),
             "cas_op_quant_weight": ([I, P, I, I, P, P, P, Z, P], I),
+            "cas_op_quant_weight_i4": ([I, P, I, I, P, P, P, Z, P], I),
             "cas_op_quant_weight_work_bytes": ([I, I, I], Z),
             "cas_op_attention": ([P, P, P, I, I, I, I, I, I, I, P, P, P, Z, P], I),
             "cas_op_attention_work_bytes": ([I, I, I, I, I, I, I], Z),
@@ -172,6 +177,10 @@ class Model:
     def build_int8(self) -> None:
         self._chk(lib().cas_build_int8(self.h))
 
+    def build_int4(self) -> None:
+        """The int4 weight copy behind act_quant = 2 (W4A4 drafts)."""
+        self._chk(lib().cas_build_int4(self.h))
+
     # state ----------------------------------------------------------------------
     @property
     def committed(self) -> int:
@@ -202,9 +211,10 @@ class Model:
 
     # the step -------------------------------------------------------------------
     def forward(self, tokens: Sequence[int], parents: Sequence[int], node_offset: int = 0,
-                skip: Optional[Sequence[int]] = None, act_quant: bool = False,
+                skip: Optional[Sequence[int]] = None, act_quant: int = 0,
                 logits: bool = True, attn_window: Optional[Tuple[int, int]] = None) -> Optional[np.ndarray]:
-        """attn_window = (sink, window): efficient-attention draft."""
+        """act_quant: 0, 1 (or True) = W8A8, 2 = W4A4.  attn_window = (sink,
+        window): efficient-attention draft."""
         t = np.ascontiguousarray(tokens, dtype=np.int32)
         p = np.ascontiguousarray(parents, dtype=np.int32)
         n = t.shape[0]
@@ -217,13 +227,13 @@ class Model:
                 raise ValueError("skip mask length")
         out = np.empty((n, self.shape.vocab), dtype=np.float32) if logits else None
         if attn_window:
-            o = DraftOpts(None if sk is None else _p(sk), 1 if act_quant else 0, int(attn_window[0]),
+            o = DraftOpts(None if sk is None else _p(sk), int(act_quant), int(attn_window[0]),
                           int(attn_window[1]))
             self._chk(lib().cas_forward_draft(self.h, _p(t), _p(p), n, int(node_offset), ctypes.byref(o),
                                               None if out is None else _p(out)))
         else:
             self._chk(lib().cas_forward(self.h, _p(t), _p(p), n, int(node_offset), None if sk is None else _p(sk),
-                                        1 if act_quant else 0, None if out is None else _p(out)))
+                                        int(act_quant), None if out is None else _p(out)))
         return out
 
     def logits_device(self) -> Tuple[int, int]:
@@ -299,14 +309,21 @@ def op_gemm(wtype: int, W, X, N: int, K: int, T: int, out, ldo: int, epi: int = 
                             int(work.numel() * work.element_size()), _stream(stream)), "cas_op_gemm")
 
 
-def op_quant_rows(atype: int, x, T: int, K: int, q, s, stream=None) -> None:
-    _ochk(lib().cas_op_quant_rows(atype, _dp(x), T, K, _dp(q), _dp(s), _stream(stream)), "cas_op_quant_rows")
+def op_quant_rows(atype: int, x, T: int, K: int, q, s, stream=None, qmax: int = 127) -> None:
+    if qmax == 127:
+        _ochk(lib().cas_op_quant_rows(atype, _dp(x), T, K, _dp(q), _dp(s), _stream(stream)), "cas_op_quant_rows")
+    else:
+        _ochk(lib().cas_op_quant_rows_q(atype, _dp(x), T, K, int(qmax), _dp(q), _dp(s), _stream(stream)),
+              "cas_op_quant_rows_q")
 
 
-def op_quant_weight(wtype: int, W, N: int, K: int, q, s, stream=None) -> None:
+def op_quant_weight(wtype: int, W, N: int, K: int, q, s, stream=None, qmax: int = 127) -> None:
+    """Per-output-channel copy of W; qmax 127 (int8) or 7 (int4, packed by the
+    library and returned unpacked)."""
     work = _work(lib().cas_op_quant_weight_work_bytes(wtype, N, K))
-    _ochk(lib().cas_op_quant_weight(wtype, _dp(W), N, K, _dp(q), _dp(s), _dp(work),
-                                    int(work.numel()), _stream(stream)), "cas_op_quant_weight")
+    fn = lib().cas_op_quant_weight if qmax == 127 else lib().cas_op_quant_weight_i4
+    _ochk(fn(wtype, _dp(W), N, K, _dp(q), _dp(s), _dp(work), int(work.numel()), _stream(stream)),
+          "cas_op_quant_weight" if qmax == 127 else "cas_op_quant_weight_i4")
 
 
 def op_attention(q, k, v, ctx_cap: int, Lc: int, n_tree: int, T: int, H: int, Hkv: int, hd: int, anc, out,

@@ -7,7 +7,7 @@
 
 namespace cas {
 
-enum ElemType { ET_F32 = 0, ET_BF16 = 1, ET_I8 = 2 };
+enum ElemType { ET_F32 = 0, ET_BF16 = 1, ET_I8 = 2, ET_I4 = 3 };
 
 // ---------------------------------------------------------------------------
 // Fragment-tiled operand layout of the weight-streaming GEMM.
@@ -38,6 +38,19 @@ __host__ __device__ inline size_t xt_off(int t, int k, int NT, int E) {
     const int KC = 16 * E, c = k / KC, kk = k % KC;
     const int g = kk / (4 * E), u = (kk / E) & 3, e = kk % E, lane = g * 16 + (t & 15);
     return ((((size_t)c * FRAG_U + u) * NT + (t >> 4)) * 64 + lane) * E + e;
+}
+
+// Packed int4 weights (ET_I4): codes q in [-7, 7] stored as the nibble q + 8,
+// chunked like int8 (256 k per chunk, the activations keep the int8 layout).
+// A 16-row tile's chunk is two 1 KB blocks: block b holds the int8 steps 2b
+// and 2b + 1, lane (g, r) 16 bytes, bytes [8h, 8h + 8) for step 2b + h, byte j
+// the step's k-offsets j (low nibble) and j + 8 (high nibble).  One wave load
+// of a block feeds two int8 MFMA steps.
+__host__ __device__ inline size_t wt4_byte(int n, int k, int Kp, int* nibble) {
+    const int c = k >> 8, kk = k & 255, g = kk >> 6, u = (kk >> 4) & 3, e = kk & 15;
+    const int lane = g * 16 + (n & 15);
+    *nibble = e >> 3;
+    return ((((size_t)(n >> 4) * (Kp >> 8) + c) * 2 + (u >> 1)) * 64 + lane) * 16 + (u & 1) * 8 + (e & 7);
 }
 
 // ---------------------------------------------------------------------------
@@ -154,14 +167,23 @@ hipError_t launch_kv_convert(int atype, void* kc, void* vt, const void* k_rows, 
 // With nparts > 0 the rows first take the pending split-K sums of the last
 // projection: h += parts[0] + ... + parts[nparts-1] (in that order; part p at
 // parts + p * pstride, [T][d]), stored back to h.
+// qmax (127: int8 codes, 7: int4 codes kept one per byte) sets the range of
+// the quantised output.
 hipError_t launch_rmsnorm(int atype, float* h, const float* g, int T, int d, float eps, void* out, int8_t* q,
-                          float* qs, const float* parts, int nparts, size_t pstride, hipStream_t s);
-// Per-row int8 quantisation of x [T][K] (act type).  tiled = 1: x is tiled
-// activations and q is written tiled; tiled = 0: both row-major.
-hipError_t launch_quant_rows(int atype, const void* x, int T, int K, int8_t* q, float* qs, int tiled,
+                          float* qs, const float* parts, int nparts, size_t pstride, int qmax, hipStream_t s);
+// Per-row quantisation of x [T][K] (act type) to codes in [-qmax, qmax]
+// (127 or 7).  tiled = 1: x is tiled activations and q is written tiled;
+// tiled = 0: both row-major.
+hipError_t launch_quant_rows(int atype, const void* x, int T, int K, int8_t* q, float* qs, int tiled, int qmax,
                              hipStream_t s);
 // Tiled int8 copy of a tiled weight matrix (N rows, width K): per-row scales.
 hipError_t launch_quant_weight(int wtype, const void* w, int N, int K, int8_t* q, float* qs, hipStream_t s);
+// Packed int4 copy (wt4_byte layout, width pad_k(K, ET_I8)) of a tiled weight
+// matrix: per-row scales amax / 7.
+hipError_t launch_quant_weight_i4(int wtype, const void* w, int N, int K, uint8_t* q, float* qs, hipStream_t s);
+hipError_t launch_untile_weight_i4(const uint8_t* src, int N, int K, int8_t* dst, hipStream_t s);
+// Row-major int8 codes in [-7, 7] [N][K] -> packed int4 (for the kernel-level entry point).
+hipError_t launch_pack_weight_i4(const int8_t* src, int N, int K, uint8_t* dst, hipStream_t s);
 // Row-major W [rows][K] (act type) -> tiled weights of width pad_k(K).
 // Source row i lands at tiled row row0 + map(i): mode 0 map(i) = i; mode 1
 // (q/k heads of hd rows) puts rows i and i + hd/2 of a head next to each

@@ -108,13 +108,30 @@ template <int WT> struct WTr;
 template <> struct WTr<ET_F32> { static constexpr int E = 4, EB = 4; using acc_t = f32x4; };
 template <> struct WTr<ET_BF16> { static constexpr int E = 8, EB = 2; using acc_t = f32x4; };
 template <> struct WTr<ET_I8> { static constexpr int E = 16, EB = 1; using acc_t = i32x4; };
+// int4 weights run on the int8 MFMA: same steps (16 k per lane), half the bytes
+template <> struct WTr<ET_I4> { static constexpr int E = 16, EB = 1; using acc_t = i32x4; };
+template <int WT> constexpr bool is_int() { return WT == ET_I8 || WT == ET_I4; }
+// 1 KB weight blocks per 16-row tile and chunk (int4: two steps per block)
+template <int WT> constexpr int wblocks() { return WT == ET_I4 ? FRAG_U / 2 : FRAG_U; }
+// steps per stage: int4 stages hold whole blocks
+template <int WT, int UC> constexpr int stage_uc() { return WT == ET_I4 && UC < 2 ? 2 : UC; }
+
+// Four packed nibbles-with-offset (q + 8, one per byte) -> four int8 codes q:
+// ((u | 0x80) - 8) ^ 0x80 per byte, no borrow crosses a byte.
+__device__ __forceinline__ uint32_t sext_nib4(uint32_t x) { return ((x | 0x80808080u) - 0x08080808u) ^ 0x80808080u; }
+// The int8 A-fragment of step h (0, 1) of a packed int4 block (wt4_byte layout).
+__device__ __forceinline__ i32x4 i4_step(const i32x4 blk, int h) {
+    const uint32_t w0 = (uint32_t)(h ? blk[2] : blk[0]), w1 = (uint32_t)(h ? blk[3] : blk[1]);
+    return i32x4{(int)sext_nib4(w0 & 0x0f0f0f0fu), (int)sext_nib4(w1 & 0x0f0f0f0fu),
+                 (int)sext_nib4((w0 >> 4) & 0x0f0f0f0fu), (int)sext_nib4((w1 >> 4) & 0x0f0f0f0fu)};
+}
 
 template <int WT>
 __device__ __forceinline__ typename WTr<WT>::acc_t mfma_step(i32x4 a, i32x4 b, typename WTr<WT>::acc_t c) {
     if constexpr (WT == ET_BF16) {
         return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a),
                                                         __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
-    } else if constexpr (WT == ET_I8) {
+    } else if constexpr (is_int<WT>()) {
         return __builtin_amdgcn_mfma_i32_16x16x64_i8(a, b, c, 0, 0, 0);
     } else {
         const f32x4 fa = __builtin_bit_cast(f32x4, a), fb = __builtin_bit_cast(f32x4, b);
@@ -173,7 +190,7 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs& a, const typename 
         const int t = 16 * j + r;
         if (t >= T) continue;
         float v[4];
-        if constexpr (WT == ET_I8) {
+        if constexpr (is_int<WT>()) {
             if constexpr (EPI == EPI_RAW) {
                 int* o = (int*)a.out + (size_t)t * a.ldo + nb;
 #pragma unroll
@@ -282,7 +299,8 @@ __global__ void __launch_bounds__(64 * WAVES) k_gemm(const GemmArgs a) {
     const int c0 = (wave * C) / WAVES, c1 = ((wave + 1) * C) / WAVES;
     const int S0 = c0 * (FRAG_U / UC), S1 = c1 * (FRAG_U / UC);  // stages of UC steps
 
-    const char* wb = (const char*)a.W + ((size_t)tile * C * FRAG_U * 64 + lane) * 16;
+    static_assert(WT != ET_I4 || UC % 2 == 0, "int4 stages hold whole blocks");
+    const char* wb = (const char*)a.W + ((size_t)tile * C * wblocks<WT>() * 64 + lane) * 16;
     const char* xb = (const char*)a.X + (size_t)lane * 16;
     ACC acc[NT];
 #pragma unroll
@@ -297,16 +315,20 @@ __global__ void __launch_bounds__(64 * WAVES) k_gemm(const GemmArgs a) {
     do {                                                                                         \
         const size_t q = (size_t)(stage) * UC;                                                   \
         _Pragma("unroll") for (int u = 0; u < UC; ++u) {                                        \
-            A[st][u] = __builtin_nontemporal_load((const i32x4*)(wb + (q + u) * 1024));          \
+            if (WT != ET_I4 || (u & 1) == 0)                                                     \
+                A[st][u] = __builtin_nontemporal_load(                                           \
+                    (const i32x4*)(wb + (WT == ET_I4 ? (q + u) / 2 : q + u) * 1024));            \
             _Pragma("unroll") for (int j = 0; j < NT; ++j) B[st][j][u] =                         \
                 *(const i32x4*)(xb + ((q + u) * NT + j) * 1024);                                 \
         }                                                                                        \
     } while (0)
 #define CAS_GEMM_MMA(st)                                                                         \
     do {                                                                                         \
-        _Pragma("unroll") for (int u = 0; u < UC; ++u)                                          \
+        _Pragma("unroll") for (int u = 0; u < UC; ++u) {                                        \
+            const i32x4 au = WT == ET_I4 ? i4_step(A[st][u & ~1], u & 1) : A[st][u];             \
             _Pragma("unroll") for (int j = 0; j < NT; ++j) acc[j] =                              \
-                mfma_step<WT>(A[st][u], B[st][j][u], acc[j]);                                    \
+                mfma_step<WT>(au, B[st][j][u], acc[j]);                                          \
+        }                                                                                        \
     } while (0)
 
     if (S1 > S0) {
@@ -339,7 +361,7 @@ __global__ void __launch_bounds__(64 * WAVES) k_gemm(const GemmArgs a) {
 #undef CAS_GEMM_LOAD
 
     if constexpr (WAVES > 1) {
-        using S = typename std::conditional<WT == ET_I8, int, float>::type;
+        using S = typename std::conditional<is_int<WT>(), int, float>::type;
         __shared__ S red[WAVES - 1][NT][4][64];
         if (wave > 0) {
 #pragma unroll
@@ -373,6 +395,9 @@ __global__ void __launch_bounds__(64 * WAVES) k_gemm_wide(const GemmArgs a) {
     constexpr int NB = NT * UC;  // 1 KB activation blocks per stage
     constexpr int LPT = (NB + WAVES - 1) / WAVES;  // 1 KB blocks per wave per stage
     static_assert(D % 2 == 0 && FRAG_U % UC == 0, "stage shape");
+    static_assert(WT != ET_I4 || UC % 2 == 0, "int4 stages hold whole blocks");
+    constexpr int WB = wblocks<WT>();                  // weight blocks per chunk
+    constexpr int UB = WT == ET_I4 ? UC / 2 : UC;     // weight blocks per stage
     __shared__ __attribute__((aligned(16))) char lds[2][NB * 1024];
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -384,15 +409,15 @@ __global__ void __launch_bounds__(64 * WAVES) k_gemm_wide(const GemmArgs a) {
     const int c0 = (int)(((long)blockIdx.y * C) / gridDim.y);
     const int c1 = (int)(((long)(blockIdx.y + 1) * C) / gridDim.y);
     const int s0 = c0 * (FRAG_U / UC), NS = (c1 - c0) * (FRAG_U / UC);
-    const char* wb = (const char*)a.W + ((size_t)tile0 * C * FRAG_U * 64 + lane) * 16 + (size_t)s0 * UC * 1024;
-    const size_t tstride = (size_t)C * FRAG_U * 1024;  // bytes of one tile
+    const char* wb = (const char*)a.W + ((size_t)tile0 * C * WB * 64 + lane) * 16 + (size_t)s0 * UB * 1024;
+    const size_t tstride = (size_t)C * WB * 1024;  // bytes of one tile
     const char* xb = (const char*)a.X + (size_t)lane * 16 + (size_t)s0 * NB * 1024;
     ACC acc[TPW][NT];
 #pragma unroll
     for (int t = 0; t < TPW; ++t)
 #pragma unroll
         for (int j = 0; j < NT; ++j) acc[t][j] = ACC{0, 0, 0, 0};
-    i32x4 A[D][TPW][UC];
+    i32x4 A[D][TPW][UB];
     i32x4 Bv[D][LPT];
     QkvPre<NT> qp[TPW];
     if constexpr (EPI == EPI_QKV) {
@@ -402,9 +427,9 @@ __global__ void __launch_bounds__(64 * WAVES) k_gemm_wide(const GemmArgs a) {
 
 #define CAS_W_LOAD(st, stage)                                                                    \
     do {                                                                                         \
-        const size_t q = (size_t)(stage) * UC;                                                   \
+        const size_t q = (size_t)(stage) * UB;                                                   \
         _Pragma("unroll") for (int t = 0; t < TPW; ++t)                                         \
-            _Pragma("unroll") for (int u = 0; u < UC; ++u) A[st][t][u] =                        \
+            _Pragma("unroll") for (int u = 0; u < UB; ++u) A[st][t][u] =                        \
                 __builtin_nontemporal_load((const i32x4*)(wb + t * tstride + (q + u) * 1024));   \
         /* a block index past the stage (WAVES not dividing NB) reloads the last block, */  \
         /* so every wave issues the same loads; it is not stored */                         \
@@ -416,12 +441,16 @@ __global__ void __launch_bounds__(64 * WAVES) k_gemm_wide(const GemmArgs a) {
         _Pragma("unroll") for (int p = 0; p < LPT; ++p) if (p * WAVES + wave < NB)              \
             *(i32x4*)(&lds[slot][(p * WAVES + wave) * 1024 + lane * 16]) = Bv[st][p];            \
         __syncthreads();                                                                         \
-        _Pragma("unroll") for (int u = 0; u < UC; ++u)                                          \
+        _Pragma("unroll") for (int u = 0; u < UC; ++u) {                                        \
+            i32x4 au[TPW];                                                                       \
+            _Pragma("unroll") for (int t = 0; t < TPW; ++t)                                     \
+                au[t] = WT == ET_I4 ? i4_step(A[st][t][u >> 1], u & 1) : A[st][t][u];            \
             _Pragma("unroll") for (int j = 0; j < NT; ++j) {                                    \
                 const i32x4 b = *(const i32x4*)(&lds[slot][(u * NT + j) * 1024 + lane * 16]);    \
                 _Pragma("unroll") for (int t = 0; t < TPW; ++t)                                 \
-                    acc[t][j] = mfma_step<WT>(A[st][t][u], b, acc[t][j]);                        \
+                    acc[t][j] = mfma_step<WT>(au[t], b, acc[t][j]);                              \
             }                                                                                    \
+        }                                                                                        \
     } while (0)
 
 #pragma unroll
@@ -473,13 +502,18 @@ template <int NT, int TPW> struct WideStage {
     static constexpr int UC = TPW == 2 ? (NT == 2 ? 4 : 2) : (NT == 8 ? 1 : 2);
     static constexpr int D = TPW == 2 && NT == 2 ? 2 : 4;
 };
+// ... with whole int4 blocks per stage
+template <int WT, int NT, int TPW> struct WideStageW {
+    static constexpr int UC = stage_uc<WT, WideStage<NT, TPW>::UC>();
+    static constexpr int D = WideStage<NT, TPW>::D;
+};
 
 template <int WT, int NT, int EPI, typename AT>
 static hipError_t gemm_go(const GemmArgs& a, hipStream_t s) {
-    constexpr int UC = NT == 2 ? 4 : (NT == 4 ? 2 : 1);
+    constexpr int UC = stage_uc<WT, NT == 2 ? 4 : (NT == 4 ? 2 : 1)>();
     if (a.N >= 8192 && ((a.N / 16) % 4 == 0 || (a.N / 16) % 3 == 0)) {
-        using S1 = WideStage<NT, 1>;
-        using S2 = WideStage<NT, 2>;
+        using S1 = WideStageW<WT, NT, 1>;
+        using S2 = WideStageW<WT, NT, 2>;
         // Every workgroup should stay resident on a CU of its own (a CU that
         // holds two workgroups while others hold one sets the pace): take the
         // split of the tiles into equal workgroups of 4x1, 3x1, 4x2 or 3x2
@@ -507,7 +541,8 @@ static hipError_t gemm_go(const GemmArgs& a, hipStream_t s) {
             hipLaunchKernelGGL((k_gemm_wide<WT, NT, S2::UC, S2::D, 3, 2, EPI, AT>), dim3(bg), dim3(192), 0, s, a);
         return hipGetLastError();
     }
-    constexpr int D = NT == 2 ? 2 : 4;
+    // (int4 at 8 column tiles: two steps per stage, so a shallower ring)
+    constexpr int D = NT == 2 || (WT == ET_I4 && NT == 8) ? 2 : 4;
     hipLaunchKernelGGL((k_gemm<WT, NT, UC, D, 4, EPI, AT>), dim3(a.N / 16), dim3(256), 0, s, a);
     return hipGetLastError();
 }
@@ -553,6 +588,17 @@ hipError_t launch_gemm(int wtype, int atype, int epi, const GemmArgs& a, hipStre
             return bf ? gemm_nt<ET_I8, EPI_QKV, uint16_t>(a, s) : gemm_nt<ET_I8, EPI_QKV, float>(a, s);
         }
         break;
+    case ET_I4:
+        switch (epi) {
+        case EPI_STORE: return gemm_nt<ET_I4, EPI_STORE, float>(a, s);
+        case EPI_RESID: return gemm_nt<ET_I4, EPI_RESID, float>(a, s);
+        case EPI_RAW: return gemm_nt<ET_I4, EPI_RAW, float>(a, s);
+        case EPI_SWIGLU:
+            return bf ? gemm_nt<ET_I4, EPI_SWIGLU, uint16_t>(a, s) : gemm_nt<ET_I4, EPI_SWIGLU, float>(a, s);
+        case EPI_QKV:
+            return bf ? gemm_nt<ET_I4, EPI_QKV, uint16_t>(a, s) : gemm_nt<ET_I4, EPI_QKV, float>(a, s);
+        }
+        break;
     }
     return hipErrorInvalidValue;
 }
@@ -576,7 +622,9 @@ static hipError_t gemm_parts_go(const GemmArgs& a, hipStream_t s) {
     switch (col_tiles(a.T)) {
     case 2: hipLaunchKernelGGL((k_gemm_wide<WT, 2, 4, 2, 4, 1, EPI_STORE, AT>), grid, dim3(256), 0, s, a); break;
     case 4: hipLaunchKernelGGL((k_gemm_wide<WT, 4, 2, 4, 4, 1, EPI_STORE, AT>), grid, dim3(256), 0, s, a); break;
-    default: hipLaunchKernelGGL((k_gemm_wide<WT, 8, 1, 4, 4, 1, EPI_STORE, AT>), grid, dim3(256), 0, s, a); break;
+    default:
+        hipLaunchKernelGGL((k_gemm_wide<WT, 8, stage_uc<WT, 1>(), 4, 4, 1, EPI_STORE, AT>), grid, dim3(256), 0, s, a);
+        break;
     }
     return hipGetLastError();
 }
@@ -589,6 +637,7 @@ hipError_t launch_gemm_parts(int wtype, const GemmArgs& a, hipStream_t s) {
     if (wtype == ET_F32) return gemm_parts_go<ET_F32, float>(a, s);
     // int8: each split dequantises its own int32 sums, (acc * xs[t]) * ws[n]
     if (wtype == ET_I8) return gemm_parts_go<ET_I8, float>(a, s);
+    if (wtype == ET_I4) return gemm_parts_go<ET_I4, float>(a, s);
     return hipErrorInvalidValue;
 }
 
@@ -1308,12 +1357,14 @@ __device__ __forceinline__ void st4q(int8_t* q, size_t o, float a, float b, floa
                        ((uint32_t)(uint8_t)(int8_t)c << 16) | ((uint32_t)(uint8_t)(int8_t)d << 24);
     *(uint32_t*)(q + o) = v;
 }
-__device__ __forceinline__ float q8(float x, float sc) {
-    return sc != 0.f ? fminf(fmaxf(rintf(x / sc), -127.f), 127.f) : 0.f;
+// Code of x at scale sc in [-qm, qm] (qm 127: int8, 7: int4).
+__device__ __forceinline__ float qcode(float x, float sc, float qm) {
+    return sc != 0.f ? fminf(fmaxf(rintf(x / sc), -qm), qm) : 0.f;
 }
 
 // RMSNorm of one row of the residual stream, written as tiled activations
-// (pad columns zero) or, with Q, straight to the row's int8 quantisation.
+// (pad columns zero) or, with Q, straight to the row's quantisation (codes
+// in [-qm, qm], one per byte: int8, or int4 for the W4A4 weights).
 // With nparts > 0 the row first takes the pending split-K sums of the last
 // projection (summed in split order, then added to the residual, which is
 // stored back).  NV float4 per thread; loads are unconditional (clamped into
@@ -1321,7 +1372,7 @@ __device__ __forceinline__ float q8(float x, float sc) {
 template <typename AT, bool Q, int NV>
 __global__ void __launch_bounds__(NORM_THREADS) k_rmsnorm(float* h, const float* gain, int d, float eps, AT* out,
                                                  int8_t* q, float* qs, const float* parts, int nparts,
-                                                 size_t pstride) {
+                                                 size_t pstride, float qm) {
     __shared__ float red[NORM_THREADS / 64];
     const int t = blockIdx.x, NT = col_tiles(gridDim.x), tid = threadIdx.x;
     float* x = h + (size_t)t * d;
@@ -1387,25 +1438,28 @@ __global__ void __launch_bounds__(NORM_THREADS) k_rmsnorm(float* h, const float*
         }
     } else {
         amax = block_max<NORM_THREADS / 64>(amax, red);
-        const float sc = amax / 127.0f;
+        const float sc = amax / qm;
         if (threadIdx.x == 0) qs[t] = sc;
         const int kpq = (d + 255) / 256 * 256;
 #pragma unroll
         for (int i = 0; i < NV; ++i) {
             const int k4 = (tid + NORM_THREADS * i) * 4;
-            if (k4 < kpq) st4q(q, xt_off(t, k4, NT, 16), q8(v[i].x, sc), q8(v[i].y, sc), q8(v[i].z, sc), q8(v[i].w, sc));
+            if (k4 < kpq)
+                st4q(q, xt_off(t, k4, NT, 16), qcode(v[i].x, sc, qm), qcode(v[i].y, sc, qm), qcode(v[i].z, sc, qm),
+                     qcode(v[i].w, sc, qm));
         }
     }
 }
 
 template <typename AT, bool Q>
 static hipError_t rmsnorm_go(float* h, const float* g, int T, int d, float eps, AT* out, int8_t* q, float* qs,
-                             const float* parts, int nparts, size_t pstride, hipStream_t s) {
+                             const float* parts, int nparts, size_t pstride, float qm, hipStream_t s) {
     // float4 per thread covering the padded row (int8 output pads to 256, bf16 to 128)
     const int span = (d + 255) / 256 * 256;
     const int nv = (span + 4 * NORM_THREADS - 1) / (4 * NORM_THREADS);
 #define CAS_NORM(NV) \
-    hipLaunchKernelGGL((k_rmsnorm<AT, Q, NV>), dim3(T), dim3(NORM_THREADS), 0, s, h, g, d, eps, out, q, qs, parts, nparts, pstride)
+    hipLaunchKernelGGL((k_rmsnorm<AT, Q, NV>), dim3(T), dim3(NORM_THREADS), 0, s, h, g, d, eps, out, q, qs, parts, nparts, \
+                       pstride, qm)
     if (nv <= 1) CAS_NORM(1);
     else if (nv <= 2) CAS_NORM(2);
     else CAS_NORM(NORM_MAXV);
@@ -1414,19 +1468,22 @@ static hipError_t rmsnorm_go(float* h, const float* g, int T, int d, float eps, 
 }
 
 hipError_t launch_rmsnorm(int atype, float* h, const float* g, int T, int d, float eps, void* out, int8_t* q,
-                          float* qs, const float* parts, int nparts, size_t pstride, hipStream_t s) {
-    if (d > 4 * NORM_THREADS * NORM_MAXV || d % 16 || nparts < 0 || (nparts > 0 && (!parts || pstride < (size_t)T * d)))
+                          float* qs, const float* parts, int nparts, size_t pstride, int qmax, hipStream_t s) {
+    if (d > 4 * NORM_THREADS * NORM_MAXV || d % 16 || nparts < 0 || (nparts > 0 && (!parts || pstride < (size_t)T * d)) ||
+        (q && qmax != 127 && qmax != 7))
         return hipErrorInvalidValue;
+    const float qm = (float)qmax;
     if (atype == ET_BF16) {
-        if (q) return rmsnorm_go<uint16_t, true>(h, g, T, d, eps, (uint16_t*)out, q, qs, parts, nparts, pstride, s);
-        return rmsnorm_go<uint16_t, false>(h, g, T, d, eps, (uint16_t*)out, q, qs, parts, nparts, pstride, s);
+        if (q) return rmsnorm_go<uint16_t, true>(h, g, T, d, eps, (uint16_t*)out, q, qs, parts, nparts, pstride, qm, s);
+        return rmsnorm_go<uint16_t, false>(h, g, T, d, eps, (uint16_t*)out, q, qs, parts, nparts, pstride, qm, s);
     }
-    if (q) return rmsnorm_go<float, true>(h, g, T, d, eps, (float*)out, q, qs, parts, nparts, pstride, s);
-    return rmsnorm_go<float, false>(h, g, T, d, eps, (float*)out, q, qs, parts, nparts, pstride, s);
+    if (q) return rmsnorm_go<float, true>(h, g, T, d, eps, (float*)out, q, qs, parts, nparts, pstride, qm, s);
+    return rmsnorm_go<float, false>(h, g, T, d, eps, (float*)out, q, qs, parts, nparts, pstride, qm, s);
 }
 
-// Per-row symmetric int8 of tiled activations: s = amax / 127,
-// q = clamp(rne(x / s), -127, 127), codes written tiled (pad zero).  One
+// Per-row symmetric quantisation of tiled activations: s = amax / qm,
+// q = clamp(rne(x / s), -qm, qm) (qm 127 or 7), codes written tiled, one per
+// byte (pad zero).  One
 // workgroup of 1024 threads per row; a thread takes whole 16-byte fragments
 // of the row (EA consecutive k each, which land in one int8 fragment of 16
 // k), NF fragments per thread held in registers between the amax and the
@@ -1434,7 +1491,7 @@ hipError_t launch_rmsnorm(int atype, float* h, const float* g, int T, int d, flo
 static constexpr int QR_THREADS = 1024;
 
 template <typename AT, int NF>
-__global__ void __launch_bounds__(QR_THREADS) k_quant_rows_tiled(const AT* x, int K, int8_t* q, float* qs) {
+__global__ void __launch_bounds__(QR_THREADS) k_quant_rows_tiled(const AT* x, int K, int8_t* q, float* qs, float qm) {
     __shared__ float red[QR_THREADS / 64];
     constexpr int EA = 16 / sizeof(AT);
     const int t = blockIdx.x, NT = col_tiles(gridDim.x), tid = threadIdx.x;
@@ -1452,7 +1509,7 @@ __global__ void __launch_bounds__(QR_THREADS) k_quant_rows_tiled(const AT* x, in
             if (f < nfa && f * EA + j < K) amax = fmaxf(amax, fabsf(Act<AT>::ld(e, j)));
     }
     amax = block_max<QR_THREADS / 64>(amax, red);
-    const float sc = amax / 127.0f;
+    const float sc = amax / qm;
     if (tid == 0) qs[t] = sc;
 #pragma unroll
     for (int i = 0; i < NF; ++i) {
@@ -1466,7 +1523,7 @@ __global__ void __launch_bounds__(QR_THREADS) k_quant_rows_tiled(const AT* x, in
 #pragma unroll
             for (int u = 0; u < 4; ++u) {
                 const int k = f * EA + 4 * j + u;
-                const float c = (f < nfa && k < K) ? q8(Act<AT>::ld(e, 4 * j + u), sc) : 0.f;
+                const float c = (f < nfa && k < K) ? qcode(Act<AT>::ld(e, 4 * j + u), sc, qm) : 0.f;
                 b |= (uint32_t)(uint8_t)(int8_t)c << (8 * u);
             }
             w[j] = b;
@@ -1479,7 +1536,7 @@ __global__ void __launch_bounds__(QR_THREADS) k_quant_rows_tiled(const AT* x, in
 
 // Row-major form ([T][K] in, [T][K] out), for the kernel-level entry point.
 template <typename AT, bool TILED>
-__global__ void __launch_bounds__(256) k_quant_rows(const AT* x, int K, int8_t* q, float* qs) {
+__global__ void __launch_bounds__(256) k_quant_rows(const AT* x, int K, int8_t* q, float* qs, float qm) {
     __shared__ float red[4];
     const int t = blockIdx.x, NT = col_tiles(gridDim.x);
     constexpr int EA = 16 / sizeof(AT);
@@ -1487,22 +1544,22 @@ __global__ void __launch_bounds__(256) k_quant_rows(const AT* x, int K, int8_t* 
     float amax = 0.f;
     for (int k = threadIdx.x; k < K; k += 256) amax = fmaxf(amax, fabsf(Act<AT>::ld(x, at(k))));
     amax = block_max256(amax, red);
-    const float sc = amax / 127.0f;
+    const float sc = amax / qm;
     if (threadIdx.x == 0) qs[t] = sc;
     const int kq = TILED ? (K + 255) / 256 * 256 : K;
     for (int k = threadIdx.x; k < kq; k += 256) {
         float rq = 0.f;
-        if (k < K && sc != 0.f) rq = fminf(fmaxf(rintf(Act<AT>::ld(x, at(k)) / sc), -127.f), 127.f);
+        if (k < K) rq = qcode(Act<AT>::ld(x, at(k)), sc, qm);
         q[TILED ? xt_off(t, k, NT, 16) : (size_t)t * K + k] = (int8_t)rq;
     }
 }
 
 template <typename AT>
-static hipError_t quant_tiled_go(const AT* x, int T, int K, int8_t* q, float* qs, hipStream_t s) {
+static hipError_t quant_tiled_go(const AT* x, int T, int K, int8_t* q, float* qs, float qm, hipStream_t s) {
     constexpr int EA = 16 / sizeof(AT);
     const int nfq = (K + 255) / 256 * 256 / EA;  // >= fragments of the padded input row
     const int nf = (nfq + QR_THREADS - 1) / QR_THREADS;
-#define CAS_QR(NF) hipLaunchKernelGGL((k_quant_rows_tiled<AT, NF>), dim3(T), dim3(QR_THREADS), 0, s, x, K, q, qs)
+#define CAS_QR(NF) hipLaunchKernelGGL((k_quant_rows_tiled<AT, NF>), dim3(T), dim3(QR_THREADS), 0, s, x, K, q, qs, qm)
     if (nf <= 1) CAS_QR(1);
     else if (nf <= 2) CAS_QR(2);
     else if (nf <= 4) CAS_QR(4);
@@ -1512,14 +1569,16 @@ static hipError_t quant_tiled_go(const AT* x, int T, int K, int8_t* q, float* qs
     return hipGetLastError();
 }
 
-hipError_t launch_quant_rows(int atype, const void* x, int T, int K, int8_t* q, float* qs, int tiled, hipStream_t s) {
-    if (T < 1 || K < 1 || (tiled && (T > 128 || K > 65536))) return hipErrorInvalidValue;
+hipError_t launch_quant_rows(int atype, const void* x, int T, int K, int8_t* q, float* qs, int tiled, int qmax,
+                             hipStream_t s) {
+    if (T < 1 || K < 1 || (tiled && (T > 128 || K > 65536)) || (qmax != 127 && qmax != 7)) return hipErrorInvalidValue;
+    const float qm = (float)qmax;
     if (atype == ET_BF16) {
-        if (tiled) return quant_tiled_go((const uint16_t*)x, T, K, q, qs, s);
-        hipLaunchKernelGGL((k_quant_rows<uint16_t, false>), dim3(T), dim3(256), 0, s, (const uint16_t*)x, K, q, qs);
+        if (tiled) return quant_tiled_go((const uint16_t*)x, T, K, q, qs, qm, s);
+        hipLaunchKernelGGL((k_quant_rows<uint16_t, false>), dim3(T), dim3(256), 0, s, (const uint16_t*)x, K, q, qs, qm);
     } else {
-        if (tiled) return quant_tiled_go((const float*)x, T, K, q, qs, s);
-        hipLaunchKernelGGL((k_quant_rows<float, false>), dim3(T), dim3(256), 0, s, (const float*)x, K, q, qs);
+        if (tiled) return quant_tiled_go((const float*)x, T, K, q, qs, qm, s);
+        hipLaunchKernelGGL((k_quant_rows<float, false>), dim3(T), dim3(256), 0, s, (const float*)x, K, q, qs, qm);
     }
     return hipGetLastError();
 }
@@ -1575,6 +1634,105 @@ __global__ void k_untile_weight_i8(const int8_t* src, int N, int K, int8_t* dst)
 
 hipError_t launch_untile_weight_i8(const int8_t* src, int N, int K, int8_t* dst, hipStream_t s) {
     hipLaunchKernelGGL(k_untile_weight_i8, dim3(grid_for((size_t)N * K)), dim3(256), 0, s, src, N, K, dst);
+    return hipGetLastError();
+}
+
+// ---- packed int4 weights (wt4_byte layout)
+
+// Tile (n >> 4), chunk c: the byte b of its 2 KB holds rows/k-offsets given
+// by wt4_byte; this inverts it: (row in tile, k of the low nibble).
+__device__ __forceinline__ void wt4_inv(int b, int c, int& r, int& k) {
+    const int blk = b >> 10, lane = (b >> 4) & 63, byte = b & 15;
+    const int g = lane >> 4, u = 2 * blk + (byte >> 3), j = byte & 7;
+    r = lane & 15;
+    k = c * 256 + g * 64 + u * 16 + j;  // the high nibble holds k + 8
+}
+
+// Tiled weights (act type) -> packed int4 codes with per-row scales amax / 7,
+// one workgroup per 16-row tile: row amax over the whole row, then 4 packed
+// bytes per thread and step.
+template <typename AT>
+__global__ void __launch_bounds__(256) k_quant_weight_i4(const AT* w, int K, uint8_t* q, float* qs) {
+    __shared__ unsigned amax_bits[16];
+    __shared__ float scale[16];
+    constexpr int EA = 16 / sizeof(AT);
+    const int tile = blockIdx.x, n0 = tile * 16;
+    const int Kpa = (K + 16 * EA - 1) / (16 * EA) * (16 * EA), C = (K + 255) / 256;
+    if (threadIdx.x < 16) amax_bits[threadIdx.x] = 0u;
+    __syncthreads();
+    {
+        const int r = threadIdx.x & 15;
+        float m = 0.f;
+        for (int k = threadIdx.x >> 4; k < K; k += 16) m = fmaxf(m, fabsf(Act<AT>::ld(w, wt_off(n0 + r, k, Kpa, EA))));
+        atomicMax(&amax_bits[r], __float_as_uint(m));  // non-negative floats order like their bits
+    }
+    __syncthreads();
+    if (threadIdx.x < 16) {
+        const float sc = __uint_as_float(amax_bits[threadIdx.x]) / 7.0f;
+        scale[threadIdx.x] = sc;
+        qs[n0 + threadIdx.x] = sc;
+    }
+    __syncthreads();
+    uint8_t* qt = q + (size_t)tile * C * 2048;
+    for (int w4 = threadIdx.x; w4 < C * 512; w4 += 256) {
+        const int c = w4 >> 9;
+        uint32_t word = 0;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            int r, k;
+            wt4_inv((w4 & 511) * 4 + i, c, r, k);
+            const float sc = scale[r];
+            const float lo = k < K ? qcode(Act<AT>::ld(w, wt_off(n0 + r, k, Kpa, EA)), sc, 7.f) : 0.f;
+            const float hi = k + 8 < K ? qcode(Act<AT>::ld(w, wt_off(n0 + r, k + 8, Kpa, EA)), sc, 7.f) : 0.f;
+            word |= (uint32_t)(((int)lo + 8) | (((int)hi + 8) << 4)) << (8 * i);
+        }
+        *(uint32_t*)(qt + (size_t)w4 * 4) = word;
+    }
+}
+
+hipError_t launch_quant_weight_i4(int wtype, const void* w, int N, int K, uint8_t* q, float* qs, hipStream_t s) {
+    if (N % 16 || K < 1) return hipErrorInvalidValue;
+    if (wtype == ET_BF16)
+        hipLaunchKernelGGL(k_quant_weight_i4<uint16_t>, dim3(N / 16), dim3(256), 0, s, (const uint16_t*)w, K, q, qs);
+    else
+        hipLaunchKernelGGL(k_quant_weight_i4<float>, dim3(N / 16), dim3(256), 0, s, (const float*)w, K, q, qs);
+    return hipGetLastError();
+}
+
+// Row-major codes [N][K] in [-7, 7] -> packed int4 (one thread per packed byte).
+__global__ void k_pack_weight_i4(const int8_t* src, int N, int K, uint8_t* dst) {
+    const int C = (K + 255) / 256;
+    const size_t total = (size_t)(N / 16) * C * 2048;
+    for (size_t idx = blockIdx.x * (size_t)blockDim.x + threadIdx.x; idx < total;
+         idx += (size_t)gridDim.x * blockDim.x) {
+        const int tile = (int)(idx / ((size_t)C * 2048)), rem = (int)(idx % ((size_t)C * 2048));
+        int r, k;
+        wt4_inv(rem & 2047, rem >> 11, r, k);
+        const size_t row = (size_t)(tile * 16 + r) * K;
+        const int lo = k < K ? src[row + k] : 0, hi = k + 8 < K ? src[row + k + 8] : 0;
+        dst[idx] = (uint8_t)((lo + 8) | ((hi + 8) << 4));
+    }
+}
+hipError_t launch_pack_weight_i4(const int8_t* src, int N, int K, uint8_t* dst, hipStream_t s) {
+    if (N % 16 || K < 1) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(k_pack_weight_i4, dim3(grid_for((size_t)(N / 16) * ((K + 255) / 256) * 2048)), dim3(256), 0, s,
+                       src, N, K, dst);
+    return hipGetLastError();
+}
+
+// Packed int4 -> row-major codes (for checking the copy).
+__global__ void k_untile_weight_i4(const uint8_t* src, int N, int K, int8_t* dst) {
+    const int Kp = (K + 255) / 256 * 256;
+    const size_t total = (size_t)N * K;
+    for (size_t idx = blockIdx.x * (size_t)blockDim.x + threadIdx.x; idx < total;
+         idx += (size_t)gridDim.x * blockDim.x) {
+        int nib;
+        const size_t b = wt4_byte((int)(idx / K), (int)(idx % K), Kp, &nib);
+        dst[idx] = (int8_t)(((src[b] >> (4 * nib)) & 15) - 8);
+    }
+}
+hipError_t launch_untile_weight_i4(const uint8_t* src, int N, int K, int8_t* dst, hipStream_t s) {
+    hipLaunchKernelGGL(k_untile_weight_i4, dim3(grid_for((size_t)N * K)), dim3(256), 0, s, src, N, K, dst);
     return hipGetLastError();
 }
 

@@ -32,6 +32,8 @@ struct LayerW {
     float* ffn_norm = nullptr;
     int8_t* q8[4] = {nullptr, nullptr, nullptr, nullptr};  // int8 copies in the same row layouts
     float* s8[4] = {nullptr, nullptr, nullptr, nullptr};
+    uint8_t* q4[4] = {nullptr, nullptr, nullptr, nullptr};  // packed int4 copies (same rows, int8 chunking)
+    float* s4[4] = {nullptr, nullptr, nullptr, nullptr};
     unsigned loaded = 0;    // bit per tensor kind
 };
 
@@ -67,6 +69,7 @@ struct cas_ctx {
     unsigned global_loaded = 0;
     std::vector<LayerW> layers;
     bool int8_ready = false;
+    bool int4_ready = false;
 
     void* kc = nullptr;  // [L][Hkv][ctx_cap][hd]
     void* vt = nullptr;  // [L][Hkv][hd][ctx_cap]
@@ -282,14 +285,19 @@ hipError_t enqueue_forward(cas_ctx* c, int T, const uint8_t* skip, int aq) {
     const int S = attention_splits_win(at.Lc_host, at.n_tree_host, at.win_sink, at.win_len);
     at.part_o = c->d_part;
     at.part_ml = c->d_part + (size_t)S * H * T * hd;
-    const int wq = aq ? (int)ET_I8 : et;
+    // act_quant 1: int8 codes against the int8 copy; 2: int4 codes (one per
+    // byte) against the packed int4 copy
+    const int wq = aq == 2 ? (int)ET_I4 : aq ? (int)ET_I8 : et;
+    const int qmax = aq == 2 ? 7 : 127;
+    auto wcopy = [&](const LayerW& w, int i) -> const void* { return aq == 2 ? (const void*)w.q4[i] : (const void*)w.q8[i]; };
+    auto scopy = [&](const LayerW& w, int i) -> const float* { return aq == 2 ? w.s4[i] : w.s8[i]; };
     // split-K sums of the last O / down projection that the next RMSNorm
     // adds to the residual stream (0: the projection updated it itself)
     int pend = 0;
     const size_t pstride = (size_t)T * d;
     auto norm = [&](const float* gain, void* out, int8_t* qo, float* qso) -> hipError_t {
         const hipError_t r = launch_rmsnorm(et, c->d_h, gain, T, d, f.rms_eps, out, qo, qso, c->d_gpart, pend,
-                                            pstride, s);
+                                            pstride, qmax, s);
         pend = 0;
         return r;
     };
@@ -316,10 +324,10 @@ hipError_t enqueue_forward(cas_ctx* c, int T, const uint8_t* skip, int aq) {
         g.T = T;
         g.N = c->qkv_rows;
         g.Kp = aq ? c->kq_d : c->kp_d;
-        g.W = aq ? (const void*)w.q8[0] : w.wqkv;
+        g.W = aq ? wcopy(w, 0) : w.wqkv;
         g.X = aq ? (const void*)c->d_xq : c->d_xn;
         g.xs = c->d_xs;
-        g.ws = w.s8[0];
+        g.ws = scopy(w, 0);
         g.out = c->d_q;
         g.rope_cos = c->rope_cos;
         g.rope_sin = c->rope_sin;
@@ -335,15 +343,15 @@ hipError_t enqueue_forward(cas_ctx* c, int T, const uint8_t* skip, int aq) {
         at.kc = kc;
         at.vt = vt;
         RUN(CAS_K_ATTN, launch_attention(et, at, s));
-        if (aq) RUN(CAS_K_QUANT, launch_quant_rows(et, c->d_ao, T, H * hd, c->d_xq, c->d_xs, 1, s));
+        if (aq) RUN(CAS_K_QUANT, launch_quant_rows(et, c->d_ao, T, H * hd, c->d_xq, c->d_xs, 1, qmax, s));
         GemmArgs go{};
         go.T = T;
         go.N = d;
         go.Kp = aq ? c->kq_q : c->kp_q;
-        go.W = aq ? (const void*)w.q8[1] : w.wo;
+        go.W = aq ? wcopy(w, 1) : w.wo;
         go.X = aq ? (const void*)c->d_xq : c->d_ao;
         go.xs = c->d_xs;
-        go.ws = w.s8[1];
+        go.ws = scopy(w, 1);
         go.out = c->d_h;
         go.ldo = d;
         RUN(CAS_K_GEMM_O, resid_proj(go));
@@ -353,23 +361,23 @@ hipError_t enqueue_forward(cas_ctx* c, int T, const uint8_t* skip, int aq) {
         gu.T = T;
         gu.N = 2 * ffn;
         gu.Kp = aq ? c->kq_d : c->kp_d;
-        gu.W = aq ? (const void*)w.q8[2] : w.wgu;
+        gu.W = aq ? wcopy(w, 2) : w.wgu;
         gu.X = aq ? (const void*)c->d_xq : c->d_xn;
         gu.xs = c->d_xs;
-        gu.ws = w.s8[2];
+        gu.ws = scopy(w, 2);
         gu.out = c->d_sw;
         gu.ldo = ffn;
         gu.out_k = ffn;
         RUN(CAS_K_GEMM_GATEUP, launch_gemm(wq, et, EPI_SWIGLU, gu, s));
-        if (aq) RUN(CAS_K_QUANT, launch_quant_rows(et, c->d_sw, T, ffn, c->d_xq, c->d_xs, 1, s));
+        if (aq) RUN(CAS_K_QUANT, launch_quant_rows(et, c->d_sw, T, ffn, c->d_xq, c->d_xs, 1, qmax, s));
         GemmArgs gd{};
         gd.T = T;
         gd.N = d;
         gd.Kp = aq ? c->kq_f : c->kp_f;
-        gd.W = aq ? (const void*)w.q8[3] : w.wd;
+        gd.W = aq ? wcopy(w, 3) : w.wd;
         gd.X = aq ? (const void*)c->d_xq : c->d_sw;
         gd.xs = c->d_xs;
-        gd.ws = w.s8[3];
+        gd.ws = scopy(w, 3);
         gd.out = c->d_h;
         gd.ldo = d;
         RUN(CAS_K_GEMM_DOWN, resid_proj(gd));
@@ -415,7 +423,7 @@ cas_status do_forward(cas_ctx* c, const int32_t* tokens, const int32_t* parent, 
     if (win_len == 0) win_sink = 0;
     if (n < 1) return fail(c, CAS_ERR_ARG, "n must be >= 1");
     if (node_offset < 0) return fail(c, CAS_ERR_ARG, "node_offset must be >= 0");
-    if (aq != 0 && aq != 1) return fail(c, CAS_ERR_ARG, "act_quant must be 0 or 1");
+    if (aq < 0 || aq > 2) return fail(c, CAS_ERR_ARG, "act_quant must be 0, 1 or 2");
     if (node_offset != 0 && node_offset != c->n_nodes)
         return fail(c, CAS_ERR_TREE, "node_offset must be 0 (new round) or the round's node count " +
                                          std::to_string(c->n_nodes));
@@ -433,7 +441,8 @@ cas_status do_forward(cas_ctx* c, const int32_t* tokens, const int32_t* parent, 
             any_skip |= skip[l] != 0;
         }
     }
-    if (aq && !c->int8_ready) return fail(c, CAS_ERR_STATE, "act_quant needs cas_build_int8 first");
+    if (aq == 1 && !c->int8_ready) return fail(c, CAS_ERR_STATE, "act_quant 1 needs cas_build_int8 first");
+    if (aq == 2 && !c->int4_ready) return fail(c, CAS_ERR_STATE, "act_quant 2 needs cas_build_int4 first");
     std::vector<int> depth;
     std::string why;
     if (!tree_depths(parent, node_offset, n, c->parent, &depth, &why)) return fail(c, CAS_ERR_TREE, why);
@@ -780,6 +789,32 @@ cas_status cas_load_tensor(cas_ctx* c, int32_t kind, int32_t layer, const void* 
         c->global_loaded |= 1u << kind;
     }
     c->int8_ready = false;
+    c->int4_ready = false;
+    return CAS_OK;
+}
+
+cas_status cas_build_int4(cas_ctx* c) {
+    if (!c) return CAS_ERR_ARG;
+    cas_status st = check_ready(c, nullptr);
+    if (st != CAS_OK) return st;
+    const cas_config& f = c->cfg;
+    const size_t d = f.d_model, ffn = f.ffn_dim;
+    for (auto& w : c->layers) {
+        const void* src[4] = {w.wqkv, w.wo, w.wgu, w.wd};
+        const size_t N[4] = {(size_t)c->qkv_rows, d, 2 * ffn, d};
+        const size_t K[4] = {d, (size_t)c->qrows, d, ffn};
+        const size_t KQ[4] = {(size_t)c->kq_d, (size_t)c->kq_q, (size_t)c->kq_d, (size_t)c->kq_f};
+        for (int i = 0; i < 4; ++i) {
+            if (!w.q4[i]) {
+                if (dalloc(c, &w.q4[i], N[i] * KQ[i] / 2) != hipSuccess || dalloc(c, &w.s4[i], N[i] * 4) != hipSuccess)
+                    return fail(c, CAS_ERR_OOM, "hipMalloc of the int4 weight copy");
+            }
+            hipError_t e = launch_quant_weight_i4(c->et, src[i], (int)N[i], (int)K[i], w.q4[i], w.s4[i], c->stream);
+            if (e != hipSuccess) return hip_fail(c, e, "int4 weight quantisation");
+        }
+    }
+    HIPCHK(c, hipStreamSynchronize(c->stream));
+    c->int4_ready = true;
     return CAS_OK;
 }
 
@@ -1015,7 +1050,11 @@ cas_status cas_sync(cas_ctx* c) {
 static size_t align256(size_t x) { return (x + 255) / 256 * 256; }
 
 size_t cas_op_gemm_work_bytes(int32_t wtype, int32_t N, int32_t K, int32_t T) {
-    if (wtype < CAS_W_F32 || wtype > CAS_W_I8 || N < 1 || K < 1 || T < 1 || T > 128) return 0;
+    if (wtype < CAS_W_F32 || wtype > CAS_W_I4 || N < 1 || K < 1 || T < 1 || T > 128) return 0;
+    if (wtype == CAS_W_I4) {  // packed weights, int8 activations
+        const size_t Kp = pad_k(K, ET_I8);
+        return align256((size_t)N * Kp / 2) + align256((size_t)16 * col_tiles(T) * Kp);
+    }
     const size_t Kp = pad_k(K, wtype), eb = frag_elem_bytes(wtype);
     return align256((size_t)N * Kp * eb) + align256((size_t)16 * col_tiles(T) * Kp * eb);
 }
@@ -1024,16 +1063,19 @@ cas_status cas_op_gemm(int32_t wtype, const void* W, const void* X, int32_t N, i
                        const float* ws, int32_t epi, void* out, int32_t ldo, void* work, size_t work_bytes,
                        void* stream) {
     if (!W || !X || !out || !work) return CAS_ERR_ARG;
-    if (wtype < CAS_W_F32 || wtype > CAS_W_I8) return CAS_ERR_ARG;
+    if (wtype < CAS_W_F32 || wtype > CAS_W_I4) return CAS_ERR_ARG;
     if (N < 16 || N % 16 || K < 16 || K % 16 || T < 1 || T > 128 || ldo < N) return CAS_ERR_UNSUPPORTED;
     if (epi != CAS_EPI_STORE && epi != CAS_EPI_RESID && epi != CAS_EPI_RAW_I32) return CAS_ERR_ARG;
-    if (epi == CAS_EPI_RAW_I32 && wtype != CAS_W_I8) return CAS_ERR_UNSUPPORTED;
-    if (wtype == CAS_W_I8 && epi != CAS_EPI_RAW_I32 && (!xs || !ws)) return CAS_ERR_ARG;
+    const bool integer = wtype == CAS_W_I8 || wtype == CAS_W_I4;
+    if (epi == CAS_EPI_RAW_I32 && !integer) return CAS_ERR_UNSUPPORTED;
+    if (integer && epi != CAS_EPI_RAW_I32 && (!xs || !ws)) return CAS_ERR_ARG;
     if (work_bytes < cas_op_gemm_work_bytes(wtype, N, K, T)) return CAS_ERR_ARG;
     hipStream_t s = (hipStream_t)stream;
-    const size_t Kp = pad_k(K, wtype), eb = frag_elem_bytes(wtype);
+    const int at = wtype == CAS_W_I4 ? (int)ET_I8 : wtype;  // int4 weights take int8 activations
+    const size_t Kp = pad_k(K, at), eb = frag_elem_bytes(at);
+    const size_t wbytes = wtype == CAS_W_I4 ? (size_t)N * Kp / 2 : (size_t)N * Kp * eb;
     void* wt = work;
-    void* xt = (char*)work + align256((size_t)N * Kp * eb);
+    void* xt = (char*)work + align256(wbytes);
     GemmArgs a{};
     a.W = wt;
     a.X = xt;
@@ -1045,8 +1087,9 @@ cas_status cas_op_gemm(int32_t wtype, const void* W, const void* X, int32_t N, i
     a.out = out;
     a.ldo = ldo;
     const int ep = epi == CAS_EPI_STORE ? EPI_STORE : epi == CAS_EPI_RESID ? EPI_RESID : EPI_RAW;
-    hipError_t e = launch_tile_weight(wtype, W, N, K, wt, 0, 0, 0, s);
-    if (e == hipSuccess) e = launch_tile_act(wtype, X, T, K, xt, s);
+    hipError_t e = wtype == CAS_W_I4 ? launch_pack_weight_i4((const int8_t*)W, N, K, (uint8_t*)wt, s)
+                                     : launch_tile_weight(wtype, W, N, K, wt, 0, 0, 0, s);
+    if (e == hipSuccess) e = launch_tile_act(at, X, T, K, xt, s);
     if (e == hipSuccess) e = launch_gemm(wtype, ET_F32, ep, a, s);
     return e == hipSuccess ? CAS_OK : CAS_ERR_DEVICE;
 }
@@ -1054,7 +1097,14 @@ cas_status cas_op_gemm(int32_t wtype, const void* W, const void* X, int32_t N, i
 cas_status cas_op_quant_rows(int32_t atype, const void* x, int32_t T, int32_t K, int8_t* q, float* s, void* stream) {
     if (!x || !q || !s || T < 1 || K < 1) return CAS_ERR_ARG;
     if (atype != CAS_W_F32 && atype != CAS_W_BF16) return CAS_ERR_ARG;
-    hipError_t e = launch_quant_rows(atype, x, T, K, q, s, 0, (hipStream_t)stream);
+    hipError_t e = launch_quant_rows(atype, x, T, K, q, s, 0, 127, (hipStream_t)stream);
+    return e == hipSuccess ? CAS_OK : CAS_ERR_DEVICE;
+}
+cas_status cas_op_quant_rows_q(int32_t atype, const void* x, int32_t T, int32_t K, int32_t qmax, int8_t* q, float* s,
+                               void* stream) {
+    if (!x || !q || !s || T < 1 || K < 1 || (qmax != 127 && qmax != 7)) return CAS_ERR_ARG;
+    if (atype != CAS_W_F32 && atype != CAS_W_BF16) return CAS_ERR_ARG;
+    hipError_t e = launch_quant_rows(atype, x, T, K, q, s, 0, qmax, (hipStream_t)stream);
     return e == hipSuccess ? CAS_OK : CAS_ERR_DEVICE;
 }
 
@@ -1074,6 +1124,19 @@ cas_status cas_op_quant_weight(int32_t wtype, const void* W, int32_t N, int32_t 
     hipError_t e = launch_tile_weight(wtype, W, N, K, wt, 0, 0, 0, st);
     if (e == hipSuccess) e = launch_quant_weight(wtype, wt, N, K, qt, s, st);
     if (e == hipSuccess) e = launch_untile_weight_i8(qt, N, K, q, st);
+    return e == hipSuccess ? CAS_OK : CAS_ERR_DEVICE;
+}
+cas_status cas_op_quant_weight_i4(int32_t wtype, const void* W, int32_t N, int32_t K, int8_t* q, float* s,
+                                  void* work, size_t work_bytes, void* stream) {
+    if (!W || !q || !s || !work || N < 16 || N % 16 || K < 16 || K % 16) return CAS_ERR_ARG;
+    if (wtype != CAS_W_F32 && wtype != CAS_W_BF16) return CAS_ERR_ARG;
+    if (work_bytes < cas_op_quant_weight_work_bytes(wtype, N, K)) return CAS_ERR_ARG;
+    hipStream_t st = (hipStream_t)stream;
+    void* wt = work;
+    uint8_t* qt = (uint8_t*)((char*)work + align256((size_t)N * pad_k(K, wtype) * frag_elem_bytes(wtype)));
+    hipError_t e = launch_tile_weight(wtype, W, N, K, wt, 0, 0, 0, st);
+    if (e == hipSuccess) e = launch_quant_weight_i4(wtype, wt, N, K, qt, s, st);
+    if (e == hipSuccess) e = launch_untile_weight_i4(qt, N, K, q, st);
     return e == hipSuccess ? CAS_OK : CAS_ERR_DEVICE;
 }
 

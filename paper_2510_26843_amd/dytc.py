@@ -192,13 +192,15 @@ def pld_propose(seq: Sequence[int], k: int, n_max: int = 3, n_min: int = 1) -> T
 # latency prediction (cost coefficients)
 # ----------------------------------------------------------------------------
 
-def roofline_features(shape, run_layers: int, n_rows: int, ctx: int, int8: bool = False) -> np.ndarray:
+def roofline_features(shape, run_layers: int, n_rows: int, ctx: int, act_quant: int = 0) -> np.ndarray:
     """Roofline features of one forward: [1, weight GB of the layers that run
     (+ LM head), KV GB read, dense TFLOP, layers run].  The constant and the
     layer count absorb launch and latency floors, the byte terms the HBM
-    time, the FLOP term the matrix-core time."""
+    time, the FLOP term the matrix-core time.  act_quant 1 (W8A8) reads one
+    byte per weight of the run layers, 2 (W4A4) half a byte."""
     es = 2 if shape.dtype == "bf16" else 4
-    wbytes = run_layers * shape.layer_params() * (1 if int8 else es) + shape.vocab * shape.d_model * es
+    wb = {0: es, 1: 1, 2: 0.5}[int(act_quant)]
+    wbytes = run_layers * shape.layer_params() * wb + shape.vocab * shape.d_model * es
     kv = run_layers * 2 * shape.n_kv_heads * shape.head_dim * es * (ctx + n_rows)
     flops = 2.0 * n_rows * (run_layers * shape.layer_params() + shape.vocab * shape.d_model)
     return np.array([1.0, wbytes / 1e9, kv / 1e9, flops / 1e12, float(run_layers)])
@@ -237,11 +239,11 @@ class LatencyModel:
 @dataclasses.dataclass
 class DraftConfig:
     """A draft model: a DSIA variant of the target (skip mask over the
-    layers, optional int8 activations, optional sink + window attention) or
-    prompt lookup (skip is None and pld is True)."""
+    layers, optional quantised activations: 1 = W8A8, 2 = W4A4, optional sink
+    + window attention) or prompt lookup (skip is None and pld is True)."""
     name: str
     skip: Optional[Tuple[int, ...]] = None
-    act_quant: bool = False
+    act_quant: int = 0
     pld: bool = False
     window: Optional[Tuple[int, int]] = None  # efficient attention: (sink, window) committed slots
 

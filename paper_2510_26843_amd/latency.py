@@ -45,23 +45,24 @@ def skip_mask(n_layers: int, rule: str) -> Optional[List[int]]:
 
 
 def parse_draft(spec: str, n_layers: int):
-    """A draft configuration from '<skip rule>[+int8][@sink:window]'."""
+    """A draft configuration from '<skip rule>[+int8|+int4][@sink:window]'
+    -> (skip mask, act_quant 0/1/2, window)."""
     window = None
     if "@" in spec:
         spec, w = spec.split("@")
         sink, win = w.split(":")
         window = (int(sink), int(win))
-    aq = spec.endswith("+int8")
+    aq = 1 if spec.endswith("+int8") else 2 if spec.endswith("+int4") else 0
     return skip_mask(n_layers, spec.split("+")[0]), aq, window
 
 
-def algorithmic_bytes(shape, T: int, Lc: int, run_layers: int, int8: bool = False,
+def algorithmic_bytes(shape, T: int, Lc: int, run_layers: int, int8: int = 0,
                       window: Optional[Tuple[int, int]] = None) -> int:
     """Bytes one forward must move: the weights of the layers that run (bf16
-    or fp32, or int8 codes plus fp32 per-channel scales) and the LM head
-    once, the KV reads of all visible slots (only the sink and the window
-    of the committed ones under a window) and the writes of the new ones,
-    the embedding rows and the fp32 logits."""
+    or fp32; int8 = 1: int8 codes, 2: 4-bit codes, plus fp32 per-channel
+    scales) and the LM head once, the KV reads of all visible slots (only
+    the sink and the window of the committed ones under a window) and the
+    writes of the new ones, the embedding rows and the fp32 logits."""
     if window and window[1] > 0:
         Lc = min(Lc, window[0] + window[1])
     es = 2 if shape.dtype == "bf16" else 4
@@ -69,7 +70,7 @@ def algorithmic_bytes(shape, T: int, Lc: int, run_layers: int, int8: bool = Fals
     if int8:
         d, q, kv, f = shape.d_model, shape.n_heads * shape.head_dim, shape.n_kv_heads * shape.head_dim, shape.ffn_dim
         rows = (q + 2 * kv) + d + 2 * f + d
-        b = run_layers * (shape.layer_params() + 4 * rows)
+        b = run_layers * (shape.layer_params() // (2 if int(int8) == 2 else 1) + 4 * rows)
     else:
         b = run_layers * shape.layer_params() * es
     b += shape.vocab * shape.d_model * es
@@ -113,11 +114,11 @@ def time_forward(model, toks, parents, skip, aq: bool, reps: int, warmup: int = 
 def sweep(model, shape, Ts: Sequence[int], ctxs: Sequence[int], drafts: Sequence[str], reps: int = 20,
           log=None) -> List[Dict]:
     """One record per (configuration, T, ctx): 'verify' at full depth for
-    every T, and each draft configuration ('<rule>' or '<rule>+int8') for
+    every T, and each draft configuration ('<rule>', '<rule>+int8', '<rule>+int4') for
     every T as well (tree-parallel drafting runs drafts over several rows)."""
     from .synth import gen_tree_tokens
     out = []
-    configs = [("verify", None, False, None)] + [(d,) + parse_draft(d, shape.n_layers) for d in drafts]
+    configs = [("verify", None, 0, None)] + [(d,) + parse_draft(d, shape.n_layers) for d in drafts]
     for ctx in ctxs:
         for T in Ts:
             parents = tree_for(T)
@@ -132,7 +133,7 @@ def sweep(model, shape, Ts: Sequence[int], ctxs: Sequence[int], drafts: Sequence
                 b = algorithmic_bytes(shape, T, ctx, run, int8=aq, window=window)
                 ctx_vis = min(ctx, window[0] + window[1]) if window and window[1] > 0 else ctx
                 fl = algorithmic_flops(shape, T, ctx_vis, run, float(np.mean(depth)))
-                rec = {"config": name, "T": T, "ctx": ctx, "run_layers": run, "act_int8": aq,
+                rec = {"config": name, "T": T, "ctx": ctx, "run_layers": run, "act_quant": aq,
                        "ms": round(r["ms"], 4), "ms_min": round(r["ms_min"], 4), "ms_max": round(r["ms_max"], 4),
                        "tokens_per_s": round(T / (r["ms"] * 1e-3), 1), "bytes": b,
                        "hbm_gbps": round(b / (r["ms"] * 1e-3) / 1e9, 1),
@@ -162,8 +163,8 @@ def main(argv=None) -> None:
     ap.add_argument("--T", default="1,8,16,32,64,128")
     ap.add_argument("--ctx", default="512,2048,8192")
     ap.add_argument("--drafts", default="",
-                    help="draft configurations separated by ';', e.g. 'odd;q3;odd+int8;odd@4:1024' "
-                         "(skip rule, +int8 activations, @sink:window attention)")
+                    help="draft configurations separated by ';', e.g. 'odd;q3;odd+int8;odd+int4;odd@4:1024' "
+                         "(skip rule, +int8 or +int4 activations, @sink:window attention)")
     ap.add_argument("--reps", type=int, default=20)
     ap.add_argument("--out", default="")
     ap.add_argument("--md", default="")
@@ -178,8 +179,10 @@ def main(argv=None) -> None:
     w = synth.gen_weights(shape, seed=0)
     m = cas.Model(shape, max_ctx=max(ctxs) + max(Ts), max_tree=max(128, max(Ts)), device=0)
     m.load_weights(w)
-    if any(d.endswith("+int8") for d in drafts):
+    if any(d.split("@")[0].endswith("+int8") for d in drafts):
         m.build_int8()
+    if any(d.split("@")[0].endswith("+int4") for d in drafts):
+        m.build_int4()
     del w
     log(f"[latency] {args.shape} ready in {time.perf_counter() - t0:.1f} s")
     recs = sweep(m, shape, Ts, ctxs, drafts, args.reps, log)

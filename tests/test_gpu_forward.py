@@ -1,5 +1,5 @@
 """Forward-level parity of the HIP path against the CPU oracle through the C
-ABI: tree verify, draft calls (layer skip, int8 activations), greedy
+ABI: tree verify, draft calls (layer skip, int8 and int4 activations), greedy
 acceptance, KV compaction, prefill, losslessness, error paths.
 
 Tolerances (per tree node row): max_v |gpu - oracle| <= tol * max_v |oracle|,
@@ -12,6 +12,11 @@ the next int8 code with probability ~1/6, a full code step each, so the two
 sides' drafts drift apart by about as much as int8 noise itself (measured
 2.9e-2..3.7e-2 against 3.0e-2..4.5e-2 int8-vs-full); with a single node and
 no context the attention is exact and the int8 path agrees to 1e-3.
+W4A4 (int4 codes, 18x coarser steps): 2e-2 for fp32 decoders (one flipped
+code moves a product 18x as far as an int8 flip); 1e-2 for bf16 decoders
+with one node and no context; over a bf16 tree, where the drift argument
+above applies with rarer but larger flips, the library-vs-oracle error must
+stay below half the oracle's own W4A4-vs-full distance.
 Acceptance and compaction are index and byte work: exact.
 """
 import dataclasses
@@ -36,12 +41,14 @@ def weights():
     return {s.name: synth.gen_weights(s, seed=9) for s in (TINY, GQA, MHA)}
 
 
-def _pair(shape, w, prompt, max_ctx=512, int8=False):
+def _pair(shape, w, prompt, max_ctx=512, int8=False, int4=False):
     g = cas.Model(shape, max_ctx=max_ctx, max_tree=128)
     g.load_weights(w)
     if int8:
         g.build_int8()
-    o = O.OracleModel(shape, w, max_ctx=max_ctx, int8=int8)
+    if int4:
+        g.build_int4()
+    o = O.OracleModel(shape, w, max_ctx=max_ctx, int8=int8, int4=int4)
     if len(prompt):
         g.prefill(prompt)
         o.prefill(list(prompt))
@@ -71,14 +78,15 @@ def test_verify_parity(weights, name, tree, plen):
 @pytest.mark.parametrize("name,skip,aq,tol", [("tiny", [0, 1, 1, 0], False, 1e-4), ("tiny", [0, 1, 1, 0], True, 1e-3),
                                               ("tiny", [1, 1, 1, 1], False, 1e-4), ("gqa_small", [0, 1], True, 6e-2),
                                               ("mha_small", [1, 0], False, 2e-2), ("mha_small", [0, 0], True, 6e-2),
-                                              ("gqa_small", [0, 1], False, 2e-2)])
+                                              ("gqa_small", [0, 1], False, 2e-2), ("tiny", [0, 1, 1, 0], 2, 2e-2),
+                                              ("tiny", [0, 0, 0, 0], 2, 2e-2)])
 def test_draft_parity(weights, name, skip, aq, tol):
     shape = {"tiny": TINY, "gqa_small": GQA, "mha_small": MHA}[name]
     w = weights[name]
     prompt = synth.gen_prompt(shape.vocab, 33, seed=3)
     parents = synth.tree_from_branching((3, 2, 1), 15)
     toks = synth.gen_tree_tokens(parents, shape.vocab, seed=4)
-    g, o = _pair(shape, w, prompt, int8=aq)
+    g, o = _pair(shape, w, prompt, int8=aq == 1, int4=aq == 2)
     # the tree fed depth by depth in appended calls, as tree-parallel drafts do
     for a, b in ((0, 1), (1, 4), (4, 10), (10, 15)):
         got = g.forward(toks[a:b], parents[a:b], a, skip=skip, act_quant=aq)
@@ -100,6 +108,48 @@ def test_int8_draft_bf16_single_node(weights, name):
         ref = o.forward([tok], [-1], act_quant=True)
         err = _row_err(got, ref)
         assert err < 1e-3, (tok, err)
+    g.close()
+
+
+@pytest.mark.parametrize("name", ["gqa_small", "mha_small"])
+def test_int4_draft_bf16_single_node(weights, name):
+    """W4A4 with one node and no context, where the attention is exact: codes,
+    scales, packed weights and dequantisation agree with the oracle (a code
+    flip from fp32-against-fp64 rounding of an input is rare at 15 levels)."""
+    shape = {"gqa_small": GQA, "mha_small": MHA}[name]
+    g, o = _pair(shape, weights[name], [], int4=True)
+    for tok in (3, 77, 500):
+        got = g.forward([tok], [-1], act_quant=2)
+        ref = o.forward([tok], [-1], act_quant=2)
+        err = _row_err(got, ref)
+        assert err < 1e-2, (tok, err)
+    g.close()
+
+
+@pytest.mark.parametrize("name", ["gqa_small", "mha_small"])
+def test_int4_draft_bf16_tree_report(weights, name):
+    """W4A4 over a 15-node tree after a 33-token prompt, fed depth by depth:
+    prints the library-vs-oracle row error next to the oracle's own
+    W4A4-vs-full distance (the quantisation noise itself)."""
+    shape = {"gqa_small": GQA, "mha_small": MHA}[name]
+    w = weights[name]
+    prompt = synth.gen_prompt(shape.vocab, 33, seed=3)
+    parents = synth.tree_from_branching((3, 2, 1), 15)
+    toks = synth.gen_tree_tokens(parents, shape.vocab, seed=4)
+    g, o = _pair(shape, w, prompt, int4=True)
+    worst, noise = 0.0, 0.0
+    for a, b in ((0, 1), (1, 4), (4, 10), (10, 15)):
+        got = g.forward(toks[a:b], parents[a:b], a, act_quant=2)
+        ref = o.forward(toks[a:b], parents[a:b], a, act_quant=2)
+        worst = max(worst, _row_err(got, ref))
+    full = O.OracleModel(shape, w, max_ctx=512)
+    full.prefill(list(prompt))
+    fref = full.forward(toks, parents)
+    o2 = O.OracleModel(shape, w, max_ctx=512, int4=True)
+    o2.prefill(list(prompt))
+    noise = _row_err(o2.forward(toks, parents, act_quant=2), fref)
+    print(f"[w4a4] {name}: library vs oracle {worst:.3e}; oracle W4A4 vs full {noise:.3e}", flush=True)
+    assert worst < 0.5 * noise, (worst, noise)
     g.close()
 
 
@@ -301,6 +351,8 @@ def test_validation_errors_leave_state_unchanged(weights):
     expect(cas.ERR_CAPACITY, lambda: g.forward(list(range(17)), synth.chain_parents(17)))  # > max_tree
     expect(cas.ERR_CAPACITY, lambda: g.forward(list(range(16)), synth.chain_parents(16)))  # > max_ctx
     expect(cas.ERR_STATE, lambda: g.forward(toks, [-1, 0, 1], act_quant=True))  # no int8 copy
+    expect(cas.ERR_STATE, lambda: g.forward(toks, [-1, 0, 1], act_quant=2))  # no int4 copy
+    expect(cas.ERR_ARG, lambda: g.forward(toks, [-1, 0, 1], act_quant=3))
     expect(cas.ERR_TREE, lambda: g.forward(toks, [0, 0, 1], node_offset=3))    # no open round
     expect(cas.ERR_STATE, lambda: g.accept())
     expect(cas.ERR_STATE, lambda: g.compact([0]))

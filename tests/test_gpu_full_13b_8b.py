@@ -5,7 +5,9 @@ Each model has all of its layers.
   - a verify forward over the 64-node tree (4,4,4,4);
   - a draft level that skips the odd layers (20 of 40) with per-token int8
     activations against the per-channel int8 weight copy: the root, then
-    its four children appended to the round.
+    its four children appended to the round;
+  - the same draft level in the W4A4 form (int4 codes against the packed
+    int4 weight copy).
 - Llama-3-8B (GQA: 32 query heads on 8 KV heads, vocab 128256, theta 5e5),
   bf16, context 4096:
   - a verify forward over a balanced 64-node tree;
@@ -19,7 +21,9 @@ Bars, per row relative to max |oracle logit|:
 - 4e-2 for bf16 forwards at full depth;
 - 1e-1 for the int8 draft over 20 layers, and less than half of the
   distance between the oracle's int8 and bf16 drafts (the test measures
-  both).
+  both);
+- for the W4A4 draft, less than half of the distance between the oracle's
+  W4A4 and bf16 drafts.
 
 At full depth the random N(0, 0.02^2) decoders amplify differences of one
 bf16 step. With int8 activations two correct implementations drift apart at
@@ -81,7 +85,7 @@ def _verify_sampled(g, o, shape, ctx, parents, sample, seed):
 
 
 @pytest.mark.timeout(900)
-def test_13b_verify_and_int8_draft():
+def test_13b_verify_and_quantised_drafts():
     shape = synth.SHAPES["llama2_13b"]
     ctx = 2048
     print("[full] generating 13B weights", flush=True)
@@ -90,13 +94,14 @@ def test_13b_verify_and_int8_draft():
     try:
         g.load_weights(w)
         g.build_int8()
+        g.build_int4()
         o = O.OracleModel(shape, w, max_ctx=ctx + 128)
         odd = [l % 2 for l in range(shape.n_layers)]
         wd = dict(w)
         wd["layers"] = [None if odd[l] else w["layers"][l] for l in range(shape.n_layers)]
-        od = O.OracleModel(shape, wd, max_ctx=ctx + 128, int8=True)
+        od = O.OracleModel(shape, wd, max_ctx=ctx + 128, int8=True, int4=True)
         _load_cache(shape, ctx, 2000, [g, o, od])
-        print("[full] 13B model, int8 copy and cache ready", flush=True)
+        print("[full] 13B model, int8 and int4 copies and cache ready", flush=True)
         parents = synth.tree_from_branching(*synth.TREE_13B)
         err = _verify_sampled(g, o, shape, ctx, parents, (63, 30), seed=13)
         assert err < TOL_DEEP, err
@@ -116,6 +121,16 @@ def test_13b_verify_and_int8_draft():
         assert max(e1, e2) < TOL_DEEP_I8, (e1, e2)
         # and closer to the oracle's int8 draft than int8 is to bf16
         assert e1 < 0.5 * q1 and e2 < 0.5 * q2, (e1, q1, e2, q2)
+        # W4A4 draft level, same calls (a new round)
+        h1 = g.forward(toks[:1], [-1], 0, skip=odd, act_quant=2)
+        s1 = od.forward(toks[:1], [-1], 0, skip=odd, act_quant=2)
+        h2 = g.forward(toks[1:5], parents[1:5], 1, skip=odd, act_quant=2)
+        s2 = od.forward(toks[1:5], parents[1:5], 1, skip=odd, act_quant=2)
+        f1, f2 = _row_err(h1, s1), _row_err(h2, s2)
+        p1, p2 = _row_err(s1, b1), _row_err(s2, b2)
+        print(f"[full] 13B W4A4 draft (20 of 40 layers): library vs oracle root {f1:.2e}, level 1 {f2:.2e}; "
+              f"W4A4 vs bf16 (oracle) root {p1:.2e}, level 1 {p2:.2e}", flush=True)
+        assert f1 < 0.5 * p1 and f2 < 0.5 * p2, (f1, p1, f2, p2)
     finally:
         g.close()
 

@@ -1,7 +1,7 @@
 """Kernel-level parity of the HIP library against the CPU oracle, through the
 C ABI (include/cas_ops.h), on identical seeded inputs.
 
-Bars: int8 codes, scales and integer accumulators bit-exact; the fp32/bf16
+Bars: int8 and int4 codes, scales and integer accumulators bit-exact; the fp32/bf16
 GEMM within the rigorous fp32 summation bound K * 2^-23 * sum_k |x_k w_k|; the
 bf16 attention within 1e-2 of max |v| (probabilities are rounded to bf16 for
 the PV product: a relative 2^-9 per weight on a convex combination of v).
@@ -91,6 +91,71 @@ def test_gemm_int8_bit_exact(N, K, T):
     # dequantisation in fp32: (float(acc) * s_x) * s_w
     want = (ref.astype(np.float32) * xs[:, None]).astype(np.float32) * ws[None, :]
     assert np.array_equal(y.cpu().numpy().view(np.uint32), want.astype(np.float32).view(np.uint32))
+
+
+@pytest.mark.parametrize("N,K,T", [(64, 4096, 32), (48, 688, 5), (16, 13824, 3), (32, 256, 100), (16, 5120, 64),
+                                   (8192, 512, 32), (8256, 256, 1), (8192, 256, 65), (16512, 256, 17),
+                                   (12288, 128, 5), (24480, 128, 33), (64, 272, 128), (8208, 4096, 1)])
+def test_gemm_int4_bit_exact(N, K, T):
+    """Packed int4 weights (codes in [-7, 7]) against int8-held int4
+    activation codes: exact int32 accumulators on every kernel path (one-tile
+    workgroups, multi-tile, all column-tile counts, K not a multiple of the
+    256-wide chunk), and the fp32 dequantisation."""
+    rng = np.random.default_rng(N * 5 + K + T)
+    qw = rng.integers(-7, 8, (N, K)).astype(np.int8)
+    qx = rng.integers(-7, 8, (T, K)).astype(np.int8)
+    qx[0, :] = -7
+    qw[0, :] = 7  # largest accumulator magnitude
+    qw[1, ::2] = -7
+    if T > 1:
+        qx[1, :] = 0
+    acc = torch.zeros((T, N), dtype=torch.int32, device=DEV)
+    cas.op_gemm(cas.W_I4, _i8_dev(qw), _i8_dev(qx), N, K, T, acc, N, epi=cas.EPI_RAW_I32)
+    xs = (rng.random(T).astype(np.float32) + np.float32(0.01)) / np.float32(7)
+    ws = (rng.random(N).astype(np.float32) + np.float32(0.01)) / np.float32(7)
+    y = torch.zeros((T, N), dtype=torch.float32, device=DEV)
+    cas.op_gemm(cas.W_I4, _i8_dev(qw), _i8_dev(qx), N, K, T, y, N, epi=cas.EPI_STORE, xs=_f32_dev(xs), ws=_f32_dev(ws))
+    torch.cuda.synchronize()
+    ref = O.dot_i8_matrix(qx, qw)
+    assert np.array_equal(acc.cpu().numpy(), ref)
+    want = (ref.astype(np.float32) * xs[:, None]).astype(np.float32) * ws[None, :]
+    assert np.array_equal(y.cpu().numpy().view(np.uint32), want.astype(np.float32).view(np.uint32))
+
+
+@pytest.mark.parametrize("T,K,bf16", [(64, 4096, True), (9, 688, False), (3, 11008, True)])
+def test_quant_rows_int4_bit_exact(T, K, bf16):
+    x = synth.gen_activations(T, K, seed=T + K + 1)
+    if bf16:
+        xb = synth.f32_to_bf16_bits(x)
+        xf = synth.bf16_bits_to_f32(xb)
+        xd = _bf16_dev(xb)
+    else:
+        xf = x
+        xd = _f32_dev(x)
+    q = torch.zeros((T, K), dtype=torch.int8, device=DEV)
+    s = torch.zeros(T, dtype=torch.float32, device=DEV)
+    cas.op_quant_rows(cas.W_BF16 if bf16 else cas.W_F32, xd, T, K, q, s, qmax=7)
+    torch.cuda.synchronize()
+    qr, sr = O.quant_rows(xf, 7)
+    assert np.array_equal(s.cpu().numpy().view(np.uint32), sr.view(np.uint32))
+    assert np.array_equal(q.cpu().numpy(), qr)
+
+
+@pytest.mark.parametrize("rows,cols", [(96, None), (48, 688)])
+def test_quant_weight_int4_bit_exact(rows, cols):
+    """The packed int4 copy, unpacked by the library: codes and scales equal
+    the oracle's (K = 4096, and K = 688 with a partial last chunk)."""
+    shape = synth.SHAPES["llama2_7b"]
+    w = synth.gen_tensor(shape.with_layers(1), "wo", 0, seed=4)[:rows]
+    if cols:
+        w = np.ascontiguousarray(w[:, :cols])
+    q = torch.zeros(w.shape, dtype=torch.int8, device=DEV)
+    s = torch.zeros(w.shape[0], dtype=torch.float32, device=DEV)
+    cas.op_quant_weight(cas.W_BF16, _bf16_dev(w), w.shape[0], w.shape[1], q, s, qmax=7)
+    torch.cuda.synchronize()
+    qr, sr = O.quant_weight(w, bf16=True, qmax=7)
+    assert np.array_equal(s.cpu().numpy().view(np.uint32), sr.view(np.uint32))
+    assert np.array_equal(q.cpu().numpy(), qr)
 
 
 @pytest.mark.parametrize("T,K,bf16", [(64, 4096, True), (9, 688, False), (3, 11008, True), (128, 256, False)])
