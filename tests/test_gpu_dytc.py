@@ -4,7 +4,8 @@
   bit-exact (stable descending order, ties to the lower id), probabilities
   against an fp64 softmax of the same row.
 - DyTC speculative decoding through the library (tree-parallel draft calls
-  that append nodes, top-K candidates, full-depth verify, commit) equals
+  that append nodes, over layer-skip, W8A8 and W4A4 levels and prompt
+  lookup; top-K candidates, full-depth verify, commit) equals
   greedy autoregressive decoding of the oracle and of the library, token for
   token.  The models are the tiny fp32 decoder and a small bf16 GQA decoder;
   bf16 mismatches are excused only where the oracle's top-1/top-2 margin is
@@ -67,8 +68,8 @@ def test_topk_errors(weights):
 def _cfgs(L):
     q3 = tuple(1 if l % 4 == 3 else 0 for l in range(L))
     odd = tuple(l % 2 for l in range(L))
-    return [dytc.DraftConfig("q3", q3), dytc.DraftConfig("odd", odd), dytc.DraftConfig("odd_i8", odd, True),
-            dytc.DraftConfig("pld", pld=True)]
+    return [dytc.DraftConfig("q3", q3), dytc.DraftConfig("odd", odd), dytc.DraftConfig("odd_i8", odd, 1),
+            dytc.DraftConfig("odd_i4", odd, 2), dytc.DraftConfig("pld", pld=True)]
 
 
 @pytest.mark.parametrize("name", ["tiny", "gqa"])
@@ -82,13 +83,14 @@ def test_dytc_decoding_through_the_library_is_lossless(weights, name):
     g = cas.Model(shape, max_ctx=256, max_tree=64)
     g.load_weights(w)
     g.build_int8()
+    g.build_int4()
     cfgs = _cfgs(shape.n_layers)
     params = dytc.DytcParams(max_tree=24, k_max=3, t_min=1.1, top_k=3, top_p=0.5)
     out, excused = [], 0
     stats = {}
     while len(out) < n_new:
-        est = dytc.AcceptanceEstimator({"q3": 0.9, "odd": 0.8, "odd_i8": 0.75, "pld": 0.05})
-        cost = {"q3": 0.3, "odd": 0.2, "odd_i8": 0.18, "pld": 0.01}
+        est = dytc.AcceptanceEstimator({"q3": 0.9, "odd": 0.8, "odd_i8": 0.75, "odd_i4": 0.72, "pld": 0.05})
+        cost = {"q3": 0.3, "odd": 0.2, "odd_i8": 0.18, "odd_i4": 0.15, "pld": 0.01}
         seg = dytc.cas_decode_dytc(dytc.LibraryBackend(g), prompt + out, n_new - len(out), cfgs, cfgs[-1], est,
                                    cost, params, shape.n_layers, stats)
         i = next((k for k, (a, b) in enumerate(zip(seg, ref[len(out):])) if a != b), None)
@@ -105,7 +107,7 @@ def test_dytc_decoding_through_the_library_is_lossless(weights, name):
         excused += 1
         out = ref[:pos + 1]
     assert out[:n_new] == ref
-    assert sum(stats["expansions"].get(c, 0) for c in ("q3", "odd", "odd_i8")) > 0
+    assert sum(stats["expansions"].get(c, 0) for c in ("q3", "odd", "odd_i8", "odd_i4")) > 0
     # the library's own greedy decoding agrees with its speculative decoding
     if excused == 0:
         assert decode.ar_decode(g, prompt, n_new) == ref
