@@ -887,7 +887,8 @@ __device__ __forceinline__ void attn_merge_o(f32x4& acc, const f32x4 o, float f)
 }
 __device__ __forceinline__ void attn_merge_l(float& L, float l, float f) { L = fmaf(l, f, L); }
 
-// Workgroup = (split of KV slots, kv head, chunk of 32 query rows).  The query
+// Workgroup = (split of KV slots, kv head, JT query tiles of 16 rows); each
+// of the four waves owns one part (two key tiles) of the split.  The query
 // rows of a kv head are its G query heads x T tokens (each head padded to a
 // multiple of 16 rows), so GQA groups share every K/V fragment.  Scores come
 // out of the QK^T MFMA with slots along the row index; the cache puts slots
