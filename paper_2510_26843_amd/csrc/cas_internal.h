@@ -147,6 +147,11 @@ struct AttnArgs {
     // [0, win_sink) and [Lc - win_len, Lc) are visible; the grid covers only
     // the key tiles that hold them
     int win_sink, win_len;
+    // bf16 path with qout set: the output is the rows' per-token codes in
+    // [-qmax, qmax] (tiled int8 layout) with their scales, in place of out
+    int8_t* qout;
+    float* qscale;
+    int qmax;
 };
 size_t attention_work_bytes(int n_slots, int T, int H, int hd);
 int attention_splits(int n_slots);

@@ -732,6 +732,16 @@ __device__ __forceinline__ void st4(uint16_t* out, size_t o, float a, float b, f
     *(uint2*)(out + o) = make_uint2(lo, hi);
 }
 
+__device__ __forceinline__ void st4q(int8_t* q, size_t o, float a, float b, float c, float d) {
+    const uint32_t v = (uint32_t)(uint8_t)(int8_t)a | ((uint32_t)(uint8_t)(int8_t)b << 8) |
+                       ((uint32_t)(uint8_t)(int8_t)c << 16) | ((uint32_t)(uint8_t)(int8_t)d << 24);
+    *(uint32_t*)(q + o) = v;
+}
+// Code of x at scale sc in [-qm, qm] (qm 127: int8, 7: int4).
+__device__ __forceinline__ float qcode(float x, float sc, float qm) {
+    return sc != 0.f ? fminf(fmaxf(rintf(x / sc), -qm), qm) : 0.f;
+}
+
 // A workgroup covers 4 waves x ATT_TPW key tiles of 32 slots.
 static constexpr int ATT_WAVES = 4;
 static constexpr int ATT_TPW = 2;
@@ -1172,43 +1182,51 @@ __global__ void __launch_bounds__(64 * QT, 2) k_attn_rows(const AttnArgs a, floa
     }
 }
 
-// Merge the KV splits of R query rows of one head.  Each thread owns one
-// (row, 4 d) item and merges the splits in split order with a running max
+// The attention output of one query row of one head at 4 consecutive d: the
+// KV splits' partial states merged in split order with a running max
 // (online softmax), eight splits' (m, l) pairs and partial outputs loaded at
-// a time: a single round of loads for contexts up to 2048 slots.
+// a time (one round of loads for contexts up to 2048 slots), then
+// normalised.  row = head * T + t.
+template <int HD>
+__device__ __forceinline__ f32x4 attn_merge_row(const AttnArgs& a, int S, size_t row, int d4) {
+#pragma clang fp contract(off)
+    const size_t sstride = (size_t)a.H * a.T;  // rows between splits
+    float M = -1e30f, L = 0.f;
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+    for (int s0 = 0; s0 < S; s0 += 8) {
+        float2 ml[8];
+        f32x4 po[8];
+#pragma unroll
+        for (int k = 0; k < 8; ++k) {
+            const size_t r = row + (size_t)min(s0 + k, S - 1) * sstride;
+            ml[k] = *(const float2*)(a.part_ml + r * 2);
+            po[k] = *(const f32x4*)(a.part_o + r * HD + d4);
+        }
+#pragma unroll
+        for (int k = 0; k < 8; ++k) {
+            if (s0 + k < S) {
+                const float mn = fmaxf(M, ml[k].x);
+                const float fo = exp2f(M - mn), fn = exp2f(ml[k].x - mn);
+                acc = acc * fo + po[k] * fn;
+                L = L * fo + ml[k].y * fn;
+                M = mn;
+            }
+        }
+    }
+    const float inv = L > 0.f ? 1.f / L : 0.f;
+    return acc * inv;
+}
+
+// Merge the KV splits of R query rows of one head; each thread owns one
+// (row, 4 d) item.
 template <int HD, int R = 16>
 __global__ void __launch_bounds__(256) k_attn_merge(const AttnArgs a, int S) {
     const int h = blockIdx.y, t0 = blockIdx.x * R, T = a.T;
     const int NTo = col_tiles(T);
-    const size_t sstride = (size_t)a.H * T;  // rows between splits
     for (int idx = threadIdx.x; idx < R * (HD / 4); idx += blockDim.x) {
         const int rr = idx / (HD / 4), d4 = (idx % (HD / 4)) * 4, t = t0 + rr;
         if (t >= T) continue;
-        const size_t row = (size_t)h * T + t;
-        float M = -1e30f, L = 0.f;
-        f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-        for (int s0 = 0; s0 < S; s0 += 8) {
-            float2 ml[8];
-            f32x4 po[8];
-#pragma unroll
-            for (int k = 0; k < 8; ++k) {
-                const size_t r = row + (size_t)min(s0 + k, S - 1) * sstride;
-                ml[k] = *(const float2*)(a.part_ml + r * 2);
-                po[k] = *(const f32x4*)(a.part_o + r * HD + d4);
-            }
-#pragma unroll
-            for (int k = 0; k < 8; ++k) {
-                if (s0 + k < S) {
-                    const float mn = fmaxf(M, ml[k].x);
-                    const float fo = exp2f(M - mn), fn = exp2f(ml[k].x - mn);
-                    acc = acc * fo + po[k] * fn;
-                    L = L * fo + ml[k].y * fn;
-                    M = mn;
-                }
-            }
-        }
-        const float inv = L > 0.f ? 1.f / L : 0.f;
-        acc *= inv;
+        const f32x4 acc = attn_merge_row<HD>(a, S, (size_t)h * T + t, d4);
         const int kk = h * HD + d4;
         if (a.out_tiled) {
             st4((uint16_t*)a.out, xt_off(t, kk, NTo, 8), acc[0], acc[1], acc[2], acc[3]);
@@ -1219,6 +1237,43 @@ __global__ void __launch_bounds__(256) k_attn_merge(const AttnArgs a, int S) {
             o[2] = f2bf(acc[2]);
             o[3] = f2bf(acc[3]);
         }
+    }
+}
+
+// Merge and quantise for the quantised-activation drafts: one workgroup per
+// query row merges every head of the row (the values k_attn_merge would
+// store, rounded to bf16), takes the row's amax and writes the row's codes
+// (s = amax / qm, tiled int8 layout, pad zero) and scale, the work of
+// k_attn_merge and k_quant_rows_tiled in one launch.  NI (row, 4 d) items
+// per thread.
+static constexpr int MQ_THREADS = 1024;
+template <int HD, int NI>
+__global__ void __launch_bounds__(MQ_THREADS) k_attn_merge_q(const AttnArgs a, int S) {
+    __shared__ float red[MQ_THREADS / 64];
+    const int t = blockIdx.x, T = a.T, NT = col_tiles(T), K = a.H * HD;
+    const int kpq = (K + 255) / 256 * 256;
+    f32x4 v[NI];
+    float amax = 0.f;
+#pragma unroll
+    for (int i = 0; i < NI; ++i) {
+        const int k4 = (threadIdx.x + MQ_THREADS * i) * 4;
+        v[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+        if (k4 < K) {
+            const f32x4 acc = attn_merge_row<HD>(a, S, (size_t)(k4 / HD) * T + t, k4 % HD);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) v[i][e] = bf2f(f2bf(acc[e]));
+            amax = fmaxf(amax, fmaxf(fmaxf(fabsf(v[i][0]), fabsf(v[i][1])), fmaxf(fabsf(v[i][2]), fabsf(v[i][3]))));
+        }
+    }
+    amax = block_max<MQ_THREADS / 64>(amax, red);
+    const float qm = (float)a.qmax, sc = amax / qm;
+    if (threadIdx.x == 0) a.qscale[t] = sc;
+#pragma unroll
+    for (int i = 0; i < NI; ++i) {
+        const int k4 = (threadIdx.x + MQ_THREADS * i) * 4;
+        if (k4 < kpq)
+            st4q(a.qout, xt_off(t, k4, NT, 16), qcode(v[i][0], sc, qm), qcode(v[i][1], sc, qm), qcode(v[i][2], sc, qm),
+                 qcode(v[i][3], sc, qm));
     }
 }
 
@@ -1296,16 +1351,26 @@ hipError_t launch_attention(int atype, const AttnArgs& a, hipStream_t s) {
     const bool rows = nct >= 4 && Tp >= 32;
     const int JT = (G == 1 && S * a.Hkv * nct >= 1024) ? 2 : 1;
     const int nrc = (nct + JT - 1) / JT;
+    // quantised output: one merge-and-quantise workgroup per row
+    const int K = a.H * a.hd, kpq = (K + 255) / 256 * 256;
+    const int ni = (kpq / 4 + MQ_THREADS - 1) / MQ_THREADS;
+    if (a.qout && (ni > 4 || (a.qmax != 127 && a.qmax != 7))) return hipErrorInvalidValue;
     if (a.hd == 128) {
         if (rows) hipLaunchKernelGGL((k_attn_rows<128, 4>), dim3(S, a.Hkv, (nct + 3) / 4), dim3(256), 0, s, a, scale_log2);
         else if (JT == 2) hipLaunchKernelGGL((k_attn_bf16<128, 2>), dim3(S, a.Hkv, nrc), dim3(256), 0, s, a, scale_log2);
         else hipLaunchKernelGGL((k_attn_bf16<128, 1>), dim3(S, a.Hkv, nrc), dim3(256), 0, s, a, scale_log2);
-        hipLaunchKernelGGL((k_attn_merge<128, 4>), mg, dim3(128), 0, s, a, S);
+        if (!a.qout) hipLaunchKernelGGL((k_attn_merge<128, 4>), mg, dim3(128), 0, s, a, S);
+        else if (ni <= 1) hipLaunchKernelGGL((k_attn_merge_q<128, 1>), dim3(a.T), dim3(MQ_THREADS), 0, s, a, S);
+        else if (ni <= 2) hipLaunchKernelGGL((k_attn_merge_q<128, 2>), dim3(a.T), dim3(MQ_THREADS), 0, s, a, S);
+        else hipLaunchKernelGGL((k_attn_merge_q<128, 4>), dim3(a.T), dim3(MQ_THREADS), 0, s, a, S);
     } else if (a.hd == 64) {
         if (rows) hipLaunchKernelGGL((k_attn_rows<64, 4>), dim3(S, a.Hkv, (nct + 3) / 4), dim3(256), 0, s, a, scale_log2);
         else if (JT == 2) hipLaunchKernelGGL((k_attn_bf16<64, 2>), dim3(S, a.Hkv, nrc), dim3(256), 0, s, a, scale_log2);
         else hipLaunchKernelGGL((k_attn_bf16<64, 1>), dim3(S, a.Hkv, nrc), dim3(256), 0, s, a, scale_log2);
-        hipLaunchKernelGGL((k_attn_merge<64, 4>), mg, dim3(64), 0, s, a, S);
+        if (!a.qout) hipLaunchKernelGGL((k_attn_merge<64, 4>), mg, dim3(64), 0, s, a, S);
+        else if (ni <= 1) hipLaunchKernelGGL((k_attn_merge_q<64, 1>), dim3(a.T), dim3(MQ_THREADS), 0, s, a, S);
+        else if (ni <= 2) hipLaunchKernelGGL((k_attn_merge_q<64, 2>), dim3(a.T), dim3(MQ_THREADS), 0, s, a, S);
+        else hipLaunchKernelGGL((k_attn_merge_q<64, 4>), dim3(a.T), dim3(MQ_THREADS), 0, s, a, S);
     } else {
         return hipErrorInvalidValue;
     }
@@ -1352,16 +1417,6 @@ hipError_t launch_kv_convert(int atype, void* kc, void* vt, const void* k_rows, 
 // whole CU (measured faster than 4 waves once split-K partials are folded in).
 static constexpr int NORM_THREADS = 1024;
 static constexpr int NORM_MAXV = 4;  // float4 per thread: rows up to 16384 elements
-
-__device__ __forceinline__ void st4q(int8_t* q, size_t o, float a, float b, float c, float d) {
-    const uint32_t v = (uint32_t)(uint8_t)(int8_t)a | ((uint32_t)(uint8_t)(int8_t)b << 8) |
-                       ((uint32_t)(uint8_t)(int8_t)c << 16) | ((uint32_t)(uint8_t)(int8_t)d << 24);
-    *(uint32_t*)(q + o) = v;
-}
-// Code of x at scale sc in [-qm, qm] (qm 127: int8, 7: int4).
-__device__ __forceinline__ float qcode(float x, float sc, float qm) {
-    return sc != 0.f ? fminf(fmaxf(rintf(x / sc), -qm), qm) : 0.f;
-}
 
 // RMSNorm of one row of the residual stream, written as tiled activations
 // (pad columns zero) or, with Q, straight to the row's quantisation (codes

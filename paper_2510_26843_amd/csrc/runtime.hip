@@ -342,8 +342,14 @@ hipError_t enqueue_forward(cas_ctx* c, int T, const uint8_t* skip, int aq) {
         RUN(CAS_K_GEMM_QKV, launch_gemm(wq, et, EPI_QKV, g, s));
         at.kc = kc;
         at.vt = vt;
+        // quantised drafts on bf16 models: the attention's merge writes the
+        // O projection's input codes itself
+        const bool fused_q = aq && et == ET_BF16;
+        at.qout = fused_q ? c->d_xq : nullptr;
+        at.qscale = fused_q ? c->d_xs : nullptr;
+        at.qmax = qmax;
         RUN(CAS_K_ATTN, launch_attention(et, at, s));
-        if (aq) RUN(CAS_K_QUANT, launch_quant_rows(et, c->d_ao, T, H * hd, c->d_xq, c->d_xs, 1, qmax, s));
+        if (aq && !fused_q) RUN(CAS_K_QUANT, launch_quant_rows(et, c->d_ao, T, H * hd, c->d_xq, c->d_xs, 1, qmax, s));
         GemmArgs go{};
         go.T = T;
         go.N = d;
