@@ -11,7 +11,8 @@ quarter of the attention outputs by one bf16 step, and each such move flips
 the next int8 code with probability ~1/6, a full code step each, so the two
 sides' drafts drift apart by about as much as int8 noise itself (measured
 2.9e-2..3.7e-2 against 3.0e-2..4.5e-2 int8-vs-full); with a single node and
-no context the attention is exact and the int8 path agrees to 1e-3.
+no context the attention is exact and the int8 path agrees to 1e-3, and
+with the same synthetic committed KV on both sides rows match to 1e-5.
 W4A4 (int4 codes, 18x coarser steps): 2e-2 for fp32 decoders (one flipped
 code moves a product 18x as far as an int8 flip); 1e-2 for bf16 decoders
 with one node and no context, and 1e-4 for a bf16 tree without context.
@@ -127,13 +128,13 @@ def test_int4_draft_bf16_single_node(weights, name):
     g.close()
 
 
-def _int4_tree(shape, w, ctx, skip, window):
-    """15-node W4A4 tree fed depth by depth after ctx committed slots of a
-    seeded synthetic KV cache loaded identically into both sides (so the two
-    start from the same bits)."""
+def _int4_tree(shape, w, ctx, skip, window, aq=2):
+    """15-node quantised draft tree (aq 2: W4A4, 1: W8A8) fed depth by depth
+    after ctx committed slots of a seeded synthetic KV cache loaded
+    identically into both sides (so the two start from the same bits)."""
     parents = synth.tree_from_branching((3, 2, 1), 15)
     toks = synth.gen_tree_tokens(parents, shape.vocab, seed=4)
-    g, o = _pair(shape, w, [], int4=True)
+    g, o = _pair(shape, w, [], int8=aq == 1, int4=aq == 2)
     if ctx:
         for l in range(shape.n_layers):
             k, v = synth.gen_kv(1, shape.n_kv_heads, ctx, shape.head_dim, seed=700 + l)
@@ -144,8 +145,8 @@ def _int4_tree(shape, w, ctx, skip, window):
         o.set_committed(ctx)
     errs = []
     for a, b in ((0, 1), (1, 4), (4, 10), (10, 15)):
-        got = g.forward(toks[a:b], parents[a:b], a, skip=skip, act_quant=2, attn_window=window)
-        ref = o.forward(toks[a:b], parents[a:b], a, skip=skip, act_quant=2, attn_window=window)
+        got = g.forward(toks[a:b], parents[a:b], a, skip=skip, act_quant=aq, attn_window=window)
+        ref = o.forward(toks[a:b], parents[a:b], a, skip=skip, act_quant=aq, attn_window=window)
         errs += list(np.abs(got - ref).max(axis=1) / np.abs(ref).max(axis=1))
     g.close()
     return np.array(errs), toks, parents
@@ -191,6 +192,22 @@ def test_int4_draft_bf16_tree_with_context(weights, name, skip, window):
           f"quantisation noise {noise.min():.3e}..{noise.max():.3e}", flush=True)
     assert exact >= 5, errs
     assert errs.max() < noise.max(), (errs, noise)
+
+
+@pytest.mark.parametrize("name,skip,window", [("gqa_small", None, None), ("mha_small", [1, 0], (4, 64))])
+def test_int8_draft_bf16_tree_with_context(weights, name, skip, window):
+    """W8A8 after 300 committed slots of the same synthetic KV on both sides
+    (the draft path alone, without the drift of independently prefilled
+    caches): rows match the oracle to rounding unless an fp32-against-fp64
+    difference flips a code, which moves a product by 1/127 of the row's
+    range.  At least 12 of the 15 rows must match to 1e-5 (measured: all),
+    and every row within 1e-2."""
+    shape = {"gqa_small": GQA, "mha_small": MHA}[name]
+    errs, _, _ = _int4_tree(shape, weights[name], 300, skip, window, aq=1)
+    exact = int((errs < 1e-5).sum())
+    print(f"[w8a8] {name} skip {skip} window {window}: {exact}/15 rows exact, worst {errs.max():.3e}", flush=True)
+    assert exact >= 12, errs
+    assert errs.max() < 1e-2, errs
 
 
 def test_accept_exact_on_identical_logits(weights):
