@@ -423,6 +423,44 @@ def test_validation_errors_leave_state_unchanged(weights):
     g.close()
 
 
+def test_capacity_boundary_and_empty_call(weights):
+    """A tree that fills the cache to max_ctx exactly is accepted and matches
+    the oracle; an empty call is an argument error that changes nothing."""
+    shape = TINY
+    g = cas.Model(shape, max_ctx=50, max_tree=16)
+    g.load_weights(weights["tiny"])
+    o = O.OracleModel(shape, weights["tiny"], max_ctx=50)
+    prompt = synth.gen_prompt(shape.vocab, 40, seed=15)
+    g.prefill(prompt)
+    o.prefill(list(prompt))
+    with pytest.raises(cas.CasError, match="CAS_ERR_ARG"):
+        g.forward([], [])
+    assert g.committed == 40
+    parents = synth.tree_from_branching((3, 2), 10)
+    toks = synth.gen_tree_tokens(parents, shape.vocab, seed=16)
+    got = g.forward(toks, parents)
+    ref = o.forward(toks, parents)
+    assert _row_err(got, ref) < TOL["f32"]
+    g.close()
+
+
+@pytest.mark.parametrize("name", ["tiny", "gqa_small"])
+def test_star_tree_parity(weights, name):
+    """A root with 127 children: every child's ancestor set is itself and the
+    root, most of them in the second 64-bit word of the mask; the widest tree
+    of one level the library takes."""
+    shape = {"tiny": TINY, "gqa_small": GQA}[name]
+    prompt = synth.gen_prompt(shape.vocab, 70, seed=17)
+    parents = [-1] + [0] * 127
+    toks = synth.gen_tree_tokens(parents, shape.vocab, seed=18)
+    g, o = _pair(shape, weights[name], prompt)
+    got = g.forward(toks, parents)
+    ref = o.forward(toks, parents)
+    err = _row_err(got, ref)
+    assert err < TOL[shape.dtype], err
+    g.close()
+
+
 @pytest.mark.parametrize("name", ["tiny", "mha_small", "gqa_small"])
 def test_root_row_is_bit_identical_for_every_tree_size(weights, name):
     """The verify kernels reduce every row in an order that does not depend on
