@@ -126,6 +126,19 @@ __device__ __forceinline__ i32x4 i4_step(const i32x4 blk, int h) {
                  (int)sext_nib4((w0 >> 4) & 0x0f0f0f0fu), (int)sext_nib4((w1 >> 4) & 0x0f0f0f0fu)};
 }
 
+// A VALU read of an MFMA result needs a number of wait states after the MFMA
+// (8 for the bf16 and int8 16x16 forms, 10 for the fp32 one).  The compiler
+// pads straight-line code, but a drain that branches right after its MFMAs
+// has been compiled with the accumulators read back at the join two
+// instructions later (the last stage's contribution lost for part of a
+// tile).  16 wait states after each conditional MFMA group close every such
+// path; they cost a few cycles per drain stage.
+__device__ __forceinline__ void mfma_result_pad() {
+    __builtin_amdgcn_sched_barrier(0);
+    asm volatile("s_nop 7\n\ts_nop 7");
+    __builtin_amdgcn_sched_barrier(0);
+}
+
 template <int WT>
 __device__ __forceinline__ typename WTr<WT>::acc_t mfma_step(i32x4 a, i32x4 b, typename WTr<WT>::acc_t c) {
     if constexpr (WT == ET_BF16) {
@@ -350,12 +363,16 @@ __global__ void __launch_bounds__(64 * WAVES) k_gemm(const GemmArgs a) {
         for (int s = 0; s < D; ++s) {
             if (c + s < S1) {
                 CAS_GEMM_MMA(s);
+                mfma_result_pad();
                 if (c + s + D < S1) CAS_GEMM_LOAD(s, c + s + D);
             }
         }
 #pragma unroll
         for (int s = 0; s < D; ++s)
-            if (c + D + s < S1) CAS_GEMM_MMA(s);
+            if (c + D + s < S1) {
+                CAS_GEMM_MMA(s);
+                mfma_result_pad();
+            }
     }
 #undef CAS_GEMM_MMA
 #undef CAS_GEMM_LOAD
@@ -470,12 +487,16 @@ __global__ void __launch_bounds__(64 * WAVES) k_gemm_wide(const GemmArgs a) {
     for (int s = 0; s < D; ++s) {
         if (c + s < NS) {
             CAS_W_STAGE(s, s & 1);
+            mfma_result_pad();
             if (c + s + D < NS) CAS_W_LOAD(s, c + s + D);
         }
     }
 #pragma unroll
     for (int s = 0; s < D; ++s)
-        if (c + D + s < NS) CAS_W_STAGE(s, s & 1);
+        if (c + D + s < NS) {
+            CAS_W_STAGE(s, s & 1);
+            mfma_result_pad();
+        }
 #undef CAS_W_STAGE
 #undef CAS_W_LOAD
     if (gridDim.y == 1) {
