@@ -488,6 +488,31 @@ def test_root_row_is_bit_identical_for_every_tree_size(weights, name):
     g.close()
 
 
+@pytest.mark.parametrize("name,aq", [("mha_small", 1), ("mha_small", 2), ("gqa_small", 2)])
+def test_quantised_draft_root_row_is_bit_identical_for_every_tree_size(weights, name, aq):
+    """The same property for the W8A8 (aq 1) and W4A4 (aq 2) drafts with the
+    odd layers skipped: a row's codes and scale depend on that row only, and
+    the integer GEMMs sum each column in the same order whether the call's
+    activation rows stay resident in LDS (int4 weights, up to 16 rows) or
+    stream through the stage ring (every other call), so the root's logits
+    are the same bits for T = 1, 7, 33 and 70."""
+    shape = {"gqa_small": GQA, "mha_small": MHA}[name]
+    g = cas.Model(shape, max_ctx=512)
+    g.load_weights(weights[name])
+    g.build_int8() if aq == 1 else g.build_int4()
+    prompt = [int(x) for x in synth.gen_prompt(shape.vocab, 50, seed=6)]
+    g.prefill(prompt[:-1])
+    skip = [l % 2 for l in range(shape.n_layers)]
+    rows = []
+    for T in (1, 7, 33, 70):
+        parents = synth.balanced_tree(T)
+        toks = synth.gen_tree_tokens(parents, shape.vocab, seed=T, root_token=prompt[-1])
+        rows.append(g.forward(toks, parents, 0, skip=skip, act_quant=aq)[0].copy())
+    for r in rows[1:]:
+        assert np.array_equal(r.view(np.uint32), rows[0].view(np.uint32))
+    g.close()
+
+
 @pytest.mark.parametrize("name,sink,win,tol", [("tiny", 4, 16, 1e-4), ("mha_small", 4, 64, 2e-2),
                                                ("gqa_small", 0, 40, 2e-2), ("mha_small", 40, 33, 2e-2)])
 def test_attention_window_draft_parity(weights, name, sink, win, tol):
