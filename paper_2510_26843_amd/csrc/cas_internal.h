@@ -118,6 +118,11 @@ struct GemmArgs {
     // to out + k * part_stride, [T][ldo]
     int ksplit;
     size_t part_stride;
+    // quantise on load (int8 / int4 weights, calls of at most QX_MAX_T rows;
+    // gemm_qx_ok says which): X holds bf16 tiled rows of width xk (pad
+    // columns zero), and each workgroup derives every row's scale amax / qx
+    // and the codes of its own K range itself (xs unused).  0: X holds codes.
+    int qx, xk;
 };
 
 // wtype: element type of W and X; atype: activation type written by the
@@ -128,8 +133,11 @@ hipError_t launch_gemm(int wtype, int atype, int epi, const GemmArgs& a, hipStre
 // workgroups already, int8 weights, or too few stages).
 int gemm_parts_count(int wtype, int N, int Kp, int T);
 // The split-K form: a.ksplit splits, each writing fp32 sums of its K range to
-// a.out + k * a.part_stride ([T][a.ldo]); bf16 / fp32 weights only.
+// a.out + k * a.part_stride ([T][a.ldo]).
 hipError_t launch_gemm_parts(int wtype, const GemmArgs& a, hipStream_t s);
+// Whether a split-K GEMM of N rows (padded width Kp, T rows of activations,
+// ksplit splits) can quantise its bf16 input on load (launch_gemm cannot).
+bool gemm_qx_ok(int wtype, int N, int Kp, int T, int ksplit);
 
 struct AttnArgs {
     const void* q;        // [T][H][hd]

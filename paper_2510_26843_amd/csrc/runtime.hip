@@ -291,6 +291,14 @@ hipError_t enqueue_forward(cas_ctx* c, int T, const uint8_t* skip, int aq) {
     const int qmax = aq == 2 ? 7 : 127;
     auto wcopy = [&](const LayerW& w, int i) -> const void* { return aq == 2 ? (const void*)w.q4[i] : (const void*)w.q8[i]; };
     auto scopy = [&](const LayerW& w, int i) -> const float* { return aq == 2 ? w.s4[i] : w.s8[i]; };
+    // one-node quantised drafts on bf16 models: the O and down projections
+    // quantise their bf16 input on load when they can (no codes from the
+    // attention merge, no separate quantiser of the SwiGLU output); the QKV
+    // and gate/up inputs keep the codes their RMSNorm writes
+    const bool qxs = aq && et == ET_BF16;
+    const int ks_o = gemm_parts_count(wq, d, c->kq_q, T), ks_d = gemm_parts_count(wq, d, c->kq_f, T);
+    const bool qx_o = qxs && gemm_qx_ok(wq, d, c->kq_q, T, ks_o);
+    const bool qx_d = qxs && gemm_qx_ok(wq, d, c->kq_f, T, ks_d);
     // split-K sums of the last O / down projection that the next RMSNorm
     // adds to the residual stream (0: the projection updated it itself)
     int pend = 0;
@@ -343,19 +351,23 @@ hipError_t enqueue_forward(cas_ctx* c, int T, const uint8_t* skip, int aq) {
         at.kc = kc;
         at.vt = vt;
         // quantised drafts on bf16 models: the attention's merge writes the
-        // O projection's input codes itself
-        const bool fused_q = aq && et == ET_BF16;
+        // O projection's input codes itself, unless that projection quantises
+        // on load
+        const bool fused_q = aq && et == ET_BF16 && !qx_o;
         at.qout = fused_q ? c->d_xq : nullptr;
         at.qscale = fused_q ? c->d_xs : nullptr;
         at.qmax = qmax;
         RUN(CAS_K_ATTN, launch_attention(et, at, s));
-        if (aq && !fused_q) RUN(CAS_K_QUANT, launch_quant_rows(et, c->d_ao, T, H * hd, c->d_xq, c->d_xs, 1, qmax, s));
+        if (aq && !fused_q && !qx_o)
+            RUN(CAS_K_QUANT, launch_quant_rows(et, c->d_ao, T, H * hd, c->d_xq, c->d_xs, 1, qmax, s));
         GemmArgs go{};
         go.T = T;
         go.N = d;
         go.Kp = aq ? c->kq_q : c->kp_q;
         go.W = aq ? wcopy(w, 1) : w.wo;
-        go.X = aq ? (const void*)c->d_xq : c->d_ao;
+        go.X = aq && !qx_o ? (const void*)c->d_xq : c->d_ao;
+        go.qx = qx_o ? qmax : 0;
+        go.xk = H * hd;
         go.xs = c->d_xs;
         go.ws = scopy(w, 1);
         go.out = c->d_h;
@@ -375,13 +387,15 @@ hipError_t enqueue_forward(cas_ctx* c, int T, const uint8_t* skip, int aq) {
         gu.ldo = ffn;
         gu.out_k = ffn;
         RUN(CAS_K_GEMM_GATEUP, launch_gemm(wq, et, EPI_SWIGLU, gu, s));
-        if (aq) RUN(CAS_K_QUANT, launch_quant_rows(et, c->d_sw, T, ffn, c->d_xq, c->d_xs, 1, qmax, s));
+        if (aq && !qx_d) RUN(CAS_K_QUANT, launch_quant_rows(et, c->d_sw, T, ffn, c->d_xq, c->d_xs, 1, qmax, s));
         GemmArgs gd{};
         gd.T = T;
         gd.N = d;
         gd.Kp = aq ? c->kq_f : c->kp_f;
         gd.W = aq ? wcopy(w, 3) : w.wd;
-        gd.X = aq ? (const void*)c->d_xq : c->d_sw;
+        gd.X = aq && !qx_d ? (const void*)c->d_xq : c->d_sw;
+        gd.qx = qx_d ? qmax : 0;
+        gd.xk = ffn;
         gd.xs = c->d_xs;
         gd.ws = scopy(w, 3);
         gd.out = c->d_h;
