@@ -117,6 +117,44 @@ __device__ __forceinline__ float amax_bf8(const i32x4 v) {
     return m;
 }
 
+// The attention output of one query row of one head at 4 consecutive d: the
+// KV splits' partial states merged in split order with a running max
+// (online softmax), eight splits' (m, l) pairs and partial outputs loaded at
+// a time (one round of loads for contexts up to 2048 slots), then
+// normalised.  row = head * T + t.
+__device__ __forceinline__ f32x4 attn_merge_row_hd(const AttnArgs& a, int S, size_t row, int d4, int HD) {
+#pragma clang fp contract(off)
+    const size_t sstride = (size_t)a.H * a.T;  // rows between splits
+    float M = -1e30f, L = 0.f;
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+    for (int s0 = 0; s0 < S; s0 += 8) {
+        float2 ml[8];
+        f32x4 po[8];
+#pragma unroll
+        for (int k = 0; k < 8; ++k) {
+            const size_t r = row + (size_t)min(s0 + k, S - 1) * sstride;
+            ml[k] = *(const float2*)(a.part_ml + r * 2);
+            po[k] = *(const f32x4*)(a.part_o + r * HD + d4);
+        }
+#pragma unroll
+        for (int k = 0; k < 8; ++k) {
+            if (s0 + k < S) {
+                const float mn = fmaxf(M, ml[k].x);
+                const float fo = exp2f(M - mn), fn = exp2f(ml[k].x - mn);
+                acc = acc * fo + po[k] * fn;
+                L = L * fo + ml[k].y * fn;
+                M = mn;
+            }
+        }
+    }
+    const float inv = L > 0.f ? 1.f / L : 0.f;
+    return acc * inv;
+}
+template <int HD>
+__device__ __forceinline__ f32x4 attn_merge_row(const AttnArgs& a, int S, size_t row, int d4) {
+    return attn_merge_row_hd(a, S, row, d4, HD);
+}
+
 // ---------------------------------------------------------------- GEMM
 
 template <int WT> struct WTr;
@@ -438,13 +476,19 @@ static constexpr int RX_PIECES = 6;  // 16-byte activation pieces per thread (RX
 // W4A4 1.75 -> 1.63 ms; at four rows the same use was 2% slower, and the
 // QKV and gate/up inputs, whose norm already writes codes, were slower too).
 static constexpr int QX_MAX_T = 1;
-template <int WT, int NT, int UC, int D, int WAVES, int TPW, int EPI, typename AT, bool RX, bool QX = false>
+// MX (with RX, bf16 weights, one row): the input row is merged on load from
+// the attention's split partials by the same routine, with the same bf16
+// rounding, as the merge kernel; each workgroup merges only its K range (the
+// heads it covers), and the merge kernel is not launched.
+template <int WT, int NT, int UC, int D, int WAVES, int TPW, int EPI, typename AT, bool RX, bool QX = false,
+          bool MX = false>
 __global__ void __launch_bounds__(64 * WAVES) k_gemm_wide(const GemmArgs a) {
     using Tr = WTr<WT>;
     using ACC = typename Tr::acc_t;
     constexpr int E = Tr::E;
     static_assert(!RX || NT == 1, "resident activations feed one column tile");
     static_assert(!QX || (RX && is_int<WT>()), "quantise-on-load feeds resident integer codes");
+    static_assert(!MX || (RX && WT == ET_BF16), "merge-on-load feeds a resident bf16 row");
     __shared__ float qsc[QX ? QX_MAX_T : 1], qred[QX ? WAVES : 1];
     constexpr int NB = NT * UC;  // 1 KB activation blocks per stage
     constexpr int LPT = (NB + WAVES - 1) / WAVES;  // 1 KB blocks per wave per stage
@@ -570,6 +614,22 @@ __global__ void __launch_bounds__(64 * WAVES) k_gemm_wide(const GemmArgs a) {
             *(i32x4*)(xr + (size_t)t * RS + k) = q;
         }
         __syncthreads();
+    } else if constexpr (MX) {
+        // one row: element k0 + k of the K range at xr + 2k (bf16)
+        AttnArgs m{};
+        m.H = a.H;
+        m.T = 1;
+        m.part_o = (float*)a.mx_o;
+        m.part_ml = (float*)a.mx_ml;
+        const int k0 = c0 * 16 * E, kin = a.H * a.hd;
+        for (int i = threadIdx.x; i < KR / 4; i += 64 * WAVES) {
+            const int k = k0 + 4 * i;
+            f32x4 v = {0.f, 0.f, 0.f, 0.f};
+            if (k < kin) v = attn_merge_row_hd(m, a.mx_S, (size_t)(k / a.hd), k % a.hd, a.hd);
+            *(uint2*)(xr + (size_t)8 * i) = make_uint2((uint32_t)f2bf(v[0]) | ((uint32_t)f2bf(v[1]) << 16),
+                                                       (uint32_t)f2bf(v[2]) | ((uint32_t)f2bf(v[3]) << 16));
+        }
+        __syncthreads();
     } else if constexpr (RX) {
         // after the first weight loads are in flight: all pieces' loads issue
         // back to back (at most RX_PIECES per thread), then the LDS stores
@@ -659,6 +719,10 @@ static int rx_lds_bytes(int wtype, int T, int Kp, int ksplit) {
     const int kr = (C + ksplit - 1) / ksplit * kc;  // elements of the longest K range
     return T * (kr * (int)frag_elem_bytes(wtype) + 16);
 }
+bool gemm_mx_ok(int wtype, int N, int Kp, int T, int ksplit) {
+    if (wtype != ET_BF16 || T != 1 || N % 64 || Kp % chunk_k(wtype)) return false;
+    return ksplit >= 2 && rx_lds_bytes(wtype, T, Kp, ksplit) <= 65536;
+}
 bool gemm_qx_ok(int wtype, int N, int Kp, int T, int ksplit) {
     if ((wtype != ET_I8 && wtype != ET_I4) || T < 1 || T > QX_MAX_T || N % 64 || Kp % chunk_k(wtype)) return false;
     return ksplit >= 2 && rx_lds_bytes(wtype, T, Kp, ksplit) <= 65536;
@@ -671,7 +735,7 @@ static bool rx_use(int wtype, const GemmArgs& a, int ksplit) {
 
 template <int WT, int NT, int EPI, typename AT>
 static hipError_t gemm_go(const GemmArgs& a, hipStream_t s) {
-    if (a.qx) return hipErrorInvalidValue;  // quantise-on-load: the split-K form only
+    if (a.qx || a.mx_o) return hipErrorInvalidValue;  // quantise / merge on load: the split-K form only
     constexpr int UC = stage_uc<WT, NT == 2 ? 4 : (NT == 4 ? 2 : 1)>();
     if (a.N >= 8192 && ((a.N / 16) % 4 == 0 || (a.N / 16) % 3 == 0)) {
         using S1 = WideStageW<WT, NT, 1>;
@@ -799,6 +863,14 @@ int gemm_parts_count(int wtype, int N, int Kp, int T) {
 template <int WT, typename AT>
 static hipError_t gemm_parts_go(const GemmArgs& a, hipStream_t s) {
     const dim3 grid(a.N / 64, a.ksplit);
+    if (a.mx_o) {
+        if constexpr (WT == ET_BF16) {
+            hipLaunchKernelGGL((k_gemm_wide<WT, 1, 4, 2, 4, 1, EPI_STORE, AT, true, false, true>), grid, dim3(256),
+                               (unsigned)rx_lds_bytes(WT, a.T, a.Kp, a.ksplit), s, a);
+            return hipGetLastError();
+        }
+        return hipErrorInvalidValue;
+    }
     if (a.qx) {
         if constexpr (is_int<WT>()) {
             hipLaunchKernelGGL((k_gemm_wide<WT, 1, 4, 2, 4, 1, EPI_STORE, AT, true, true>), grid, dim3(256),
@@ -1374,40 +1446,6 @@ __global__ void __launch_bounds__(64 * QT, 2) k_attn_rows(const AttnArgs a, floa
     }
 }
 
-// The attention output of one query row of one head at 4 consecutive d: the
-// KV splits' partial states merged in split order with a running max
-// (online softmax), eight splits' (m, l) pairs and partial outputs loaded at
-// a time (one round of loads for contexts up to 2048 slots), then
-// normalised.  row = head * T + t.
-template <int HD>
-__device__ __forceinline__ f32x4 attn_merge_row(const AttnArgs& a, int S, size_t row, int d4) {
-#pragma clang fp contract(off)
-    const size_t sstride = (size_t)a.H * a.T;  // rows between splits
-    float M = -1e30f, L = 0.f;
-    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-    for (int s0 = 0; s0 < S; s0 += 8) {
-        float2 ml[8];
-        f32x4 po[8];
-#pragma unroll
-        for (int k = 0; k < 8; ++k) {
-            const size_t r = row + (size_t)min(s0 + k, S - 1) * sstride;
-            ml[k] = *(const float2*)(a.part_ml + r * 2);
-            po[k] = *(const f32x4*)(a.part_o + r * HD + d4);
-        }
-#pragma unroll
-        for (int k = 0; k < 8; ++k) {
-            if (s0 + k < S) {
-                const float mn = fmaxf(M, ml[k].x);
-                const float fo = exp2f(M - mn), fn = exp2f(ml[k].x - mn);
-                acc = acc * fo + po[k] * fn;
-                L = L * fo + ml[k].y * fn;
-                M = mn;
-            }
-        }
-    }
-    const float inv = L > 0.f ? 1.f / L : 0.f;
-    return acc * inv;
-}
 
 // Merge the KV splits of R query rows of one head; each thread owns one
 // (row, 4 d) item.
@@ -1547,11 +1585,13 @@ hipError_t launch_attention(int atype, const AttnArgs& a, hipStream_t s) {
     const int K = a.H * a.hd, kpq = (K + 255) / 256 * 256;
     const int ni = (kpq / 4 + MQ_THREADS - 1) / MQ_THREADS;
     if (a.qout && (ni > 4 || (a.qmax != 127 && a.qmax != 7))) return hipErrorInvalidValue;
+    if (a.no_merge && a.qout) return hipErrorInvalidValue;
     if (a.hd == 128) {
         if (rows) hipLaunchKernelGGL((k_attn_rows<128, 4>), dim3(S, a.Hkv, (nct + 3) / 4), dim3(256), 0, s, a, scale_log2);
         else if (JT == 2) hipLaunchKernelGGL((k_attn_bf16<128, 2>), dim3(S, a.Hkv, nrc), dim3(256), 0, s, a, scale_log2);
         else hipLaunchKernelGGL((k_attn_bf16<128, 1>), dim3(S, a.Hkv, nrc), dim3(256), 0, s, a, scale_log2);
-        if (!a.qout) hipLaunchKernelGGL((k_attn_merge<128, 4>), mg, dim3(128), 0, s, a, S);
+        if (a.no_merge) {
+        } else if (!a.qout) hipLaunchKernelGGL((k_attn_merge<128, 4>), mg, dim3(128), 0, s, a, S);
         else if (ni <= 1) hipLaunchKernelGGL((k_attn_merge_q<128, 1>), dim3(a.T), dim3(MQ_THREADS), 0, s, a, S);
         else if (ni <= 2) hipLaunchKernelGGL((k_attn_merge_q<128, 2>), dim3(a.T), dim3(MQ_THREADS), 0, s, a, S);
         else hipLaunchKernelGGL((k_attn_merge_q<128, 4>), dim3(a.T), dim3(MQ_THREADS), 0, s, a, S);
@@ -1559,7 +1599,8 @@ hipError_t launch_attention(int atype, const AttnArgs& a, hipStream_t s) {
         if (rows) hipLaunchKernelGGL((k_attn_rows<64, 4>), dim3(S, a.Hkv, (nct + 3) / 4), dim3(256), 0, s, a, scale_log2);
         else if (JT == 2) hipLaunchKernelGGL((k_attn_bf16<64, 2>), dim3(S, a.Hkv, nrc), dim3(256), 0, s, a, scale_log2);
         else hipLaunchKernelGGL((k_attn_bf16<64, 1>), dim3(S, a.Hkv, nrc), dim3(256), 0, s, a, scale_log2);
-        if (!a.qout) hipLaunchKernelGGL((k_attn_merge<64, 4>), mg, dim3(64), 0, s, a, S);
+        if (a.no_merge) {
+        } else if (!a.qout) hipLaunchKernelGGL((k_attn_merge<64, 4>), mg, dim3(64), 0, s, a, S);
         else if (ni <= 1) hipLaunchKernelGGL((k_attn_merge_q<64, 1>), dim3(a.T), dim3(MQ_THREADS), 0, s, a, S);
         else if (ni <= 2) hipLaunchKernelGGL((k_attn_merge_q<64, 2>), dim3(a.T), dim3(MQ_THREADS), 0, s, a, S);
         else hipLaunchKernelGGL((k_attn_merge_q<64, 4>), dim3(a.T), dim3(MQ_THREADS), 0, s, a, S);

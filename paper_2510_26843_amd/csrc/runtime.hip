@@ -299,6 +299,9 @@ hipError_t enqueue_forward(cas_ctx* c, int T, const uint8_t* skip, int aq) {
     const int ks_o = gemm_parts_count(wq, d, c->kq_q, T), ks_d = gemm_parts_count(wq, d, c->kq_f, T);
     const bool qx_o = qxs && gemm_qx_ok(wq, d, c->kq_q, T, ks_o);
     const bool qx_d = qxs && gemm_qx_ok(wq, d, c->kq_f, T, ks_d);
+    // one-row bf16 forwards: the O projection merges the attention's split
+    // partials itself (no merge launch)
+    const bool mx_o = !aq && et == ET_BF16 && gemm_mx_ok(et, d, c->kp_q, T, gemm_parts_count(et, d, c->kp_q, T));
     // split-K sums of the last O / down projection that the next RMSNorm
     // adds to the residual stream (0: the projection updated it itself)
     int pend = 0;
@@ -357,6 +360,7 @@ hipError_t enqueue_forward(cas_ctx* c, int T, const uint8_t* skip, int aq) {
         at.qout = fused_q ? c->d_xq : nullptr;
         at.qscale = fused_q ? c->d_xs : nullptr;
         at.qmax = qmax;
+        at.no_merge = mx_o ? 1 : 0;
         RUN(CAS_K_ATTN, launch_attention(et, at, s));
         if (aq && !fused_q && !qx_o)
             RUN(CAS_K_QUANT, launch_quant_rows(et, c->d_ao, T, H * hd, c->d_xq, c->d_xs, 1, qmax, s));
@@ -368,6 +372,11 @@ hipError_t enqueue_forward(cas_ctx* c, int T, const uint8_t* skip, int aq) {
         go.X = aq && !qx_o ? (const void*)c->d_xq : c->d_ao;
         go.qx = qx_o ? qmax : 0;
         go.xk = H * hd;
+        go.mx_o = mx_o ? at.part_o : nullptr;
+        go.mx_ml = at.part_ml;
+        go.mx_S = S;
+        go.H = H;
+        go.hd = hd;
         go.xs = c->d_xs;
         go.ws = scopy(w, 1);
         go.out = c->d_h;
