@@ -539,6 +539,27 @@ def test_attention_window_draft_parity(weights, name, sink, win, tol):
     g.close()
 
 
+@pytest.mark.parametrize("name,sink,win", [("mha_small", 4, 64), ("gqa_small", 0, 40), ("mha_small", 0, 0)])
+def test_one_node_call_merges_attention_in_the_o_projection(weights, name, sink, win):
+    """A one-row bf16 call launches no attention merge: each workgroup of the
+    split-K O projection merges the partials of its heads itself.  Its root
+    row equals, bit for bit, the root row of a two-node call (which launches
+    the merge kernel), with layer skip and sink + window attention as well
+    as at full depth (win 0), and the oracle's to the bf16 tolerance."""
+    shape = {"gqa_small": GQA, "mha_small": MHA}[name]
+    prompt = [int(x) for x in synth.gen_prompt(shape.vocab, 300, seed=31)]
+    g, o = _pair(shape, weights[name], prompt[:-1], max_ctx=512)
+    skip = [l % 2 for l in range(shape.n_layers)] if name == "gqa_small" else None
+    window = (sink, win) if win else None
+    root, child = prompt[-1], (prompt[-1] + 7) % shape.vocab
+    one = g.forward([root], [-1], 0, skip=skip, attn_window=window)
+    two = g.forward([root, child], [-1, 0], 0, skip=skip, attn_window=window)
+    assert np.array_equal(one[0].view(np.uint32), two[0].view(np.uint32))
+    ref = o.forward([root], [-1], 0, skip=skip, attn_window=window)
+    assert _row_err(one, ref) < 2e-2
+    g.close()
+
+
 def test_attention_window_covering_the_prefix_is_exact(weights):
     shape = MHA
     prompt = [int(x) for x in synth.gen_prompt(shape.vocab, 200, seed=23)]
