@@ -1566,10 +1566,10 @@ hipError_t launch_attention(int atype, const AttnArgs& a, hipStream_t s) {
     // the merge: 4 query rows per workgroup, i.e. many small workgroups
     // (7B layer: attention + merge 12.1 us against 14.2 with 16 rows)
     const dim3 mg((a.T + 3) / 4, a.H);
-    // Four or more query tiles per kv head, each head with at least 32 rows:
+    // Several query tiles per kv head, each head with at least 32 rows:
     // four tiles per workgroup share one pass of the split's K/V through LDS
-    // (k_attn_rows; per layer, 8B 64 nodes at 4096: 27.7 -> 23.3 us, 13B 64
-    // nodes at 2048: 22.7 -> 19.3 us, 7B 128 nodes at 8192: 112 -> 65 us).
+    // (k_attn_rows; per layer, 8B 64 nodes at 4096: 27.7 -> 23.3 us, 7B 128
+    // nodes at 8192: 112 -> 65 us).
     // A single-token call of a grouped-query model has four tiles of one row
     // each and keeps the larger grid of k_attn_bf16 (8B one node at 4096:
     // 3.80 ms per forward against 3.91 with k_attn_rows).  Both kernels give
@@ -1578,7 +1578,12 @@ hipError_t launch_attention(int atype, const AttnArgs& a, hipStream_t s) {
     // workgroup unless the grid of (split, kv head, tile) units is large; then
     // two tiles share each K/V load (7B 32 nodes at 8192: fewer, longer
     // workgroups halve the per-CU key traffic).
-    const bool rows = nct >= 4 && Tp >= 32;
+    // With three or four tiles per kv head the shared pass pays only when the
+    // per-tile grid is large (7B 48 nodes at 8192: 5.22 -> 4.94 ms, 13B 64
+    // nodes at 4096: 7.13 -> 6.97 ms); below about 2048 tile workgroups the
+    // larger grid wins (13B 64 nodes at 2048: 6.51 ms with k_attn_rows, 6.46
+    // without; 7B 64 nodes at 1024: 4.03 and 3.94 ms).
+    const bool rows = (nct >= 5 || (nct >= 3 && (long)S * a.Hkv * nct >= 2048)) && Tp >= 32;
     const int JT = (G == 1 && S * a.Hkv * nct >= 1024) ? 2 : 1;
     const int nrc = (nct + JT - 1) / JT;
     // quantised output: one merge-and-quantise workgroup per row
