@@ -123,10 +123,11 @@ struct GemmArgs {
     // columns zero), and each workgroup derives every row's scale amax / qx
     // and the codes of its own K range itself (xs unused).  0: X holds codes.
     int qx, xk;
-    // merge on load (bf16 O projection of a one-row call; gemm_mx_ok says
-    // when): the input row is the attention's mx_S split partials
-    // ([split][H][1][hd] sums, [split][H][1][2] max and sum, H heads of hd),
-    // merged by each workgroup for its own K range (X unused).  nullptr: off.
+    // merge on load (bf16 O projection of a call of one or two rows;
+    // gemm_mx_ok says when): the input rows are the attention's mx_S split
+    // partials ([split][H][T][hd] sums, [split][H][T][2] max and sum, H heads
+    // of hd), merged by each workgroup for its own K range (X unused).
+    // nullptr: off.
     const float* mx_o;
     const float* mx_ml;
     int mx_S;
@@ -145,7 +146,7 @@ hipError_t launch_gemm_parts(int wtype, const GemmArgs& a, hipStream_t s);
 // Whether a split-K GEMM of N rows (padded width Kp, T rows of activations,
 // ksplit splits) can quantise its bf16 input on load (launch_gemm cannot).
 bool gemm_qx_ok(int wtype, int N, int Kp, int T, int ksplit);
-// Whether a split-K GEMM can merge its one input row from attention partials.
+// Whether a split-K GEMM can merge its input rows from attention partials.
 bool gemm_mx_ok(int wtype, int N, int Kp, int T, int ksplit);
 
 struct AttnArgs {

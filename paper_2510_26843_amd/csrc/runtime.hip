@@ -299,8 +299,8 @@ hipError_t enqueue_forward(cas_ctx* c, int T, const uint8_t* skip, int aq) {
     const int ks_o = gemm_parts_count(wq, d, c->kq_q, T), ks_d = gemm_parts_count(wq, d, c->kq_f, T);
     const bool qx_o = qxs && gemm_qx_ok(wq, d, c->kq_q, T, ks_o);
     const bool qx_d = qxs && gemm_qx_ok(wq, d, c->kq_f, T, ks_d);
-    // one-row bf16 forwards: the O projection merges the attention's split
-    // partials itself (no merge launch)
+    // bf16 forwards of one or two rows: the O projection merges the
+    // attention's split partials itself (no merge launch)
     const bool mx_o = !aq && et == ET_BF16 && gemm_mx_ok(et, d, c->kp_q, T, gemm_parts_count(et, d, c->kp_q, T));
     // split-K sums of the last O / down projection that the next RMSNorm
     // adds to the residual stream (0: the projection updated it itself)

@@ -541,20 +541,23 @@ def test_attention_window_draft_parity(weights, name, sink, win, tol):
 
 @pytest.mark.parametrize("name,sink,win", [("mha_small", 4, 64), ("gqa_small", 0, 40), ("mha_small", 0, 0)])
 def test_one_node_call_merges_attention_in_the_o_projection(weights, name, sink, win):
-    """A one-row bf16 call launches no attention merge: each workgroup of the
-    split-K O projection merges the partials of its heads itself.  Its root
-    row equals, bit for bit, the root row of a two-node call (which launches
-    the merge kernel), with layer skip and sink + window attention as well
-    as at full depth (win 0), and the oracle's to the bf16 tolerance."""
+    """bf16 calls of one or two rows launch no attention merge: each
+    workgroup of the split-K O projection merges the partials of its heads
+    itself.  The root rows of one- and two-node calls equal, bit for bit, the
+    root row of a three-node call (which launches the merge kernel), with
+    layer skip and sink + window attention as well as at full depth (win 0),
+    and the oracle's to the bf16 tolerance."""
     shape = {"gqa_small": GQA, "mha_small": MHA}[name]
     prompt = [int(x) for x in synth.gen_prompt(shape.vocab, 300, seed=31)]
     g, o = _pair(shape, weights[name], prompt[:-1], max_ctx=512)
     skip = [l % 2 for l in range(shape.n_layers)] if name == "gqa_small" else None
     window = (sink, win) if win else None
-    root, child = prompt[-1], (prompt[-1] + 7) % shape.vocab
+    root, c1, c2 = prompt[-1], (prompt[-1] + 7) % shape.vocab, (prompt[-1] + 11) % shape.vocab
     one = g.forward([root], [-1], 0, skip=skip, attn_window=window)
-    two = g.forward([root, child], [-1, 0], 0, skip=skip, attn_window=window)
-    assert np.array_equal(one[0].view(np.uint32), two[0].view(np.uint32))
+    two = g.forward([root, c1], [-1, 0], 0, skip=skip, attn_window=window)
+    three = g.forward([root, c1, c2], [-1, 0, 0], 0, skip=skip, attn_window=window)
+    assert np.array_equal(one[0].view(np.uint32), three[0].view(np.uint32))
+    assert np.array_equal(two[:2].view(np.uint32), three[:2].view(np.uint32))
     ref = o.forward([root], [-1], 0, skip=skip, attn_window=window)
     assert _row_err(one, ref) < 2e-2
     g.close()
