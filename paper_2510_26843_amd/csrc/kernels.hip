@@ -2036,6 +2036,14 @@ hipError_t launch_untile_weight_i4(const uint8_t* src, int N, int K, int8_t* dst
 
 // ---------------------------------------------------------------- embedding + tree metadata
 
+// Element e of a 16-byte piece of activations (bf16 bits or fp32), as fp32.
+template <typename AT> __device__ __forceinline__ float piece_val(const i32x4 v, int e);
+template <> __device__ __forceinline__ float piece_val<uint16_t>(const i32x4 v, int e) {
+    const uint32_t w = (uint32_t)v[e >> 1];
+    return __uint_as_float((e & 1) ? (w & 0xffff0000u) : (w << 16));
+}
+template <> __device__ __forceinline__ float piece_val<float>(const i32x4 v, int e) { return __int_as_float(v[e]); }
+
 template <typename AT>
 __global__ void __launch_bounds__(256) k_embed(const AT* E, int d, const int* rtok, const int* rpar,
                                                const StepParams* sp, float* h, int* row_pos, int* row_slot,
@@ -2045,7 +2053,26 @@ __global__ void __launch_bounds__(256) k_embed(const AT* E, int d, const int* rt
     const int node = sp->node_offset + t, Lc = sp->Lc, n_tree = sp->n_tree;
     if (threadIdx.x < n_tree) par[threadIdx.x] = rpar[threadIdx.x];
     const int tok = rtok[node];
-    for (int k = threadIdx.x; k < d; k += 256) h[(size_t)t * d + k] = Act<AT>::ld(E, (size_t)tok * d + k);
+    // the row in 16-byte pieces (d is a multiple of 16), all loads first
+    constexpr int EV = 16 / sizeof(AT), MAXP = 4;  // elements per piece; pieces per thread up to d = 8192
+    const AT* er = E + (size_t)tok * d;
+    float* hr = h + (size_t)t * d;
+    i32x4 pc[MAXP];
+#pragma unroll
+    for (int i = 0; i < MAXP; ++i) {
+        const int k = (threadIdx.x + 256 * i) * EV;
+        if (k < d) pc[i] = *(const i32x4*)(er + k);
+    }
+#pragma unroll
+    for (int i = 0; i < MAXP; ++i) {
+        const int k = (threadIdx.x + 256 * i) * EV;
+        if (k >= d) continue;
+#pragma unroll
+        for (int e = 0; e < EV; e += 4)
+            *(float4*)(hr + k + e) = make_float4(piece_val<AT>(pc[i], e), piece_val<AT>(pc[i], e + 1),
+                                                 piece_val<AT>(pc[i], e + 2), piece_val<AT>(pc[i], e + 3));
+    }
+    for (int k = 256 * MAXP * EV + threadIdx.x; k < d; k += 256) hr[k] = Act<AT>::ld(er, k);  // wider rows
     __syncthreads();
     if (threadIdx.x == 0) {
         int depth = 0;
