@@ -476,12 +476,16 @@ static constexpr int RX_PIECES = 6;  // 16-byte activation pieces per thread (RX
 // W4A4 1.75 -> 1.63 ms; at four rows the same use was 2% slower, and the
 // QKV and gate/up inputs, whose norm already writes codes, were slower too).
 static constexpr int QX_MAX_T = 1;
-// MX (with RX, bf16 weights, at most MX_MAX_T rows): the input rows are
-// merged on load from the attention's split partials by the same routine,
-// with the same bf16 rounding, as the merge kernel; each workgroup merges
-// only its K range (the heads it covers), and the merge kernel is not
-// launched.  7B 16-layer draft: one node 1.55 -> 1.52 ms, two nodes 1.55 ->
-// 1.53 ms; at four rows the merged reads cost more than the launch saves.
+// MX (with RX, bf16 weights, at most one merge item of 4 elements per
+// thread): the input rows are merged on load from the attention's split
+// partials by the same routine, with the same bf16 rounding, as the merge
+// kernel; each workgroup merges only its K range (the heads it covers), and
+// the merge kernel is not launched.  Measured one-row verify: 7B 3.10 ->
+// 3.02 ms (ctx 1024) and 3.91 -> 3.84 ms (8192), 8B 3.49 -> 3.42 and 3.76 ->
+// 3.67 ms (1024, 4096).  With two items per thread (two rows of 7B, or the
+// 13B K ranges of 14 heads) the serial merges cost more than the launch at
+// longer contexts (7B two rows at 8192: 3.90 -> 4.01 ms; 13B one row at 4096:
+// 5.65 -> 5.70 ms).
 static constexpr int MX_MAX_T = 2;
 template <int WT, int NT, int UC, int D, int WAVES, int TPW, int EPI, typename AT, bool RX, bool QX = false,
           bool MX = false>
@@ -724,8 +728,10 @@ static int rx_lds_bytes(int wtype, int T, int Kp, int ksplit) {
     return T * (kr * (int)frag_elem_bytes(wtype) + 16);
 }
 bool gemm_mx_ok(int wtype, int N, int Kp, int T, int ksplit) {
-    if (wtype != ET_BF16 || T < 1 || T > MX_MAX_T || N % 64 || Kp % chunk_k(wtype)) return false;
-    return ksplit >= 2 && rx_lds_bytes(wtype, T, Kp, ksplit) <= 65536;
+    if (wtype != ET_BF16 || T < 1 || T > MX_MAX_T || N % 64 || Kp % chunk_k(wtype) || ksplit < 2) return false;
+    // at most one (row, 4 elements) merge item per thread of the 256-thread workgroup
+    const int kc = chunk_k(wtype), C = Kp / kc, kr = (C + ksplit - 1) / ksplit * kc;
+    return T * kr <= 4 * 256 && rx_lds_bytes(wtype, T, Kp, ksplit) <= 65536;
 }
 bool gemm_qx_ok(int wtype, int N, int Kp, int T, int ksplit) {
     if ((wtype != ET_I8 && wtype != ET_I4) || T < 1 || T > QX_MAX_T || N % 64 || Kp % chunk_k(wtype)) return false;
