@@ -95,6 +95,77 @@ cas_status cas_op_attention(const void* q, const void* k, const void* v, int32_t
 size_t cas_op_attention_work_bytes(int32_t Lc, int32_t n_tree, int32_t T, int32_t n_heads,
                                    int32_t head_dim, int32_t n_kv_heads, int32_t ctx_cap);
 
+/*
+ * The fused quantisers of the forward, each run alone.  Activation
+ * quantisation (Sec. 4.1; App. C) is applied by the forward inside three
+ * kernels rather than by a separate pass; these entry points run exactly
+ * those kernels, so their codes can be compared bit for bit with the row
+ * quantiser's rule (cas_op_quant_rows_q) on identical inputs.
+ *
+ * RMSNorm of the residual rows, optionally straight to per-token codes (the
+ * input of the QKV and gate/up projections of a quantised draft):
+ *   h:      [T][d] fp32 residual rows (device).  With nparts > 0 the rows
+ *           first take the pending split-K sums: h += parts[0] + ... +
+ *           parts[nparts-1], summed in that order, stored back to h
+ *   gain:   [d] fp32 gains; eps inside the square root (eps >= 0)
+ *   parts:  [nparts][T][d] fp32 (nparts in [0, 8])
+ *   qmax:   0: out receives the normalised rows [T][d] in the model type
+ *           (atype CAS_W_BF16: bf16 bits rounded to nearest even; CAS_W_F32:
+ *           fp32); 127 or 7: q [T][d] receives the codes and qs [T] the
+ *           scales of those normalised (rounded) rows, s = amax / qmax,
+ *           q = clamp(rne(x / s), -qmax, qmax), zero rows s = 0, q = 0
+ *   work:   device scratch of cas_op_rmsnorm_work_bytes(...) bytes (the
+ *           kernel's tiled output before it is written back row-major)
+ * Limits: 1 <= T <= 128, d a multiple of 16, d <= 16384.
+ */
+size_t cas_op_rmsnorm_work_bytes(int32_t atype, int32_t T, int32_t d, int32_t qmax);
+cas_status cas_op_rmsnorm(int32_t atype, float* h, const float* gain, int32_t T, int32_t d, float eps,
+                          const float* parts, int32_t nparts, int32_t qmax, void* out, int8_t* q, float* qs,
+                          void* work, size_t work_bytes, void* stream);
+
+/*
+ * Merge of the attention's KV-split partial states (the second kernel of
+ * the tree attention of a bf16 model), optionally straight to the O
+ * projection's per-token codes (the merge-and-quantise kernel of quantised
+ * drafts):
+ *   part_o:  [S][n_heads][T][head_dim] fp32: split s's unnormalised sum of
+ *            2^(x_j - m) v_j over its keys j, where x_j is the score in base-2
+ *            units (q.k_j / sqrt(head_dim) * log2(e))
+ *   part_ml: [S][n_heads][T][2] fp32: (m, l) = the split's largest x_j and
+ *            its sum of 2^(x_j - m)
+ *   The merged row is sum_s 2^(m_s - M) part_o_s / sum_s 2^(m_s - M) l_s with
+ *   M the running maximum, merged in split order, rounded to bf16.
+ *   qmax 0: out [T][n_heads*head_dim] bf16 bits; 127 or 7: q [T][n_heads*
+ *   head_dim] codes and qs [T] scales of those bf16 rows (row quantiser rule)
+ *   work: device scratch of cas_op_attn_merge_work_bytes(...) bytes
+ * Limits: S in [1, 64], 1 <= T <= 128, head_dim 64 or 128,
+ * n_heads * head_dim <= 16384.
+ */
+size_t cas_op_attn_merge_work_bytes(int32_t T, int32_t n_heads, int32_t head_dim, int32_t qmax);
+cas_status cas_op_attn_merge(const float* part_o, const float* part_ml, int32_t S, int32_t T, int32_t n_heads,
+                             int32_t head_dim, int32_t qmax, uint16_t* out, int8_t* q, float* qs, void* work,
+                             size_t work_bytes, void* stream);
+
+/*
+ * Split-K residual projection that quantises its bf16 input on load (the O
+ * and down projections of one-node quantised drafts on bf16 models): every
+ * workgroup takes the row's amax over the whole row, writes the codes of its
+ * own K range by the row quantiser's rule (s = amax / qmax) and runs the
+ * integer GEMM on them.
+ *   wtype:  CAS_W_I8 (W: codes in [-127, 127], qmax 127) or CAS_W_I4 (W:
+ *           codes in [-7, 7], packed to 4 bits by the library, qmax 7)
+ *   W [N][K] row-major codes, ws [N] per-output-channel weight scales,
+ *   x [T][K] bf16 bits (T = 1)
+ *   parts:  [splits][T][N] fp32: split k's dequantised sums over its K range,
+ *           (fp32(acc_k) * s) * ws[n]; splits = cas_op_gemm_qx_splits(...)
+ *           (0: the shape does not take this form)
+ *   work:   device scratch of cas_op_gemm_qx_work_bytes(...) bytes
+ */
+int32_t cas_op_gemm_qx_splits(int32_t wtype, int32_t N, int32_t K, int32_t T);
+size_t cas_op_gemm_qx_work_bytes(int32_t wtype, int32_t N, int32_t K, int32_t T);
+cas_status cas_op_gemm_qx(int32_t wtype, const int8_t* W, const float* ws, const uint16_t* x, int32_t N, int32_t K,
+                          int32_t T, int32_t qmax, float* parts, void* work, size_t work_bytes, void* stream);
+
 /* Plain device copy kernel (16-byte vector loads and stores): the reference
  * traffic for calibrating HBM byte counters.  bytes must be a multiple of 16. */
 cas_status cas_op_copy(void* dst, const void* src, size_t bytes, void* stream);

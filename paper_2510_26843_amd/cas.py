@@ -36,7 +36,9 @@ EXPORTS = ("cas_create", "cas_destroy", "cas_last_error", "cas_create_error", "c
            "cas_profile", "cas_profile_read", "cas_sync", "cas_op_gemm", "cas_op_gemm_work_bytes",
            "cas_op_quant_rows", "cas_op_quant_rows_q", "cas_op_quant_weight", "cas_op_quant_weight_i4",
            "cas_op_quant_weight_work_bytes", "cas_op_attention",
-           "cas_op_attention_work_bytes", "cas_op_copy")
+           "cas_op_attention_work_bytes", "cas_op_copy", "cas_op_rmsnorm", "cas_op_rmsnorm_work_bytes",
+           "cas_op_attn_merge", "cas_op_attn_merge_work_bytes", "cas_op_gemm_qx", "cas_op_gemm_qx_splits",
+           "cas_op_gemm_qx_work_bytes")
 
 
 class CasError(RuntimeError):
@@ -100,6 +102,13 @@ def lib():
             "cas_op_attention": ([P, P, P, I, I, I, I, I, I, I, P, P, P, Z, P], I),
             "cas_op_attention_work_bytes": ([I, I, I, I, I, I, I], Z),
             "cas_op_copy": ([P, P, Z, P], I),
+            "cas_op_rmsnorm": ([I, P, P, I, I, ctypes.c_float, P, I, I, P, P, P, P, Z, P], I),
+            "cas_op_rmsnorm_work_bytes": ([I, I, I, I], Z),
+            "cas_op_attn_merge": ([P, P, I, I, I, I, I, P, P, P, P, Z, P], I),
+            "cas_op_attn_merge_work_bytes": ([I, I, I, I], Z),
+            "cas_op_gemm_qx": ([I, P, P, P, I, I, I, I, P, P, Z, P], I),
+            "cas_op_gemm_qx_splits": ([I, I, I, I], I),
+            "cas_op_gemm_qx_work_bytes": ([I, I, I, I], Z),
         }
         for name, (args, res) in sig.items():
             fn = getattr(L, name)
@@ -336,3 +345,35 @@ def op_attention(q, k, v, ctx_cap: int, Lc: int, n_tree: int, T: int, H: int, Hk
 
 def op_copy(dst, src, nbytes: int, stream=None) -> None:
     _ochk(lib().cas_op_copy(_dp(dst), _dp(src), nbytes, _stream(stream)), "cas_op_copy")
+
+
+def op_rmsnorm(atype: int, h, gain, T: int, d: int, eps: float, out=None, q=None, qs=None, parts=None,
+               nparts: int = 0, qmax: int = 0, stream=None) -> None:
+    """RMSNorm of the residual rows h [T][d] (updated in place by pending
+    split-K sums when nparts > 0): the normalised rows in the model type
+    (qmax 0) or their per-token codes and scales (qmax 127 or 7)."""
+    work = _work(lib().cas_op_rmsnorm_work_bytes(atype, T, d, qmax))
+    _ochk(lib().cas_op_rmsnorm(atype, _dp(h), _dp(gain), T, d, float(eps), _dp(parts), int(nparts), int(qmax),
+                               _dp(out), _dp(q), _dp(qs), _dp(work), int(work.numel()), _stream(stream)),
+          "cas_op_rmsnorm")
+
+
+def op_attn_merge(part_o, part_ml, S: int, T: int, H: int, hd: int, out=None, q=None, qs=None, qmax: int = 0,
+                  stream=None) -> None:
+    """Merge of S attention split partials into bf16 rows (qmax 0) or their
+    per-token codes and scales (qmax 127 or 7)."""
+    work = _work(lib().cas_op_attn_merge_work_bytes(T, H, hd, qmax))
+    _ochk(lib().cas_op_attn_merge(_dp(part_o), _dp(part_ml), S, T, H, hd, int(qmax), _dp(out), _dp(q), _dp(qs),
+                                  _dp(work), int(work.numel()), _stream(stream)), "cas_op_attn_merge")
+
+
+def op_gemm_qx_splits(wtype: int, N: int, K: int, T: int) -> int:
+    return int(lib().cas_op_gemm_qx_splits(wtype, N, K, T))
+
+
+def op_gemm_qx(wtype: int, W, ws, x, N: int, K: int, T: int, qmax: int, parts, stream=None) -> None:
+    """Split-K integer projection that quantises its bf16 rows on load; parts
+    [splits][T][N] fp32 receives each split's dequantised sums."""
+    work = _work(lib().cas_op_gemm_qx_work_bytes(wtype, N, K, T))
+    _ochk(lib().cas_op_gemm_qx(wtype, _dp(W), _dp(ws), _dp(x), N, K, T, int(qmax), _dp(parts), _dp(work),
+                               int(work.numel()), _stream(stream)), "cas_op_gemm_qx")

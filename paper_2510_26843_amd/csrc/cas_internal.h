@@ -181,6 +181,9 @@ int attention_splits_win(int Lc, int n_tree, int win_sink, int win_len);
 // atype: ET_BF16 (MFMA path, then the merge of the KV splits) or ET_F32
 // (plain path, ctx_cap <= 4096)
 hipError_t launch_attention(int atype, const AttnArgs& a, hipStream_t s);
+// Only the merge of S split partials (a.part_o, a.part_ml; a.T rows of a.H
+// heads): bf16 rows into a.out, or with a.qout their codes and scales.
+hipError_t launch_attn_merge(const AttnArgs& a, int S, hipStream_t s);
 // Copy n slots of every kv head between the row-major [Hkv][n][hd] form and
 // the cache layout of one layer (to_cache = 1: into the cache).
 hipError_t launch_kv_convert(int atype, void* kc, void* vt, const void* k_rows, const void* v_rows, int Hkv,
@@ -218,6 +221,8 @@ hipError_t launch_tile_weight(int atype, const void* src, int rows, int K, void*
 hipError_t launch_untile_weight_i8(const int8_t* src, int N, int K, int8_t* dst, hipStream_t s);
 // Row-major X [T][K] -> tiled activations (col_tiles(T) tiles, width pad_k).
 hipError_t launch_tile_act(int atype, const void* src, int T, int K, void* dst, hipStream_t s);
+// Tiled activations of T rows (col_tiles(T) tiles) -> row-major X [T][K].
+hipError_t launch_untile_act(int atype, const void* src, int T, int K, void* dst, hipStream_t s);
 // Embedding gather for the call's rows plus tree metadata (depth -> position,
 // slot, ancestor masks) from the round's parent array.
 hipError_t launch_embed(int atype, const void* embed, int d, const int* round_tokens, const int* round_parent,

@@ -960,6 +960,23 @@ __global__ void k_tile_act(const T* src, int Tn, int K, int Kp, int NT, T* dst) 
     }
 }
 
+// Tiled activations -> row-major [Tn][K] (the inverse of k_tile_act; for the
+// kernel-level entry points that return a fused kernel's tiled output).
+template <typename T>
+__global__ void k_untile_act(const T* src, int Tn, int K, int NT, T* dst) {
+    constexpr int E = 16 / sizeof(T);
+    const int fpr = (K + E - 1) / E;
+    const size_t total = (size_t)Tn * fpr;
+    for (size_t idx = blockIdx.x * (size_t)blockDim.x + threadIdx.x; idx < total;
+         idx += (size_t)gridDim.x * blockDim.x) {
+        const int t = (int)(idx / fpr), k0 = (int)(idx % fpr) * E;
+        const T* i = src + xt_off(t, k0, NT, E);
+#pragma unroll
+        for (int e = 0; e < E; ++e)
+            if (k0 + e < K) dst[(size_t)t * K + k0 + e] = i[e];
+    }
+}
+
 static unsigned grid_for(size_t n) {
     size_t b = (n + 255) / 256;
     if (b > 16384) b = 16384;
@@ -993,6 +1010,21 @@ hipError_t launch_tile_act(int atype, const void* src, int Tn, int K, void* dst,
                            (float*)dst);
     else
         hipLaunchKernelGGL(k_tile_act<int8_t>, dim3(grid_for(n)), dim3(256), 0, s, (const int8_t*)src, Tn, K, Kp, NT,
+                           (int8_t*)dst);
+    return hipGetLastError();
+}
+
+hipError_t launch_untile_act(int atype, const void* src, int Tn, int K, void* dst, hipStream_t s) {
+    const int NT = col_tiles(Tn);
+    const size_t n = (size_t)Tn * ((K + frag_elems(atype) - 1) / frag_elems(atype));
+    if (atype == ET_BF16)
+        hipLaunchKernelGGL(k_untile_act<uint16_t>, dim3(grid_for(n)), dim3(256), 0, s, (const uint16_t*)src, Tn, K, NT,
+                           (uint16_t*)dst);
+    else if (atype == ET_F32)
+        hipLaunchKernelGGL(k_untile_act<float>, dim3(grid_for(n)), dim3(256), 0, s, (const float*)src, Tn, K, NT,
+                           (float*)dst);
+    else
+        hipLaunchKernelGGL(k_untile_act<int8_t>, dim3(grid_for(n)), dim3(256), 0, s, (const int8_t*)src, Tn, K, NT,
                            (int8_t*)dst);
     return hipGetLastError();
 }
@@ -1560,6 +1592,36 @@ __global__ void __launch_bounds__(256) k_attn_f32(const AttnArgs a, float scale)
     }
 }
 
+// The merge of the attention's S KV splits (launched by launch_attention
+// unless no_merge): bf16 rows, or with qout the rows' codes and scales.
+static bool attn_merge_ok(const AttnArgs& a) {
+    const int K = a.H * a.hd, kpq = (K + 255) / 256 * 256;
+    const int ni = (kpq / 4 + MQ_THREADS - 1) / MQ_THREADS;
+    return (a.hd == 64 || a.hd == 128) && (!a.qout || (ni <= 4 && (a.qmax == 127 || a.qmax == 7)));
+}
+
+hipError_t launch_attn_merge(const AttnArgs& a, int S, hipStream_t s) {
+    if (!attn_merge_ok(a) || S < 1 || S > ATT_MAX_SPLITS || a.T < 1) return hipErrorInvalidValue;
+    // plain merge: 4 query rows per workgroup, i.e. many small workgroups
+    // (7B layer: attention + merge 12.1 us against 14.2 with 16 rows);
+    // quantised output: one merge-and-quantise workgroup per row
+    const dim3 mg((a.T + 3) / 4, a.H);
+    const int K = a.H * a.hd, kpq = (K + 255) / 256 * 256;
+    const int ni = (kpq / 4 + MQ_THREADS - 1) / MQ_THREADS;
+    if (a.hd == 128) {
+        if (!a.qout) hipLaunchKernelGGL((k_attn_merge<128, 4>), mg, dim3(128), 0, s, a, S);
+        else if (ni <= 1) hipLaunchKernelGGL((k_attn_merge_q<128, 1>), dim3(a.T), dim3(MQ_THREADS), 0, s, a, S);
+        else if (ni <= 2) hipLaunchKernelGGL((k_attn_merge_q<128, 2>), dim3(a.T), dim3(MQ_THREADS), 0, s, a, S);
+        else hipLaunchKernelGGL((k_attn_merge_q<128, 4>), dim3(a.T), dim3(MQ_THREADS), 0, s, a, S);
+    } else {
+        if (!a.qout) hipLaunchKernelGGL((k_attn_merge<64, 4>), mg, dim3(64), 0, s, a, S);
+        else if (ni <= 1) hipLaunchKernelGGL((k_attn_merge_q<64, 1>), dim3(a.T), dim3(MQ_THREADS), 0, s, a, S);
+        else if (ni <= 2) hipLaunchKernelGGL((k_attn_merge_q<64, 2>), dim3(a.T), dim3(MQ_THREADS), 0, s, a, S);
+        else hipLaunchKernelGGL((k_attn_merge_q<64, 4>), dim3(a.T), dim3(MQ_THREADS), 0, s, a, S);
+    }
+    return hipGetLastError();
+}
+
 hipError_t launch_attention(int atype, const AttnArgs& a, hipStream_t s) {
     const int n_slots = a.Lc_host + a.n_tree_host;
     if (atype == ET_F32) {
@@ -1573,9 +1635,6 @@ hipError_t launch_attention(int atype, const AttnArgs& a, hipStream_t s) {
     const int nct = G * Tp / 16;  // 16-row query tiles per kv head
     if (a.ctx_cap % 32 || S > ATT_MAX_SPLITS) return hipErrorInvalidValue;
     const float scale_log2 = (1.0f / sqrtf((float)a.hd)) * 1.4426950408889634f;
-    // the merge: 4 query rows per workgroup, i.e. many small workgroups
-    // (7B layer: attention + merge 12.1 us against 14.2 with 16 rows)
-    const dim3 mg((a.T + 3) / 4, a.H);
     // Several query tiles per kv head, each head with at least 32 rows:
     // four tiles per workgroup share one pass of the split's K/V through LDS
     // (k_attn_rows; per layer, 8B 64 nodes at 4096: 27.7 -> 23.3 us, 7B 128
@@ -1596,33 +1655,22 @@ hipError_t launch_attention(int atype, const AttnArgs& a, hipStream_t s) {
     const bool rows = (nct >= 5 || (nct >= 3 && (long)S * a.Hkv * nct >= 2048)) && Tp >= 32;
     const int JT = (G == 1 && S * a.Hkv * nct >= 1024) ? 2 : 1;
     const int nrc = (nct + JT - 1) / JT;
-    // quantised output: one merge-and-quantise workgroup per row
-    const int K = a.H * a.hd, kpq = (K + 255) / 256 * 256;
-    const int ni = (kpq / 4 + MQ_THREADS - 1) / MQ_THREADS;
-    if (a.qout && (ni > 4 || (a.qmax != 127 && a.qmax != 7))) return hipErrorInvalidValue;
     if (a.no_merge && a.qout) return hipErrorInvalidValue;
+    if (!a.no_merge && !attn_merge_ok(a)) return hipErrorInvalidValue;
     if (a.hd == 128) {
         if (rows) hipLaunchKernelGGL((k_attn_rows<128, 4>), dim3(S, a.Hkv, (nct + 3) / 4), dim3(256), 0, s, a, scale_log2);
         else if (JT == 2) hipLaunchKernelGGL((k_attn_bf16<128, 2>), dim3(S, a.Hkv, nrc), dim3(256), 0, s, a, scale_log2);
         else hipLaunchKernelGGL((k_attn_bf16<128, 1>), dim3(S, a.Hkv, nrc), dim3(256), 0, s, a, scale_log2);
-        if (a.no_merge) {
-        } else if (!a.qout) hipLaunchKernelGGL((k_attn_merge<128, 4>), mg, dim3(128), 0, s, a, S);
-        else if (ni <= 1) hipLaunchKernelGGL((k_attn_merge_q<128, 1>), dim3(a.T), dim3(MQ_THREADS), 0, s, a, S);
-        else if (ni <= 2) hipLaunchKernelGGL((k_attn_merge_q<128, 2>), dim3(a.T), dim3(MQ_THREADS), 0, s, a, S);
-        else hipLaunchKernelGGL((k_attn_merge_q<128, 4>), dim3(a.T), dim3(MQ_THREADS), 0, s, a, S);
     } else if (a.hd == 64) {
         if (rows) hipLaunchKernelGGL((k_attn_rows<64, 4>), dim3(S, a.Hkv, (nct + 3) / 4), dim3(256), 0, s, a, scale_log2);
         else if (JT == 2) hipLaunchKernelGGL((k_attn_bf16<64, 2>), dim3(S, a.Hkv, nrc), dim3(256), 0, s, a, scale_log2);
         else hipLaunchKernelGGL((k_attn_bf16<64, 1>), dim3(S, a.Hkv, nrc), dim3(256), 0, s, a, scale_log2);
-        if (a.no_merge) {
-        } else if (!a.qout) hipLaunchKernelGGL((k_attn_merge<64, 4>), mg, dim3(64), 0, s, a, S);
-        else if (ni <= 1) hipLaunchKernelGGL((k_attn_merge_q<64, 1>), dim3(a.T), dim3(MQ_THREADS), 0, s, a, S);
-        else if (ni <= 2) hipLaunchKernelGGL((k_attn_merge_q<64, 2>), dim3(a.T), dim3(MQ_THREADS), 0, s, a, S);
-        else hipLaunchKernelGGL((k_attn_merge_q<64, 4>), dim3(a.T), dim3(MQ_THREADS), 0, s, a, S);
     } else {
         return hipErrorInvalidValue;
     }
-    return hipGetLastError();
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess || a.no_merge) return e;
+    return launch_attn_merge(a, S, s);
 }
 
 // Row-major [Hkv][n][hd] <-> cache layout, one thread per (head, slot, d).

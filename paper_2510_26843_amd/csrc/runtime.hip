@@ -1216,6 +1216,117 @@ cas_status cas_op_attention(const void* q, const void* k, const void* v, int32_t
     return e == hipSuccess ? CAS_OK : CAS_ERR_DEVICE;
 }
 
+// ---- the fused quantisers of the forward, one kernel each
+
+static size_t norm_tiled_bytes(int32_t atype, int32_t T, int32_t d, int32_t qmax) {
+    const int et = qmax ? (int)ET_I8 : atype;
+    return (size_t)16 * col_tiles(T) * pad_k(d, et) * frag_elem_bytes(et);
+}
+
+size_t cas_op_rmsnorm_work_bytes(int32_t atype, int32_t T, int32_t d, int32_t qmax) {
+    if ((atype != CAS_W_F32 && atype != CAS_W_BF16) || T < 1 || T > 128 || d < 16 || d % 16 ||
+        (qmax != 0 && qmax != 127 && qmax != 7))
+        return 0;
+    return align256(norm_tiled_bytes(atype, T, d, qmax));
+}
+
+cas_status cas_op_rmsnorm(int32_t atype, float* h, const float* gain, int32_t T, int32_t d, float eps,
+                          const float* parts, int32_t nparts, int32_t qmax, void* out, int8_t* q, float* qs,
+                          void* work, size_t work_bytes, void* stream) {
+    if (!h || !gain || !work || (nparts > 0 && !parts) || nparts < 0 || nparts > 8) return CAS_ERR_ARG;
+    if (atype != CAS_W_F32 && atype != CAS_W_BF16) return CAS_ERR_ARG;
+    if (qmax != 0 && qmax != 127 && qmax != 7) return CAS_ERR_ARG;
+    if (qmax ? (!q || !qs) : !out) return CAS_ERR_ARG;
+    if (T < 1 || T > 128 || d < 16 || d % 16 || d > 16384 || !(eps >= 0.f)) return CAS_ERR_UNSUPPORTED;
+    if (work_bytes < cas_op_rmsnorm_work_bytes(atype, T, d, qmax)) return CAS_ERR_ARG;
+    hipStream_t s = (hipStream_t)stream;
+    hipError_t e = launch_rmsnorm(atype, h, gain, T, d, eps, qmax ? nullptr : work, qmax ? (int8_t*)work : nullptr,
+                                  qs, parts, nparts, (size_t)T * d, qmax ? qmax : 127, s);
+    if (e == hipSuccess) e = launch_untile_act(qmax ? (int)ET_I8 : atype, work, T, d, qmax ? (void*)q : out, s);
+    return e == hipSuccess ? CAS_OK : CAS_ERR_DEVICE;
+}
+
+size_t cas_op_attn_merge_work_bytes(int32_t T, int32_t n_heads, int32_t head_dim, int32_t qmax) {
+    if (T < 1 || T > 128 || n_heads < 1 || (head_dim != 64 && head_dim != 128)) return 0;
+    if (qmax == 0) return 256;
+    if (qmax != 127 && qmax != 7) return 0;
+    return align256((size_t)16 * col_tiles(T) * pad_k(n_heads * head_dim, ET_I8));
+}
+
+cas_status cas_op_attn_merge(const float* part_o, const float* part_ml, int32_t S, int32_t T, int32_t n_heads,
+                             int32_t head_dim, int32_t qmax, uint16_t* out, int8_t* q, float* qs, void* work,
+                             size_t work_bytes, void* stream) {
+    if (!part_o || !part_ml || !work || S < 1 || S > 64) return CAS_ERR_ARG;
+    if (qmax != 0 && qmax != 127 && qmax != 7) return CAS_ERR_ARG;
+    if (qmax ? (!q || !qs) : !out) return CAS_ERR_ARG;
+    if (T < 1 || T > 128 || n_heads < 1 || (head_dim != 64 && head_dim != 128)) return CAS_ERR_UNSUPPORTED;
+    const size_t need = cas_op_attn_merge_work_bytes(T, n_heads, head_dim, qmax);
+    if (!need) return CAS_ERR_UNSUPPORTED;
+    if (work_bytes < need) return CAS_ERR_ARG;
+    hipStream_t s = (hipStream_t)stream;
+    AttnArgs a{};
+    a.part_o = (float*)part_o;
+    a.part_ml = (float*)part_ml;
+    a.T = T;
+    a.H = n_heads;
+    a.hd = head_dim;
+    a.out = out;
+    a.out_tiled = 0;
+    a.qout = qmax ? (int8_t*)work : nullptr;
+    a.qscale = qmax ? qs : nullptr;
+    a.qmax = qmax;
+    hipError_t e = launch_attn_merge(a, S, s);
+    if (e == hipSuccess && qmax) e = launch_untile_act(ET_I8, work, T, n_heads * head_dim, q, s);
+    return e == hipSuccess ? CAS_OK : CAS_ERR_DEVICE;
+}
+
+int32_t cas_op_gemm_qx_splits(int32_t wtype, int32_t N, int32_t K, int32_t T) {
+    if ((wtype != CAS_W_I8 && wtype != CAS_W_I4) || N < 64 || K < 16 || K % 16 || T < 1) return 0;
+    const int Kp = pad_k(K, ET_I8);
+    const int ks = gemm_parts_count(wtype, N, Kp, T);
+    return gemm_qx_ok(wtype, N, Kp, T, ks) ? ks : 0;
+}
+
+size_t cas_op_gemm_qx_work_bytes(int32_t wtype, int32_t N, int32_t K, int32_t T) {
+    if (!cas_op_gemm_qx_splits(wtype, N, K, T)) return 0;
+    const size_t Kp = pad_k(K, ET_I8);
+    const size_t wbytes = wtype == CAS_W_I4 ? (size_t)N * Kp / 2 : (size_t)N * Kp;
+    return align256(wbytes) + align256((size_t)16 * col_tiles(T) * pad_k(K, ET_BF16) * 2);
+}
+
+cas_status cas_op_gemm_qx(int32_t wtype, const int8_t* W, const float* ws, const uint16_t* x, int32_t N, int32_t K,
+                          int32_t T, int32_t qmax, float* parts, void* work, size_t work_bytes, void* stream) {
+    if (!W || !ws || !x || !parts || !work) return CAS_ERR_ARG;
+    if (wtype != CAS_W_I8 && wtype != CAS_W_I4) return CAS_ERR_ARG;
+    if (qmax != (wtype == CAS_W_I8 ? 127 : 7)) return CAS_ERR_ARG;
+    const int ks = cas_op_gemm_qx_splits(wtype, N, K, T);
+    if (!ks || N % 16) return CAS_ERR_UNSUPPORTED;
+    if (work_bytes < cas_op_gemm_qx_work_bytes(wtype, N, K, T)) return CAS_ERR_ARG;
+    hipStream_t s = (hipStream_t)stream;
+    const size_t Kp = pad_k(K, ET_I8);
+    const size_t wbytes = wtype == CAS_W_I4 ? (size_t)N * Kp / 2 : (size_t)N * Kp;
+    void* wt = work;
+    void* xt = (char*)work + align256(wbytes);
+    GemmArgs a{};
+    a.W = wt;
+    a.X = xt;
+    a.N = N;
+    a.Kp = (int)Kp;
+    a.T = T;
+    a.ws = ws;
+    a.out = parts;
+    a.ldo = N;
+    a.ksplit = ks;
+    a.part_stride = (size_t)T * N;
+    a.qx = qmax;
+    a.xk = K;
+    hipError_t e = wtype == CAS_W_I4 ? launch_pack_weight_i4(W, N, K, (uint8_t*)wt, s)
+                                     : launch_tile_weight(ET_I8, W, N, K, wt, 0, 0, 0, s);
+    if (e == hipSuccess) e = launch_tile_act(ET_BF16, x, T, K, xt, s);
+    if (e == hipSuccess) e = launch_gemm_parts(wtype, a, s);
+    return e == hipSuccess ? CAS_OK : CAS_ERR_DEVICE;
+}
+
 cas_status cas_op_copy(void* dst, const void* src, size_t bytes, void* stream) {
     if (!dst || !src || bytes % 16) return CAS_ERR_ARG;
     hipError_t e = launch_copy(dst, src, bytes, (hipStream_t)stream);

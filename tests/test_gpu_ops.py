@@ -3,8 +3,9 @@ C ABI (include/cas_ops.h), on identical seeded inputs.
 
 Bars: int8 and int4 codes, scales and integer accumulators bit-exact; the fp32/bf16
 GEMM within the rigorous fp32 summation bound K * 2^-23 * sum_k |x_k w_k|; the
-bf16 attention within 1e-2 of max |v| (probabilities are rounded to bf16 for
-the PV product: a relative 2^-9 per weight on a convex combination of v).
+bf16 attention output within half a bf16 step of the fp64 value (2^-8 |ref|,
+the output's own rounding) plus 4e-5 of max |v| (the two-term bf16
+probabilities of the PV product, 2^-17 relative per weight, and fp32 sums).
 """
 import numpy as np
 import pytest
@@ -213,7 +214,12 @@ def _attention_case(H, Hkv, hd, Lc, parents, seed):
         vis = list(range(Lc)) + [Lc + j for j in range(T) if (anc[t] >> j) & 1]
         for h in range(H):
             ref = O.attend(qf[t, h], kf[h // G, vis], vf[h // G, vis])
-            worst = max(worst, np.abs(got[t, h] - ref).max() / np.abs(vf[h // G, vis]).max())
+            # the output's bf16 rounding explains half a step, 2^-8 |ref|; the
+            # rest (two-term bf16 probabilities, 2^-17 relative per weight,
+            # i.e. up to 7.6e-6 of max |v|, plus fp32 sums) below 4e-5 of max |v|
+            vmax = np.abs(vf[h // G, vis]).max()
+            excess = np.abs(got[t, h] - ref) - 2.0 ** -8 * np.abs(ref)
+            worst = max(worst, excess.max() / vmax)
     return worst
 
 
@@ -238,7 +244,7 @@ def _attention_case(H, Hkv, hd, Lc, parents, seed):
 def test_attention_tree_mask(H, Hkv, hd, Lc, tree):
     parents = synth.tree_from_branching(*tree) if tree[0] else [-1]
     worst = _attention_case(H, Hkv, hd, Lc, parents, seed=Lc + hd + H)
-    assert worst < 1e-2, worst
+    assert worst < 4e-5, worst
 
 
 def test_copy_kernel():
