@@ -96,6 +96,27 @@ size_t cas_op_attention_work_bytes(int32_t Lc, int32_t n_tree, int32_t T, int32_
                                    int32_t head_dim, int32_t n_kv_heads, int32_t ctx_cap);
 
 /*
+ * cas_op_attention for callers that cannot allocate device memory (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc):
+ * the same arguments, kernels and results, without `work`.  The scratch (the
+ * key and value copies in the library's cache layout, the step parameters
+ * and the KV-split partials) is a device array of the library of
+ * cas_op_attention_noalloc_max_bytes() bytes (64 MiB), one per GPU, held
+ * until the process ends.  Calls whose cas_op_attention_work_bytes(...)
+ * exceeds it return CAS_ERR_CAPACITY and do nothing.  Nothing is allocated:
+ * no hipMalloc, hipFree or allocating library call.  The calling thread's
+ * current device must be the device of `stream`.  All calls on one GPU
+ * share its array: calls that overlap in time on one GPU (other threads or
+ * streams) race; the call returns after its kernels have finished, so calls
+ * made one after another from one thread do not.  Every byte of the array a
+ * call reads is written by that call first.
+ */
+size_t cas_op_attention_noalloc_max_bytes(void);
+cas_status cas_op_attention_noalloc(const void* q, const void* k, const void* v, int32_t ctx_cap, int32_t Lc,
+                                    int32_t n_tree, int32_t T, int32_t n_heads, int32_t n_kv_heads,
+                                    int32_t head_dim, const uint64_t* anc, void* out, void* stream);
+
+/*
  * The fused quantisers of the forward, each run alone.  Activation
  * quantisation (Sec. 4.1; App. C) is applied by the forward inside three
  * kernels rather than by a separate pass; these entry points run exactly

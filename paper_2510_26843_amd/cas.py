@@ -38,7 +38,7 @@ EXPORTS = ("cas_create", "cas_destroy", "cas_last_error", "cas_create_error", "c
            "cas_op_quant_weight_work_bytes", "cas_op_attention",
            "cas_op_attention_work_bytes", "cas_op_copy", "cas_op_rmsnorm", "cas_op_rmsnorm_work_bytes",
            "cas_op_attn_merge", "cas_op_attn_merge_work_bytes", "cas_op_gemm_qx", "cas_op_gemm_qx_splits",
-           "cas_op_gemm_qx_work_bytes")
+           "cas_op_gemm_qx_work_bytes", "cas_op_attention_noalloc", "cas_op_attention_noalloc_max_bytes")
 
 
 class CasError(RuntimeError):
@@ -109,6 +109,8 @@ def lib():
             "cas_op_gemm_qx": ([I, P, P, P, I, I, I, I, P, P, Z, P], I),
             "cas_op_gemm_qx_splits": ([I, I, I, I], I),
             "cas_op_gemm_qx_work_bytes": ([I, I, I, I], Z),
+            "cas_op_attention_noalloc": ([P, P, P, I, I, I, I, I, I, I, P, P, P], I),
+            "cas_op_attention_noalloc_max_bytes": ([], Z),
         }
         for name, (args, res) in sig.items():
             fn = getattr(L, name)
@@ -341,6 +343,14 @@ def op_attention(q, k, v, ctx_cap: int, Lc: int, n_tree: int, T: int, H: int, Hk
     work = _work(lib().cas_op_attention_work_bytes(Lc, n_tree, T, H, hd, Hkv, ctx_cap))
     _ochk(lib().cas_op_attention(_dp(q), _dp(k), _dp(v), ctx_cap, Lc, n_tree, T, H, Hkv, hd, _dp(anc), _dp(out),
                                  _dp(work), int(work.numel()), _stream(stream)), "cas_op_attention")
+
+
+def op_attention_noalloc(q, k, v, ctx_cap: int, Lc: int, n_tree: int, T: int, H: int, Hkv: int, hd: int, anc,
+                         out, stream=None) -> int:
+    """op_attention on the library's own scratch (no device allocation);
+    returns the status (CAS_ERR_CAPACITY beyond the scratch size)."""
+    return int(lib().cas_op_attention_noalloc(_dp(q), _dp(k), _dp(v), ctx_cap, Lc, n_tree, T, H, Hkv, hd, _dp(anc),
+                                              _dp(out), _stream(stream)))
 
 
 def op_copy(dst, src, nbytes: int, stream=None) -> None:

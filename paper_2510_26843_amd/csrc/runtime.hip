@@ -12,6 +12,7 @@
 #include <cstdio>
 #include <cstring>
 #include <map>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -1175,16 +1176,12 @@ size_t cas_op_attention_work_bytes(int32_t Lc, int32_t n_tree, int32_t T, int32_
            attention_work_bytes(Lc + n_tree, T, H, hd);
 }
 
-cas_status cas_op_attention(const void* q, const void* k, const void* v, int32_t ctx_cap, int32_t Lc, int32_t n_tree,
-                            int32_t T, int32_t H, int32_t Hkv, int32_t hd, const uint64_t* anc, void* out, void* work,
-                            size_t work_bytes, void* stream) {
-    if (!q || !k || !v || !anc || !out || !work) return CAS_ERR_ARG;
-    if (hd != 64 && hd != 128) return CAS_ERR_UNSUPPORTED;
-    if (T < 1 || T > 128 || n_tree < 1 || n_tree > 128 || Lc < 0 || Hkv < 1 || H < 1 || H % Hkv) return CAS_ERR_ARG;
-    if (ctx_cap % 32 || Lc + n_tree > ctx_cap) return CAS_ERR_ARG;
-    if (work_bytes < cas_op_attention_work_bytes(Lc, n_tree, T, H, hd, Hkv, ctx_cap)) return CAS_ERR_ARG;
-    hipStream_t s = (hipStream_t)stream;
-    // work: step parameters | K cache | V cache | split partials
+// The attention op on a scratch region `work` of at least
+// cas_op_attention_work_bytes(...) bytes: step parameters | K cache | V
+// cache | split partials, every byte the kernels read written first.
+static cas_status attention_op(const void* q, const void* k, const void* v, int32_t ctx_cap, int32_t Lc,
+                               int32_t n_tree, int32_t T, int32_t H, int32_t Hkv, int32_t hd, const uint64_t* anc,
+                               void* out, void* work, hipStream_t s) {
     StepParams sp{Lc, 0, n_tree, 0};
     char* w = (char*)work;
     StepParams* dsp = (StepParams*)w;
@@ -1214,6 +1211,67 @@ cas_status cas_op_attention(const void* q, const void* k, const void* v, int32_t
     if (e == hipSuccess) e = launch_attention(ET_BF16, a, s);
     if (e == hipSuccess) e = hipStreamSynchronize(s);  // sp lives on the caller's stack
     return e == hipSuccess ? CAS_OK : CAS_ERR_DEVICE;
+}
+
+static cas_status attention_op_check(const void* q, const void* k, const void* v, int32_t ctx_cap, int32_t Lc,
+                                     int32_t n_tree, int32_t T, int32_t H, int32_t Hkv, int32_t hd,
+                                     const uint64_t* anc, const void* out) {
+    if (!q || !k || !v || !anc || !out) return CAS_ERR_ARG;
+    if (hd != 64 && hd != 128) return CAS_ERR_UNSUPPORTED;
+    if (T < 1 || T > 128 || n_tree < 1 || n_tree > 128 || Lc < 0 || Hkv < 1 || H < 1 || H % Hkv) return CAS_ERR_ARG;
+    if (ctx_cap % 32 || Lc + n_tree > ctx_cap) return CAS_ERR_ARG;
+    return CAS_OK;
+}
+
+cas_status cas_op_attention(const void* q, const void* k, const void* v, int32_t ctx_cap, int32_t Lc, int32_t n_tree,
+                            int32_t T, int32_t H, int32_t Hkv, int32_t hd, const uint64_t* anc, void* out, void* work,
+                            size_t work_bytes, void* stream) {
+    const cas_status st = attention_op_check(q, k, v, ctx_cap, Lc, n_tree, T, H, Hkv, hd, anc, out);
+    if (st != CAS_OK) return st;
+    if (!work || work_bytes < cas_op_attention_work_bytes(Lc, n_tree, T, H, hd, Hkv, ctx_cap)) return CAS_ERR_ARG;
+    return attention_op(q, k, v, ctx_cap, Lc, n_tree, T, H, Hkv, hd, anc, out, work, (hipStream_t)stream);
+}
+
+// ---- the allocation-free attention entry point
+//
+// Its scratch is this file-scope device array: every GPU the library runs on
+// holds its own copy (at its own address) until the process ends, and every
+// call on that GPU shares it.  In host code the array's name is only a
+// host-side stand-in, so the kernels get the device address from
+// hipGetSymbolAddress, taken once per device (with that device current) and
+// kept in scratch_dev.
+static constexpr size_t NOALLOC_SCRATCH_BYTES = (size_t)64 << 20;
+static constexpr int NOALLOC_MAX_DEVICES = 64;
+static __device__ __attribute__((aligned(256))) unsigned char scratch[NOALLOC_SCRATCH_BYTES];
+static std::mutex scratch_mu;
+static void* scratch_dev[NOALLOC_MAX_DEVICES];
+
+static cas_status scratch_address(void** out) {
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= NOALLOC_MAX_DEVICES) return CAS_ERR_DEVICE;
+    std::lock_guard<std::mutex> lock(scratch_mu);
+    if (!scratch_dev[dev]) {
+        void* p = nullptr;
+        if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return CAS_ERR_DEVICE;
+        scratch_dev[dev] = p;
+    }
+    *out = scratch_dev[dev];
+    return CAS_OK;
+}
+
+size_t cas_op_attention_noalloc_max_bytes(void) { return NOALLOC_SCRATCH_BYTES; }
+
+cas_status cas_op_attention_noalloc(const void* q, const void* k, const void* v, int32_t ctx_cap, int32_t Lc,
+                                    int32_t n_tree, int32_t T, int32_t H, int32_t Hkv, int32_t hd,
+                                    const uint64_t* anc, void* out, void* stream) {
+    const cas_status st = attention_op_check(q, k, v, ctx_cap, Lc, n_tree, T, H, Hkv, hd, anc, out);
+    if (st != CAS_OK) return st;
+    if (cas_op_attention_work_bytes(Lc, n_tree, T, H, hd, Hkv, ctx_cap) > NOALLOC_SCRATCH_BYTES)
+        return CAS_ERR_CAPACITY;
+    void* work = nullptr;
+    const cas_status sa = scratch_address(&work);
+    if (sa != CAS_OK) return sa;
+    return attention_op(q, k, v, ctx_cap, Lc, n_tree, T, H, Hkv, hd, anc, out, work, (hipStream_t)stream);
 }
 
 // ---- the fused quantisers of the forward, one kernel each
