@@ -4,12 +4,16 @@ benchmark's weights (seed 0).
 
 - The benchmark step at context 1024:
   - a verify forward over the 32-node tree (4,2,2,1,1), every row checked;
-  - greedy acceptance and the KV commit;
+    its main branch (the first-child chain, depth 5) carries the oracle's
+    own greedy continuation of the root (tests/golden/greedy_paths.json);
+  - greedy acceptance against the oracle's decision on the oracle's logits:
+    the same accepted nodes and bonus wherever every top-1/top-2 margin on
+    the oracle's path exceeds 0.05 (Sec. 5.1), then the KV commit;
   - the draft forward of the root with the odd layers skipped.
 - Every one of the 32 layers alone (all others skipped) on that tree.
-- Verify forwards of the latency sweep, T in {1, 8, 16, 32, 64, 128} over
-  contexts 512 / 2048 / 8192, with layers 0 and 31 active. One of them also
-  runs at full depth.
+- Verify forwards of every point of the latency sweep, T in {1, 8, 16, 32,
+  64, 128} over contexts 512 / 2048 / 8192, with layers 0 and 31 active. Two
+  of them also run at full depth.
 - On the balanced sweep trees the oracle computes only the nodes on the
   root paths of two sampled nodes. The oracle is row-independent, so those
   rows equal its full-tree rows.
@@ -24,12 +28,13 @@ Bars, per row, relative to max |oracle logit|:
 - 2e-2 for one or two active layers.
 - 4e-2 at full depth (16 or 32 layers).
 
-This random N(0, 0.02^2) decoder is chaotic at depth. Moving one bf16 step
-on one committed V slot of layer 0 moves the 32-layer logits by about
-2e-2 of their maximum. A single layer of the library differs from the fp64
-oracle by 1.5e-3 to 3e-3, and a numpy fp32 emulation of the same bf16
-contract shows the same gap. Over 32 layers this grows to 1.5e-2 to 2e-2:
-the depth of the model, not any one kernel, sets the full-depth error.
+The full-depth bar is what a correct fp32 implementation of the bf16
+contract shows: an independent fp32 emulation (tests/fp32_contract.py) lands
+2.3e-2 from the fp64 oracle on the benchmark configuration, and two such
+emulations that differ only in summation order differ by as much from each
+other.  One changed bf16 rounding decision moves every output of the next
+linear layer, so the distance grows with depth (about 2e-3 at one layer),
+whichever implementation computes it (tests/test_fp32_contract.py).
 """
 import numpy as np
 import pytest
@@ -37,29 +42,15 @@ import pytest
 from oracle import oracle as O
 from paper_2510_26843_amd import cas, synth
 
+from full_size import (check_acceptance, greedy_record, main_path, row_err as _row_err, subtree as _subtree,
+                       tree_tokens_on_greedy_path)
+
 pytestmark = [pytest.mark.gpu, pytest.mark.slow]
 
 SHAPE = synth.SHAPES["llama2_7b"]
 KV_SLOTS = 8192
 TOL = 2e-2        # one or two active layers
 TOL_DEEP = 4e-2   # 16 or 32 active layers
-
-
-def _row_err(got, ref):
-    return float((np.abs(got - ref).max(axis=1) / np.abs(ref).max(axis=1)).max())
-
-
-def _subtree(parents, nodes):
-    """Node ids on the root paths of `nodes` (ascending, so parents first)
-    and their parent list renumbered to positions in that id list."""
-    keep = set()
-    for n in nodes:
-        while n != -1:
-            keep.add(n)
-            n = parents[n]
-    ids = sorted(keep)
-    pos = {old: i for i, old in enumerate(ids)}
-    return ids, [-1 if parents[i] == -1 else pos[parents[i]] for i in ids]
 
 
 @pytest.fixture(scope="module")
@@ -83,7 +74,7 @@ def _tree(kind, arg):
     return synth.balanced_tree(arg) if kind == "balanced" else synth.tree_from_branching(*arg)
 
 
-def _check(g, o, ctx, parents, toks, sample, active, tol, tag):
+def _check(g, o, ctx, parents, toks, sample, active, tol, tag, both=False):
     skip = None if active is None else [0 if l in active else 1 for l in range(SHAPE.n_layers)]
     g.set_committed(ctx)
     o.set_committed(ctx)
@@ -93,20 +84,16 @@ def _check(g, o, ctx, parents, toks, sample, active, tol, tag):
     err = _row_err(got[ids], ref)
     print(f"[full] {tag} ctx {ctx} T {len(parents)}: {len(ids)} rows, max row error {err:.2e}", flush=True)
     assert err < tol, err
-    return got
+    return (got, ref) if both else got
 
 
-# (context, tree, sampled nodes or None for every row, full depth too),
-# longest context first
-CASES = [
-    (8192, ("balanced", 32), (31, 20), True),
-    (2048, ("balanced", 8), (7, 4), False),
-    (2048, ("balanced", 64), (63, 40), False),
-    (1024, ("branching", synth.TREE_7B), None, True),  # the benchmark step
-    (512, ("balanced", 1), None, False),
-    (512, ("balanced", 16), (15, 9), False),
-    (512, ("balanced", 128), (127, 70), False),
-]
+# (context, tree, sampled nodes or None for every row, full depth too): every
+# point of the latency sweep plus the benchmark's tree, longest context first
+_SAMPLE = {1: None, 8: (7, 4), 16: (15, 9), 32: (31, 20), 64: (63, 40), 128: (127, 70)}
+CASES = [(ctx, ("balanced", T), _SAMPLE[T], ctx == 8192 and T == 32)
+         for ctx in (8192, 2048) for T in (1, 8, 16, 32, 64, 128)]
+CASES += [(1024, ("branching", synth.TREE_7B), None, True)]  # the benchmark step
+CASES += [(512, ("balanced", T), _SAMPLE[T], False) for T in (1, 8, 16, 32, 64, 128)]
 
 
 @pytest.mark.timeout(900)
@@ -114,16 +101,26 @@ CASES = [
 def test_verify_full_7b(m7, ctx, tree, sample, deep):
     g, o = m7
     parents = _tree(*tree)
-    toks = synth.gen_tree_tokens(parents, SHAPE.vocab, seed=ctx + len(parents))
+    if ctx == 1024:
+        rec = greedy_record("llama2_7b")
+        assert rec["ctx"] == ctx and rec["depth"] == len(main_path(parents)) - 1
+        toks = tree_tokens_on_greedy_path(parents, SHAPE.vocab, ctx + len(parents), rec["path"])
+    else:
+        toks = synth.gen_tree_tokens(parents, SHAPE.vocab, seed=ctx + len(parents))
     _check(g, o, ctx, parents, toks, sample, (0, SHAPE.n_layers - 1), TOL, "layers 0 and 31")
     if not deep:
         return
-    got = _check(g, o, ctx, parents, toks, sample, None, TOL_DEEP, "full depth")
+    got, ref = _check(g, o, ctx, parents, toks, sample, None, TOL_DEEP, "full depth", both=True)
     if ctx == 1024:
-        # the rest of the benchmark step: acceptance on the library's own
-        # logits, the KV commit, then the draft of the next root
-        path, bonus = g.accept()
-        assert (path, bonus) == O.accept_greedy(got.astype(np.float64), parents, toks)
+        # the rest of the benchmark step: acceptance against the oracle's own
+        # decision (and the walk on the library's own logits), the KV
+        # commit, then the draft of the next root
+        lib = g.accept()
+        assert lib == O.accept_greedy(got.astype(np.float64), parents, toks)
+        opath, _ = check_acceptance(lib, {i: ref[i] for i in range(len(parents))}, parents, toks,
+                                    "7B benchmark tree, 32 layers")
+        assert opath == main_path(parents), "the stored continuation is not the oracle's greedy path"
+        path, bonus = lib
         g.compact(path)
         o.compact(path)
         assert g.committed == ctx + len(path)
