@@ -756,6 +756,26 @@ static hipError_t gemm_go(const GemmArgs& a, hipStream_t s) {
         // tiles (waves x tiles per wave) with the most workgroups up to 256,
         // else 4x2.
         const int tiles = a.N / 16;
+        if constexpr (WT == ET_BF16 && NT >= 4) {
+            // Trees of more than 32 rows do 2-4x the MFMA and LDS work per
+            // weight byte: two waves per SIMD (workgroups of 8 one-tile
+            // waves, or 6 for 8 column tiles where 8 does not divide the
+            // tile count into at least 128 workgroups) let one wave's MFMA
+            // and LDS reads run under the other's loads.  Measured alone on
+            // the 7B shapes: gate/up T = 128 53.3 -> 43.8 us, T = 64 35.1 ->
+            // 34.5 us; QKV T = 128 42.9 -> 38.1 us (T = 64 keeps 3x1: 6x1
+            // measured 27.6 against 22.3 us).  A row's sums do not change.
+            if (tiles % 8 == 0 && tiles / 8 >= 128 && tiles / 8 <= 256) {
+                hipLaunchKernelGGL((k_gemm_wide<WT, NT, 2, 4, 8, 1, EPI, AT, false>), dim3(tiles / 8), dim3(512), 0, s,
+                                   a);
+                return hipGetLastError();
+            }
+            if (NT == 8 && tiles % 6 == 0 && tiles / 6 >= 96 && tiles / 6 <= 256) {
+                hipLaunchKernelGGL((k_gemm_wide<WT, NT, 2, 4, 6, 1, EPI, AT, false>), dim3(tiles / 6), dim3(384), 0, s,
+                                   a);
+                return hipGetLastError();
+            }
+        }
         static const int opt[4][2] = {{4, 1}, {3, 1}, {4, 2}, {3, 2}};
         int bw = 0, bt = 0, bg = 0;
         for (const auto& o : opt) {

@@ -15,6 +15,15 @@
       the same counter reads for the library's copy kernel (k_copy16) moving B
       bytes; the record carries the SHA-256 of the kernel source it was
       taken on.
+
+  python -m paper_2510_26843_amd.profsum counters A.csv [B.csv ...]
+         --kernel 'label=REGEX@GRID[:i/n]' [--kernel ...] [--copy-bytes B]
+      mean value per dispatch of every counter in the given counter passes,
+      for each listed kernel (GRID 0: any grid; :i/n keeps the matching
+      dispatches whose index in dispatch order is i modulo n, e.g. the O and
+      down projections, which share one kernel and grid, alternate).  With
+      --copy-bytes, FETCH_SIZE and WRITE_SIZE are also given as HBM bytes,
+      scaled by what they read for the copy kernel k_copy16 moving B bytes.
 """
 import argparse
 import collections
@@ -119,6 +128,60 @@ def traffic(args) -> dict:
             "hbm_bytes_per_launch": round(fetch_b + write_b), "kernels_sha256": sha}
 
 
+def _kernel_spec(spec: str):
+    label, rest = spec.split("=", 1)
+    regex, grid = rest.rsplit("@", 1)
+    sel = None
+    if ":" in grid:
+        grid, sel = grid.split(":")
+        i, n = sel.split("/")
+        sel = (int(i), int(n))
+    return label, regex, int(grid), sel
+
+
+def counter_table(paths, specs, copy_bytes=0) -> str:
+    """Mean value per dispatch of each counter, per listed kernel."""
+    rows = []
+    for p in paths:
+        rows += list(csv.DictReader(open(p)))
+    counters = sorted({r["Counter_Name"] for r in rows})
+    # dispatch order per (counter, kernel, grid)
+    per = collections.defaultdict(list)
+    for r in rows:
+        per[(r["Counter_Name"], r["Kernel_Name"], int(r["Grid_Size"]))].append(
+            (int(r.get("Dispatch_Id", 0) or 0), float(r["Counter_Value"])))
+    scale = {}
+    if copy_bytes:
+        for c in ("FETCH_SIZE", "WRITE_SIZE"):
+            vals = [v for (cn, k, g), vs in per.items() if cn == c and "k_copy16" in k for _, v in vs]
+            if vals:
+                scale[c] = copy_bytes / (sum(vals) / len(vals) * 1024.0)
+    head = ["kernel", "dispatches"] + counters + [f"{c} bytes" for c in ("FETCH_SIZE", "WRITE_SIZE") if c in scale]
+    out = ["| " + " | ".join(head) + " |", "|" + "---|" * len(head)]
+    for spec in specs:
+        label, regex, grid, sel = _kernel_spec(spec)
+        cells, nd = [], 0
+        means = {}
+        for c in counters:
+            vals = []
+            for (cn, k, g), vs in per.items():
+                if cn == c and re.search(regex, k) and (grid == 0 or g == grid):
+                    vals += vs
+            vals.sort()
+            if sel:
+                vals = [v for j, v in enumerate(vals) if j % sel[1] == sel[0]]
+            nd = max(nd, len(vals))
+            means[c] = sum(v for _, v in vals) / len(vals) if vals else None
+            cells.append("—" if means[c] is None else f"{means[c]:.4g}")
+        extra = [f"{means[c] * 1024.0 * scale[c]:,.0f}" if means.get(c) is not None else "—"
+                 for c in ("FETCH_SIZE", "WRITE_SIZE") if c in scale]
+        out.append(f"| {label} | {nd} | " + " | ".join(cells + extra) + " |")
+    if scale:
+        out.append("")
+        out.append("Calibration (copy kernel): " + ", ".join(f"{c} scale {v:.4f}" for c, v in scale.items()))
+    return "\n".join(out)
+
+
 def main(argv=None):
     ap = argparse.ArgumentParser()
     sub = ap.add_subparsers(dest="cmd", required=True)
@@ -135,11 +198,17 @@ def main(argv=None):
     t.add_argument("--grid", type=int, default=0)
     t.add_argument("--copy-bytes", type=int, required=True)
     t.add_argument("--out")
+    c = sub.add_parser("counters")
+    c.add_argument("csv", nargs="+")
+    c.add_argument("--kernel", action="append", required=True)
+    c.add_argument("--copy-bytes", type=int, default=0)
     a = ap.parse_args(argv)
     if a.cmd == "stats":
         print(stats_table(a.csv, a.top))
     elif a.cmd == "forward":
         print(forward_table(a.csv, a.launches))
+    elif a.cmd == "counters":
+        print(counter_table(a.csv, a.kernel, a.copy_bytes))
     else:
         rec = traffic(a)
         txt = json.dumps(rec, indent=1)
