@@ -40,7 +40,10 @@ typedef enum {
  * Limits: N multiple of 16, K multiple of 16, 1 <= T <= 128.
  * Accumulation: fp32 (float32, bf16 inputs), exact int32 (int8 and int4
  * inputs; the W4A4 form of activation quantisation, Sec. 4.1 and App. C, runs
- * its int4 codes on the int8 MFMA).
+ * its int4 codes on the int8 MFMA).  One-row calls (T = 1) with N >= 8192
+ * and bf16 or int8 weights run the GEMV-style tiles the library uses for
+ * one-node drafts (VALU dot products per lane, the four k-group lanes of a
+ * row summed at the end), other calls the MFMA tiles.
  */
 size_t cas_op_gemm_work_bytes(int32_t wtype, int32_t N, int32_t K, int32_t T);
 cas_status cas_op_gemm(int32_t wtype, const void* W, const void* X, int32_t N, int32_t K, int32_t T,

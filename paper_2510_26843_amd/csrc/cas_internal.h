@@ -131,6 +131,10 @@ struct GemmArgs {
     const float* mx_o;
     const float* mx_ml;
     int mx_S;
+    // GEMV-style tiles (wide GEMMs of one activation row, bf16 or int8
+    // weights): the caller allows a summation order of its own (drafts; not
+    // verify calls, whose rows must not depend on the tree size).  0: off.
+    int gv;
 };
 
 // wtype: element type of W and X; atype: activation type written by the

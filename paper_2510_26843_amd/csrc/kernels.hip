@@ -22,6 +22,7 @@
 // element, so this k-order is free.
 #include "cas_internal.h"
 #include <algorithm>
+#include <type_traits>
 
 #include <hip/hip_runtime.h>
 #include <math.h>
@@ -177,6 +178,25 @@ __device__ __forceinline__ i32x4 i4_step(const i32x4 blk, int h) {
     const uint32_t w0 = (uint32_t)(h ? blk[2] : blk[0]), w1 = (uint32_t)(h ? blk[3] : blk[1]);
     return i32x4{(int)sext_nib4(w0 & 0x0f0f0f0fu), (int)sext_nib4(w1 & 0x0f0f0f0fu),
                  (int)sext_nib4((w0 >> 4) & 0x0f0f0f0fu), (int)sext_nib4((w1 >> 4) & 0x0f0f0f0fu)};
+}
+
+// GEMV-style step of one activation row: the lane's 16 weight bytes (8 bf16
+// or 16 int8 k of one weight row) times the same k of the row, accumulated in
+// the lane (fp32 fma, or exact int32 dot4).  The four lanes of a weight row
+// (one per k-group) are summed once, at the end of the stream.
+__device__ __forceinline__ float gv_dot(const i32x4 w, const i32x4 x, float acc) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const uint32_t a = (uint32_t)w[i], b = (uint32_t)x[i];
+        acc = fmaf(__uint_as_float(a << 16), __uint_as_float(b << 16), acc);
+        acc = fmaf(__uint_as_float(a & 0xffff0000u), __uint_as_float(b & 0xffff0000u), acc);
+    }
+    return acc;
+}
+__device__ __forceinline__ int gv_dot(const i32x4 w, const i32x4 x, int acc) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) acc = __builtin_amdgcn_sdot4(w[i], x[i], acc, false);
+    return acc;
 }
 
 // A VALU read of an MFMA result needs a number of wait states after the MFMA
@@ -487,12 +507,22 @@ static constexpr int QX_MAX_T = 1;
 // longer contexts (7B two rows at 8192: 3.90 -> 4.01 ms; 13B one row at 4096:
 // 5.65 -> 5.70 ms).
 static constexpr int MX_MAX_T = 2;
+// GV (drafts of one row, bf16 or int8 weights): GEMV-style tiles.  Each lane
+// takes the activation row's 16 bytes at its own k-group straight from the
+// tiled activations (lane 16g of each 1 KB block) and accumulates VALU dot
+// products of its weight fragment with them; the four k-group lanes of a
+// weight row are summed with two cross-lane exchanges at the end.  No padded
+// MFMA columns, no LDS stage ring and no barrier.  Measured alone on the 7B
+// shapes at one row: gate/up 28.7 -> 27.9 us, LM head 42.8 -> 39.4 us.  The
+// sums are in a different order than the MFMA's, so verify calls (whose rows
+// must not depend on the tree size) keep the MFMA form.
 template <int WT, int NT, int UC, int D, int WAVES, int TPW, int EPI, typename AT, bool RX, bool QX = false,
-          bool MX = false>
+          bool MX = false, bool GV = false>
 __global__ void __launch_bounds__(64 * WAVES) k_gemm_wide(const GemmArgs a) {
     using Tr = WTr<WT>;
     using ACC = typename Tr::acc_t;
     constexpr int E = Tr::E;
+    static_assert(!GV || (!RX && (WT == ET_BF16 || WT == ET_I8)), "GEMV tiles: one streamed row, bf16 or int8");
     static_assert(!RX || NT == 1, "resident activations feed one column tile");
     static_assert(!QX || (RX && is_int<WT>()), "quantise-on-load feeds resident integer codes");
     static_assert(!MX || (RX && WT == ET_BF16), "merge-on-load feeds a resident bf16 row");
@@ -532,7 +562,14 @@ __global__ void __launch_bounds__(64 * WAVES) k_gemm_wide(const GemmArgs a) {
 #pragma unroll
         for (int j = 0; j < NT; ++j) acc[t][j] = ACC{0, 0, 0, 0};
     i32x4 A[D][TPW][UB];
-    i32x4 Bv[D][LPT];
+    i32x4 Bv[D][GV ? 1 : LPT];
+    // GV: the row's fragments of the stage (lane 16g of each block) and the lane sums
+    using GS = typename std::conditional<is_int<WT>(), int, float>::type;
+    i32x4 Xv[D][GV ? UC : 1];
+    GS gacc[TPW];
+#pragma unroll
+    for (int t = 0; t < TPW; ++t) gacc[t] = 0;
+    const char* xg = (const char*)a.X + (size_t)(lane >> 4) * 256 + (size_t)s0 * NB * 1024;
     QkvPre<NT> qp[TPW];
     if constexpr (EPI == EPI_QKV) {
 #pragma unroll
@@ -547,32 +584,41 @@ __global__ void __launch_bounds__(64 * WAVES) k_gemm_wide(const GemmArgs a) {
                 __builtin_nontemporal_load((const i32x4*)(wb + t * tstride + (q + u) * 1024));   \
         /* a block index past the stage (WAVES not dividing NB) reloads the last block, */  \
         /* so every wave issues the same loads; it is not stored */                         \
-        if constexpr (!RX)                                                                       \
+        if constexpr (GV)                                                                        \
+            _Pragma("unroll") for (int u = 0; u < UC; ++u) Xv[st][u] =                           \
+                *(const i32x4*)(xg + ((size_t)(stage) * NB + u * NT) * 1024);                   \
+        else if constexpr (!RX)                                                                  \
             _Pragma("unroll") for (int p = 0; p < LPT; ++p) Bv[st][p] = *(const i32x4*)(        \
                 xb + ((size_t)(stage) * NB + min(p * WAVES + wave, NB - 1)) * 1024);             \
     } while (0)
 #define CAS_W_STAGE(st, slot, stage)                                                             \
     do {                                                                                         \
-        if constexpr (!RX) {                                                                     \
-            _Pragma("unroll") for (int p = 0; p < LPT; ++p) if (p * WAVES + wave < NB)          \
-                *(i32x4*)(&lds[slot][(p * WAVES + wave) * 1024 + lane * 16]) = Bv[st][p];        \
-            __syncthreads();                                                                     \
-        }                                                                                        \
-        _Pragma("unroll") for (int u = 0; u < UC; ++u) {                                        \
-            i32x4 au[TPW];                                                                       \
-            _Pragma("unroll") for (int t = 0; t < TPW; ++t)                                     \
-                au[t] = WT == ET_I4 ? i4_step(A[st][t][u >> 1], u & 1) : A[st][t][u];            \
-            _Pragma("unroll") for (int j = 0; j < NT; ++j) {                                    \
-                i32x4 b;                                                                         \
-                if constexpr (RX) {                                                              \
-                    const int v = (stage) * UC + u; /* step of the K range */                    \
-                    b = *(const i32x4*)(xrl + ((v / FRAG_U) * 16 * E + (v % FRAG_U) * E) * EB); \
-                    if (rxz) b = i32x4{0, 0, 0, 0};                                              \
-                } else {                                                                         \
-                    b = *(const i32x4*)(&lds[slot][(u * NT + j) * 1024 + lane * 16]);            \
-                }                                                                                \
+        if constexpr (GV) {                                                                      \
+            _Pragma("unroll") for (int u = 0; u < UC; ++u)                                      \
                 _Pragma("unroll") for (int t = 0; t < TPW; ++t)                                 \
-                    acc[t][j] = mfma_step<WT>(au[t], b, acc[t][j]);                              \
+                    gacc[t] = gv_dot(A[st][t][u], Xv[st][u], gacc[t]);                           \
+        } else {                                                                                 \
+            if constexpr (!RX) {                                                                 \
+                _Pragma("unroll") for (int p = 0; p < LPT; ++p) if (p * WAVES + wave < NB)      \
+                    *(i32x4*)(&lds[slot][(p * WAVES + wave) * 1024 + lane * 16]) = Bv[st][p];    \
+                __syncthreads();                                                                 \
+            }                                                                                    \
+            _Pragma("unroll") for (int u = 0; u < UC; ++u) {                                    \
+                i32x4 au[TPW];                                                                   \
+                _Pragma("unroll") for (int t = 0; t < TPW; ++t)                                 \
+                    au[t] = WT == ET_I4 ? i4_step(A[st][t][u >> 1], u & 1) : A[st][t][u];        \
+                _Pragma("unroll") for (int j = 0; j < NT; ++j) {                                \
+                    i32x4 b;                                                                     \
+                    if constexpr (RX) {                                                          \
+                        const int v = (stage) * UC + u; /* step of the K range */                \
+                        b = *(const i32x4*)(xrl + ((v / FRAG_U) * 16 * E + (v % FRAG_U) * E) * EB); \
+                        if (rxz) b = i32x4{0, 0, 0, 0};                                          \
+                    } else {                                                                     \
+                        b = *(const i32x4*)(&lds[slot][(u * NT + j) * 1024 + lane * 16]);        \
+                    }                                                                            \
+                    _Pragma("unroll") for (int t = 0; t < TPW; ++t)                             \
+                        acc[t][j] = mfma_step<WT>(au[t], b, acc[t][j]);                          \
+                }                                                                                \
             }                                                                                    \
         }                                                                                        \
     } while (0)
@@ -682,6 +728,19 @@ __global__ void __launch_bounds__(64 * WAVES) k_gemm_wide(const GemmArgs a) {
         }
 #undef CAS_W_STAGE
 #undef CAS_W_LOAD
+    if constexpr (GV) {
+        // sum the four k-group lanes of each weight row, then put row
+        // 16 tile + 4g + i of activation row 0 where the MFMA epilogue
+        // expects it (element i of lane 16g); other lanes feed columns >= T
+#pragma unroll
+        for (int t = 0; t < TPW; ++t) {
+            GS v = gacc[t];
+            v += __shfl_xor(v, 16);
+            v += __shfl_xor(v, 32);
+#pragma unroll
+            for (int i = 0; i < 4; ++i) acc[t][0][i] = __shfl(v, 4 * (lane >> 4) + i);
+        }
+    }
     GemmArgs ae = a;
     if constexpr (QX) ae.xs = qsc;  // the scales this workgroup derived
     if (gridDim.y == 1) {
@@ -786,6 +845,25 @@ static hipError_t gemm_go(const GemmArgs& a, hipStream_t s) {
             if (tiles % 8 == 0) { bw = 4; bt = 2; bg = tiles / 8; }
             else if (tiles % 4 == 0) { bw = 4; bt = 1; bg = tiles / 4; }
             else { bw = 3; bt = 1; bg = tiles / 3; }
+        }
+        if constexpr (NT == 2 && (WT == ET_BF16 || WT == ET_I8)) {
+            if (a.gv && a.T == 1) {
+                // GEMV-style tiles, same workgroup split (stage shapes measured
+                // best alone at one row: 4x2 UC 2 D 4, 3x1 UC 4 D 4)
+                if (bw == 4 && bt == 2)
+                    hipLaunchKernelGGL((k_gemm_wide<WT, 2, 2, 4, 4, 2, EPI, AT, false, false, false, true>), dim3(bg),
+                                       dim3(256), 0, s, a);
+                else if (bw == 3 && bt == 1)
+                    hipLaunchKernelGGL((k_gemm_wide<WT, 2, 4, 4, 3, 1, EPI, AT, false, false, false, true>), dim3(bg),
+                                       dim3(192), 0, s, a);
+                else if (bw == 4 && bt == 1)
+                    hipLaunchKernelGGL((k_gemm_wide<WT, 2, 4, 4, 4, 1, EPI, AT, false, false, false, true>), dim3(bg),
+                                       dim3(256), 0, s, a);
+                else
+                    hipLaunchKernelGGL((k_gemm_wide<WT, 2, 2, 4, 3, 2, EPI, AT, false, false, false, true>), dim3(bg),
+                                       dim3(192), 0, s, a);
+                return hipGetLastError();
+            }
         }
         if constexpr (NT == 2 && WT == ET_I4) {
             if (rx_use(WT, a, 1)) {

@@ -297,6 +297,12 @@ hipError_t enqueue_forward(cas_ctx* c, int T, const uint8_t* skip, int aq) {
     // attention merge, no separate quantiser of the SwiGLU output); the QKV
     // and gate/up inputs keep the codes their RMSNorm writes
     const bool qxs = aq && et == ET_BF16;
+    // drafts of one row (a layer skipped, quantised activations or an
+    // attention window) take the GEMV-style tiles in the wide GEMMs; verify
+    // calls keep the MFMA form, whose row sums do not depend on the tree size
+    bool skips = false;
+    for (int l = 0; skip && l < f.n_layers; ++l) skips = skips || skip[l];
+    const int gv = T == 1 && (skips || aq || c->win_len > 0) ? 1 : 0;
     const int ks_o = gemm_parts_count(wq, d, c->kq_q, T), ks_d = gemm_parts_count(wq, d, c->kq_f, T);
     const bool qx_o = qxs && gemm_qx_ok(wq, d, c->kq_q, T, ks_o);
     const bool qx_d = qxs && gemm_qx_ok(wq, d, c->kq_f, T, ks_d);
@@ -341,6 +347,7 @@ hipError_t enqueue_forward(cas_ctx* c, int T, const uint8_t* skip, int aq) {
         g.xs = c->d_xs;
         g.ws = scopy(w, 0);
         g.out = c->d_q;
+        g.gv = gv;
         g.rope_cos = c->rope_cos;
         g.rope_sin = c->rope_sin;
         g.row_pos = c->d_row_pos;
@@ -396,6 +403,7 @@ hipError_t enqueue_forward(cas_ctx* c, int T, const uint8_t* skip, int aq) {
         gu.out = c->d_sw;
         gu.ldo = ffn;
         gu.out_k = ffn;
+        gu.gv = gv;
         RUN(CAS_K_GEMM_GATEUP, launch_gemm(wq, et, EPI_SWIGLU, gu, s));
         if (aq && !qx_d) RUN(CAS_K_QUANT, launch_quant_rows(et, c->d_sw, T, ffn, c->d_xq, c->d_xs, 1, qmax, s));
         GemmArgs gd{};
@@ -421,6 +429,7 @@ hipError_t enqueue_forward(cas_ctx* c, int T, const uint8_t* skip, int aq) {
     gh.X = c->d_xn;
     gh.out = c->d_logits;
     gh.ldo = f.vocab;
+    gh.gv = gv;
     RUN(CAS_K_GEMM_HEAD, launch_gemm(et, et, EPI_STORE, gh, s));
 #undef RUN
     return hipSuccess;
@@ -1116,6 +1125,7 @@ cas_status cas_op_gemm(int32_t wtype, const void* W, const void* X, int32_t N, i
     a.ws = ws;
     a.out = out;
     a.ldo = ldo;
+    a.gv = T == 1 ? 1 : 0;
     const int ep = epi == CAS_EPI_STORE ? EPI_STORE : epi == CAS_EPI_RESID ? EPI_RESID : EPI_RAW;
     hipError_t e = wtype == CAS_W_I4 ? launch_pack_weight_i4((const int8_t*)W, N, K, (uint8_t*)wt, s)
                                      : launch_tile_weight(wtype, W, N, K, wt, 0, 0, 0, s);

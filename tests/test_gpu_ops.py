@@ -41,7 +41,9 @@ def _gemm_bound(x64, w64):
 @pytest.mark.parametrize("N,K,T", [(64, 4096, 32), (48, 688, 5), (32, 256, 1), (16, 1376, 17), (64, 512, 128),
                                    (80, 11008, 64), (32, 128, 100), (8192, 512, 32), (8256, 256, 5),
                                    (8192, 384, 128), (8208, 256, 9), (8320, 128, 1), (16512, 256, 32),
-                                   (16512, 128, 100), (12288, 256, 32), (24480, 128, 20), (8240, 128, 3)])
+                                   (16512, 128, 100), (12288, 256, 32), (24480, 128, 20), (8240, 128, 3),
+                                   # one row: the GEMV-style tiles (4x1, 3x2, 3x1 and 4x2 workgroups)
+                                   (16512, 256, 1), (12288, 512, 1), (22016, 4096, 1)])
 def test_gemm_bf16(N, K, T):
     w = synth.f32_to_bf16_bits(synth.gen_activations(N, K, seed=N + K, edge_rows=False) * 0.02)
     x = synth.f32_to_bf16_bits(synth.gen_activations(T, K, seed=T + 7))
@@ -71,7 +73,9 @@ def test_gemm_f32_and_residual(N, K, T):
 
 @pytest.mark.parametrize("N,K,T", [(64, 4096, 32), (48, 688, 5), (16, 13824, 3), (32, 256, 100), (16, 5120, 64),
                                    (8192, 512, 32), (8256, 256, 1), (8192, 256, 65), (16512, 256, 17),
-                                   (12288, 128, 5), (24480, 128, 33)])
+                                   (12288, 128, 5), (24480, 128, 33),
+                                   # one row: the GEMV-style tiles (exact int32 dot4 sums)
+                                   (16512, 256, 1), (12288, 512, 1), (22016, 4096, 1)])
 def test_gemm_int8_bit_exact(N, K, T):
     rng = np.random.default_rng(N * 7 + K + T)
     qw = rng.integers(-127, 128, (N, K)).astype(np.int8)
