@@ -67,6 +67,25 @@ def _mm(x: torch.Tensor, w: torch.Tensor, k_chunks: int) -> torch.Tensor:
     return y
 
 
+def _quant_rows(x: torch.Tensor, qmax: int):
+    """Per-row symmetric codes in [-qmax, qmax]: s = amax / qmax (fp32),
+    q = clamp(round-half-even(x / s)); a zero row gives s = 0, q = 0."""
+    amax = x.abs().amax(dim=1, keepdim=True)
+    s = amax / np.float32(qmax)
+    safe = torch.where(s == 0, torch.ones_like(s), s)
+    q = torch.clamp(torch.round(x / safe), -qmax, qmax)
+    q = torch.where(s == 0, torch.zeros_like(q), q)
+    return q, s
+
+
+def _qlinear(x: torch.Tensor, qw: torch.Tensor, sw: torch.Tensor, qmax: int) -> torch.Tensor:
+    """Quantised-activation linear layer: exact integer sums (fp64 products of
+    small integers), then y = (fp32(acc) * s_x) * s_w in fp32."""
+    q, s = _quant_rows(x, qmax)
+    acc = (q.double() @ qw.double().T).float()
+    return (acc * s) * sw[None, :]
+
+
 class Fp32ContractModel:
     """A bf16-weight decoder with an fp32 KV cache holding bf16 values.
 
@@ -83,6 +102,8 @@ class Fp32ContractModel:
         self.V = [None] * shape.n_layers
         self.Lc = 0
         self.k_chunks = k_chunks
+        self.qcopy = {}           # (layer, tensor, qmax) -> (codes, scales)
+        self.round = None         # the open round: parents, depths, ancestor sets
 
     def set_kv(self, layer: int, k: np.ndarray, v: np.ndarray) -> None:
         """k, v: [Hkv][n][hd] float32 (bf16 values), placed at slots 0..n-1."""
@@ -94,56 +115,102 @@ class Fp32ContractModel:
         V[:, :n] = torch.from_numpy(np.ascontiguousarray(v, dtype=np.float32))
         self.K[layer], self.V[layer] = K, V
 
-    def forward(self, tokens: Sequence[int], parents: Sequence[int],
-                skip: Optional[Sequence[int]] = None) -> np.ndarray:
-        """Verify-style forward of a whole round (node ids 0..n-1) -> fp32 logits [n][vocab]."""
+    def _qweight(self, l: int, name: str, qmax: int):
+        key = (l, name, qmax)
+        if key not in self.qcopy:
+            w = _w(self.wts["layers"][l][name])
+            s = w.abs().amax(dim=1) / np.float32(qmax)
+            safe = torch.where(s == 0, torch.ones_like(s), s)
+            q = torch.clamp(torch.round(w / safe[:, None]), -qmax, qmax)
+            q = torch.where(s[:, None] == 0, torch.zeros_like(q), q)
+            self.qcopy[key] = (q.to(torch.int8), s)
+        return self.qcopy[key]
+
+    def prefill(self, tokens: Sequence[int]) -> None:
+        """Commit tokens as a causal chain after the committed prefix."""
+        n = len(tokens)
+        self.forward(tokens, [-1] + list(range(n - 1)))
+        self.Lc += n
+        self.round = None
+
+    def forward(self, tokens: Sequence[int], parents: Sequence[int], node_offset: int = 0,
+                skip: Optional[Sequence[int]] = None, act_quant: int = 0,
+                window: Optional[Sequence[int]] = None) -> np.ndarray:
+        """Forward over the nodes node_offset .. node_offset+n-1 of the round
+        (node_offset 0 opens a new round; parents are round node ids) ->
+        fp32 logits [n][vocab].  act_quant 1 / 2: per-token int8 / int4
+        codes for the seven linear layers of every layer that runs, against
+        per-output-channel copies of the weights (the LM head, attention and
+        KV cache keep bf16).  window = (sink, window): of the committed slots
+        only the first sink and the last window are visible."""
         s = self.s
         n = len(tokens)
         d, H, Hkv, hd = s.d_model, s.n_heads, s.n_kv_heads, s.head_dim
         G = H // Hkv
         kc = self.k_chunks
-        depth = np.zeros(n, dtype=np.int64)
-        anc = np.zeros((n, n), dtype=bool)
+        if node_offset == 0:
+            self.round = {"depth": [], "anc": []}
+        rd = self.round
         for i, p in enumerate(parents):
-            if p >= 0:
-                depth[i] = depth[p] + 1
-                anc[i] = anc[p]
-            anc[i, i] = True
+            node = node_offset + i
+            if p < 0:
+                rd["depth"].append(0)
+                rd["anc"].append({node})
+            else:
+                rd["depth"].append(rd["depth"][p] + 1)
+                rd["anc"].append(rd["anc"][p] | {node})
+        depth = np.array(rd["depth"][node_offset:node_offset + n], dtype=np.int64)
         pos = torch.from_numpy(self.Lc + depth)
         Lc = self.Lc
-        # visibility of the Lc committed slots and the n tree slots
-        vis = torch.ones(n, Lc + n, dtype=torch.bool)
-        vis[:, Lc:] = torch.from_numpy(anc)
-        neg = torch.zeros(n, Lc + n)
+        nk = node_offset + n                      # round slots that exist now
+        vis = torch.zeros(n, Lc + nk, dtype=torch.bool)
+        if window and window[1] > 0:
+            sink, win = window
+            vis[:, :min(sink, Lc)] = True
+            vis[:, max(Lc - win, min(sink, Lc)):Lc] = True
+        else:
+            vis[:, :Lc] = True
+        for i in range(n):
+            for a in rd["anc"][node_offset + i]:
+                vis[i, Lc + a] = True
+        neg = torch.zeros(n, Lc + nk)
         neg[~vis] = float("-inf")
+        qmax = {1: 127, 2: 7}.get(int(act_quant), 0)
+
+        def lin(x, l, name):
+            if qmax:
+                qw, sw = self._qweight(l, name, qmax)
+                return _qlinear(x, qw, sw, qmax)
+            return _mm(x, _w(self.wts["layers"][l][name]), kc)
+
         h = _w(self.wts["embed"][np.asarray(tokens)]).clone()
         for l in range(s.n_layers):
             if skip is not None and skip[l]:
                 continue
             lw = self.wts["layers"][l]
             x = _rmsnorm_bf16(h, torch.from_numpy(np.asarray(lw["attn_norm"], np.float32)), s.rms_eps)
-            q = _mm(x, _w(lw["wq"]), kc).view(n, H, hd)
-            k = _mm(x, _w(lw["wk"]), kc).view(n, Hkv, hd)
-            v = _mm(x, _w(lw["wv"]), kc).view(n, Hkv, hd)
+            q = lin(x, l, "wq").view(n, H, hd)
+            k = lin(x, l, "wk").view(n, Hkv, hd)
+            v = lin(x, l, "wv").view(n, Hkv, hd)
             q = _bf16(_rope(q, pos, s.rope_theta))
             k = _bf16(_rope(k, pos, s.rope_theta))
             v = _bf16(v)
-            self.K[l][:, Lc:Lc + n] = k.transpose(0, 1)
-            self.V[l][:, Lc:Lc + n] = v.transpose(0, 1)
-            Kl = self.K[l][:, :Lc + n]            # [Hkv][Lc+n][hd]
-            Vl = self.V[l][:, :Lc + n]
+            self.K[l][:, Lc + node_offset:Lc + nk] = k.transpose(0, 1)
+            self.V[l][:, Lc + node_offset:Lc + nk] = v.transpose(0, 1)
+            Kl = self.K[l][:, :Lc + nk]
+            Vl = self.V[l][:, :Lc + nk]
             o = torch.empty(n, H, hd)
             for kh in range(Hkv):
-                qh = q[:, kh * G:(kh + 1) * G, :].transpose(0, 1)      # [G][n][hd]
+                qh = q[:, kh * G:(kh + 1) * G, :].transpose(0, 1)
                 sc = (qh @ Kl[kh].T) * np.float32(1.0 / np.sqrt(hd)) + neg
                 p = torch.softmax(sc, dim=-1)
                 o[:, kh * G:(kh + 1) * G, :] = (p @ Vl[kh]).transpose(0, 1)
             o = _bf16(o.reshape(n, H * hd))
-            h = h + _mm(o, _w(lw["wo"]), kc)
+            h = h + lin(o, l, "wo")
             x = _rmsnorm_bf16(h, torch.from_numpy(np.asarray(lw["ffn_norm"], np.float32)), s.rms_eps)
-            g = _mm(x, _w(lw["w_gate"]), kc)
-            u = _mm(x, _w(lw["w_up"]), kc)
+            g = lin(x, l, "w_gate")
+            u = lin(x, l, "w_up")
             a = _bf16(torch.nn.functional.silu(g) * u)
-            h = h + _mm(a, _w(lw["w_down"]), kc)
+            h = h + lin(a, l, "w_down")
         x = _rmsnorm_bf16(h, torch.from_numpy(np.asarray(self.wts["final_norm"], np.float32)), s.rms_eps)
         return _mm(x, _w(self.wts["lm_head"]), kc).numpy()

@@ -42,8 +42,11 @@ Bars, per row relative to max |oracle logit|:
   continues from the oracle's sequence.
 
 At full depth the random N(0, 0.02^2) decoders amplify differences of one
-bf16 step. With int8 activations two correct implementations drift apart at
-least as fast as int8 noise accumulates, about 3e-2 per two layers. The
+bf16 step. With int8 activations a code that lands on the other side of a
+grid boundary moves a row much further: an independent fp32 emulation of the
+W8A8 contract (tests/fp32_contract.py) lands 8.6e-2 from the oracle on the
+level-1 rows of the 13B draft below (the library: 8.7e-2) and matches it to
+2e-7 at the root, where the library shows one such flip (4.2e-2).  The
 measured values are printed.
 """
 import numpy as np
