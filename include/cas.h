@@ -228,7 +228,8 @@ cas_status cas_kv_compact(cas_ctx* ctx, const int32_t* accepted, int32_t n_accep
 
 /* Tree metadata on the host, as the library computes it on the device:
  * depth[i] and the ancestor-or-self bitmask anc[2*i], anc[2*i+1] (bit j of
- * the 128-bit mask = node j).  Validates the parent list (n <= 128). */
+ * the 128-bit mask = node j).  Validates the parent list (n <= 128).  Either
+ * output may be NULL. */
 cas_status cas_tree_info(const int32_t* tree_parent, int32_t n, int32_t* depth, uint64_t* anc);
 
 /* Capture the forward's launches in HIP graphs keyed on (n, node_offset,
@@ -249,8 +250,41 @@ typedef enum {
 cas_status cas_profile(cas_ctx* ctx, int32_t enable);
 cas_status cas_profile_read(cas_ctx* ctx, double* ms, int32_t* launches, int32_t reset);
 
-/* Synchronise the context's stream. */
+/* Synchronise the context's stream.  In a CAS_DEBUG build it also reports a
+ * failed device check (below) as CAS_ERR_DEVICE. */
 cas_status cas_sync(cas_ctx* ctx);
+
+/*
+ * Device checks.  The library is also built with -DCAS_DEBUG
+ * (libcas_debug.so, same entry points).  Its kernels check every bound that
+ * rests on values they read from device memory rather than on their launch
+ * shape: the tree size and each row's place in the round, token ids, parent
+ * order in the tree walks (parent < child, root -1), the slot capacity of the
+ * round (Lc + n <= max_ctx), RoPE positions, KV write slots, the attention's
+ * slot range and the compaction path.  The host validates all of these before
+ * it copies them, so in a correct program no check fails.  A failed check
+ * records its code in a per-context word and skips the access it guards: the
+ * kernel ends normally, and that call's results are invalid.  The
+ * synchronising calls (cas_accept_tree, cas_topk, cas_forward with
+ * logits_host, cas_sync) then return CAS_ERR_DEVICE with the check's name and
+ * clear the word; the work of the call has been done.
+ *   cas_debug_build        1 in a CAS_DEBUG build, else 0
+ *   cas_debug_check        synchronises; *code = the recorded check code
+ *                          (0: none; 1 tree size, 2 token, 3 parent,
+ *                          4 slot capacity, 5 RoPE position, 6 KV write slot,
+ *                          7 attention slots, 8 compaction path,
+ *                          9 acceptance parent) and clears it.  Always 0 in
+ *                          a release build
+ *   cas_debug_limit_slots  makes the checks allow only slots < cap in later
+ *                          calls (0: max_ctx again), so that a test can make
+ *                          the slot checks fail while every access stays
+ *                          inside the real cache.  CAS_ERR_UNSUPPORTED in a
+ *                          release build; cap outside [0, max_ctx]:
+ *                          CAS_ERR_ARG
+ */
+int32_t cas_debug_build(void);
+cas_status cas_debug_check(cas_ctx* ctx, int32_t* code);
+cas_status cas_debug_limit_slots(cas_ctx* ctx, int32_t cap);
 
 #ifdef __cplusplus
 }

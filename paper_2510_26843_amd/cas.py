@@ -3,18 +3,27 @@
 Argument marshalling only: every step of the decoder forward, acceptance and
 compaction runs in the library's HIP kernels.  The binding refuses to run
 without the built library; there is no fallback of any kind.
+
+Environment switches read when a Model is created:
+- CAS_DEBUG=1: use libcas_debug.so, the build with device checks (failed
+  checks surface as CAS_ERR_DEVICE from the synchronising calls);
+- CAS_PROFILE=1: launch kernel by kernel with per-kernel event timing, and
+  print the per-kernel-class totals to stderr when the Model is closed.
 """
 from __future__ import annotations
 
 import ctypes
 import os
+import sys
 from typing import Dict, List, Optional, Sequence, Tuple
 
 import numpy as np
 
 _PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_PKG, "libcas.so")
+LIB_DEBUG_PATH = os.path.join(_PKG, "libcas_debug.so")
 _lib = None
+_lib_debug = None
 
 # status codes (cas_status)
 OK, ERR_ARG, ERR_TREE, ERR_CAPACITY, ERR_UNSUPPORTED, ERR_OOM, ERR_DEVICE, ERR_STATE = range(8)
@@ -38,7 +47,11 @@ EXPORTS = ("cas_create", "cas_destroy", "cas_last_error", "cas_create_error", "c
            "cas_op_quant_weight_work_bytes", "cas_op_attention",
            "cas_op_attention_work_bytes", "cas_op_copy", "cas_op_rmsnorm", "cas_op_rmsnorm_work_bytes",
            "cas_op_attn_merge", "cas_op_attn_merge_work_bytes", "cas_op_gemm_qx", "cas_op_gemm_qx_splits",
-           "cas_op_gemm_qx_work_bytes", "cas_op_attention_noalloc", "cas_op_attention_noalloc_max_bytes")
+           "cas_op_gemm_qx_work_bytes", "cas_op_attention_noalloc", "cas_op_attention_noalloc_max_bytes",
+           "cas_debug_build", "cas_debug_check", "cas_debug_limit_slots")
+# device check codes (cas_debug_check)
+DEVICE_CHECKS = ["none", "tree size", "token id", "parent order", "slot capacity", "RoPE position",
+                 "KV write slot", "attention slots", "compaction path", "acceptance parent"]
 
 
 class CasError(RuntimeError):
@@ -60,13 +73,15 @@ class Config(ctypes.Structure):
                 ("dtype", ctypes.c_int32), ("max_ctx", ctypes.c_int32), ("max_tree", ctypes.c_int32)]
 
 
-def lib():
-    """Load libcas.so; raises if it has not been built."""
-    global _lib
-    if _lib is None:
-        if not os.path.exists(LIB_PATH):
-            raise RuntimeError(f"{LIB_PATH} is not built: run `python -c 'import __graft_entry__ as g; g.build()'`")
-        L = ctypes.CDLL(LIB_PATH)
+def lib(debug: bool = False):
+    """Load libcas.so (debug: libcas_debug.so, the build with device checks);
+    raises if it has not been built."""
+    global _lib, _lib_debug
+    if (_lib_debug if debug else _lib) is None:
+        path = LIB_DEBUG_PATH if debug else LIB_PATH
+        if not os.path.exists(path):
+            raise RuntimeError(f"{path} is not built: run `python -c 'import __graft_entry__ as g; g.build()'`")
+        L = ctypes.CDLL(path)
         P, I, Z = ctypes.c_void_p, ctypes.c_int32, ctypes.c_size_t
         sig = {
             "cas_create": ([P, ctypes.c_int, P, P], I),
@@ -111,13 +126,19 @@ def lib():
             "cas_op_gemm_qx_work_bytes": ([I, I, I, I], Z),
             "cas_op_attention_noalloc": ([P, P, P, I, I, I, I, I, I, I, P, P, P], I),
             "cas_op_attention_noalloc_max_bytes": ([], Z),
+            "cas_debug_build": ([], I),
+            "cas_debug_check": ([P, P], I),
+            "cas_debug_limit_slots": ([P, I], I),
         }
         for name, (args, res) in sig.items():
             fn = getattr(L, name)
             fn.argtypes = args
             fn.restype = res
-        _lib = L
-    return _lib
+        if debug:
+            _lib_debug = L
+        else:
+            _lib = L
+    return _lib_debug if debug else _lib
 
 
 def _p(a: np.ndarray) -> int:
@@ -139,7 +160,14 @@ def tree_info(parents: Sequence[int]) -> Tuple[np.ndarray, np.ndarray]:
 class Model:
     """One decoder context (weights, KV cache, round state) on one GPU."""
 
-    def __init__(self, shape, max_ctx: int, max_tree: int = 128, device: int = 0, stream: Optional[int] = None):
+    def __init__(self, shape, max_ctx: int, max_tree: int = 128, device: int = 0, stream: Optional[int] = None,
+                 debug: Optional[bool] = None):
+        """debug: use the build with device checks (default: the CAS_DEBUG
+        environment switch)."""
+        if debug is None:
+            debug = os.environ.get("CAS_DEBUG", "0") == "1"
+        self.debug = bool(debug)
+        self._L = lib(self.debug)
         self.shape = shape
         self.bf16 = shape.dtype == "bf16"
         cfg = Config(shape.n_layers, shape.d_model, shape.n_heads, shape.n_kv_heads, shape.head_dim, shape.ffn_dim,
@@ -147,15 +175,21 @@ class Model:
                      int(max_ctx), int(max_tree))
         self.max_ctx, self.max_tree = int(max_ctx), int(max_tree)
         h = ctypes.c_void_p()
-        st = lib().cas_create(ctypes.byref(cfg), int(device), stream, ctypes.byref(h))
+        st = self._L.cas_create(ctypes.byref(cfg), int(device), stream, ctypes.byref(h))
         if st:
-            raise CasError(st, lib().cas_create_error().decode())
+            raise CasError(st, self._L.cas_create_error().decode())
         self.h = h.value
         self._acc = np.zeros(self.max_tree, dtype=np.int32)
+        self._print_profile = os.environ.get("CAS_PROFILE", "0") == "1"
+        if self._print_profile:
+            self.profile(True)
 
     def close(self) -> None:
         if getattr(self, "h", None):
-            lib().cas_destroy(self.h)
+            if getattr(self, "_print_profile", False):
+                self._print_profile = False
+                self.print_profile()
+            self._L.cas_destroy(self.h)
             self.h = None
 
     def __del__(self):
@@ -166,12 +200,12 @@ class Model:
 
     def _chk(self, st: int) -> None:
         if st:
-            raise CasError(st, lib().cas_last_error(self.h).decode())
+            raise CasError(st, self._L.cas_last_error(self.h).decode())
 
     # weights ------------------------------------------------------------------
     def load_tensor(self, name: str, layer: int, arr: np.ndarray) -> None:
         a = np.ascontiguousarray(arr)
-        self._chk(lib().cas_load_tensor(self.h, TENSOR[name], int(layer), _p(a), a.nbytes))
+        self._chk(self._L.cas_load_tensor(self.h, TENSOR[name], int(layer), _p(a), a.nbytes))
 
     def load_weights(self, w: Dict, layers: Optional[Sequence[int]] = None) -> None:
         self.load_tensor("embed", 0, w["embed"])
@@ -186,39 +220,39 @@ class Model:
             self.load_tensor("ffn_norm", l, np.asarray(lw["ffn_norm"], dtype=np.float32))
 
     def build_int8(self) -> None:
-        self._chk(lib().cas_build_int8(self.h))
+        self._chk(self._L.cas_build_int8(self.h))
 
     def build_int4(self) -> None:
         """The int4 weight copy behind act_quant = 2 (W4A4 drafts)."""
-        self._chk(lib().cas_build_int4(self.h))
+        self._chk(self._L.cas_build_int4(self.h))
 
     # state ----------------------------------------------------------------------
     @property
     def committed(self) -> int:
         n = ctypes.c_int32()
-        self._chk(lib().cas_committed_len(self.h, ctypes.byref(n)))
+        self._chk(self._L.cas_committed_len(self.h, ctypes.byref(n)))
         return n.value
 
     def set_committed(self, n: int) -> None:
-        self._chk(lib().cas_set_committed(self.h, int(n)))
+        self._chk(self._L.cas_set_committed(self.h, int(n)))
 
     def kv_load(self, layer: int, k: np.ndarray, v: np.ndarray) -> None:
         """Committed KV of one layer, [n_kv_heads][n][head_dim] in the storage type."""
         k = np.ascontiguousarray(k)
         v = np.ascontiguousarray(v)
-        self._chk(lib().cas_kv_load(self.h, int(layer), _p(k), _p(v), int(k.shape[1])))
+        self._chk(self._L.cas_kv_load(self.h, int(layer), _p(k), _p(v), int(k.shape[1])))
 
     def kv_read(self, layer: int, n: int) -> Tuple[np.ndarray, np.ndarray]:
         """KV slots 0..n-1 of one layer as [n_kv_heads][n][head_dim] (bf16 bits or float32)."""
         dt = np.uint16 if self.bf16 else np.float32
         k = np.zeros((self.shape.n_kv_heads, n, self.shape.head_dim), dtype=dt)
         v = np.zeros_like(k)
-        self._chk(lib().cas_kv_read(self.h, int(layer), _p(k), _p(v), int(n)))
+        self._chk(self._L.cas_kv_read(self.h, int(layer), _p(k), _p(v), int(n)))
         return k, v
 
     def prefill(self, tokens: Sequence[int]) -> None:
         t = np.ascontiguousarray(tokens, dtype=np.int32)
-        self._chk(lib().cas_prefill(self.h, _p(t), t.shape[0]))
+        self._chk(self._L.cas_prefill(self.h, _p(t), t.shape[0]))
 
     # the step -------------------------------------------------------------------
     def forward(self, tokens: Sequence[int], parents: Sequence[int], node_offset: int = 0,
@@ -240,23 +274,23 @@ class Model:
         if attn_window:
             o = DraftOpts(None if sk is None else _p(sk), int(act_quant), int(attn_window[0]),
                           int(attn_window[1]))
-            self._chk(lib().cas_forward_draft(self.h, _p(t), _p(p), n, int(node_offset), ctypes.byref(o),
+            self._chk(self._L.cas_forward_draft(self.h, _p(t), _p(p), n, int(node_offset), ctypes.byref(o),
                                               None if out is None else _p(out)))
         else:
-            self._chk(lib().cas_forward(self.h, _p(t), _p(p), n, int(node_offset), None if sk is None else _p(sk),
+            self._chk(self._L.cas_forward(self.h, _p(t), _p(p), n, int(node_offset), None if sk is None else _p(sk),
                                         int(act_quant), None if out is None else _p(out)))
         return out
 
     def logits_device(self) -> Tuple[int, int]:
         ptr = ctypes.c_void_p()
         n = ctypes.c_int32()
-        self._chk(lib().cas_logits_device(self.h, ctypes.byref(ptr), ctypes.byref(n)))
+        self._chk(self._L.cas_logits_device(self.h, ctypes.byref(ptr), ctypes.byref(n)))
         return ptr.value, n.value
 
     def accept(self) -> Tuple[List[int], int]:
         n = ctypes.c_int32()
         b = ctypes.c_int32()
-        self._chk(lib().cas_accept_tree(self.h, 1, _p(self._acc), ctypes.byref(n), ctypes.byref(b)))
+        self._chk(self._L.cas_accept_tree(self.h, 1, _p(self._acc), ctypes.byref(n), ctypes.byref(b)))
         return [int(x) for x in self._acc[: n.value]], int(b.value)
 
     def topk(self, K: int, n: int) -> Tuple[np.ndarray, np.ndarray]:
@@ -264,27 +298,49 @@ class Model:
         the last forward ([n][K] int32 and float32)."""
         ids = np.zeros((n, K), dtype=np.int32)
         probs = np.zeros((n, K), dtype=np.float32)
-        self._chk(lib().cas_topk(self.h, int(n), int(K), _p(ids), _p(probs)))
+        self._chk(self._L.cas_topk(self.h, int(n), int(K), _p(ids), _p(probs)))
         return ids, probs
 
     def compact(self, accepted: Sequence[int]) -> None:
         a = np.ascontiguousarray(accepted, dtype=np.int32)
-        self._chk(lib().cas_kv_compact(self.h, _p(a), a.shape[0]))
+        self._chk(self._L.cas_kv_compact(self.h, _p(a), a.shape[0]))
 
     def sync(self) -> None:
-        self._chk(lib().cas_sync(self.h))
+        self._chk(self._L.cas_sync(self.h))
 
     def set_graphs(self, on: bool) -> None:
-        self._chk(lib().cas_set_graphs(self.h, 1 if on else 0))
+        self._chk(self._L.cas_set_graphs(self.h, 1 if on else 0))
 
     def profile(self, on: bool) -> None:
-        self._chk(lib().cas_profile(self.h, 1 if on else 0))
+        self._chk(self._L.cas_profile(self.h, 1 if on else 0))
 
     def profile_read(self, reset: bool = True) -> Dict[str, Tuple[float, int]]:
         ms = np.zeros(len(KCLASS), dtype=np.float64)
         cnt = np.zeros(len(KCLASS), dtype=np.int32)
-        self._chk(lib().cas_profile_read(self.h, _p(ms), _p(cnt), 1 if reset else 0))
+        self._chk(self._L.cas_profile_read(self.h, _p(ms), _p(cnt), 1 if reset else 0))
         return {k: (float(ms[i]), int(cnt[i])) for i, k in enumerate(KCLASS)}
+
+    def print_profile(self, file=None) -> None:
+        """Per-kernel-class totals since the last read, as a table."""
+        rows = [(k, ms, n) for k, (ms, n) in self.profile_read(reset=True).items() if n]
+        out = file or sys.stderr
+        total = sum(ms for _, ms, _ in rows)
+        print(f"{'kernel class':<14}{'launches':>10}{'ms':>12}{'us/launch':>12}{'share':>8}", file=out)
+        for k, ms, n in sorted(rows, key=lambda r: -r[1]):
+            print(f"{k:<14}{n:>10}{ms:>12.3f}{1e3 * ms / n:>12.2f}{ms / total if total else 0:>8.1%}", file=out)
+
+    # device checks (CAS_DEBUG build) --------------------------------------------
+    def debug_check(self) -> int:
+        """Synchronise and return the code of a failed device check since the
+        last read (0: none; always 0 in the release build), clearing it."""
+        code = ctypes.c_int32()
+        self._chk(self._L.cas_debug_check(self.h, ctypes.byref(code)))
+        return code.value
+
+    def debug_limit_slots(self, cap: int) -> None:
+        """Make the device checks allow only KV slots < cap (0: the whole
+        cache).  Debug build only."""
+        self._chk(self._L.cas_debug_limit_slots(self.h, int(cap)))
 
 
 # ----------------------------------------------------------------------------

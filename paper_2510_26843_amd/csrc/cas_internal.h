@@ -94,8 +94,44 @@ struct StepParams {
     int Lc;           // committed slots
     int node_offset;  // id of this call's first node in the round
     int n_tree;       // nodes of the round after this call
-    int pad;
+    int cap;          // KV slots the device checks allow (the cache's capacity)
 };
+
+// Device checks of a CAS_DEBUG build.  Each guards an access whose bounds
+// rest on values the kernels read from device memory (step parameters, the
+// round's tokens and parents, row slots and positions, accepted ids): the
+// host validates all of them before they are copied, so in a correct
+// program no check fails.  A failed check stores its code in the context's
+// check word (a plain store: when several fail, any one code remains) and
+// the guarded access is skipped, so the kernel still ends normally.  Release
+// builds compile every check to `true`.
+enum DeviceCheck {
+    CHK_NONE = 0,
+    CHK_TREE_SIZE = 1,      // n_tree > 128, or a row outside the round
+    CHK_TOKEN = 2,          // token id outside [0, vocab)
+    CHK_PARENT = 3,         // parent not in [0, node) (root: not -1)
+    CHK_SLOTS = 4,          // Lc + n_tree beyond the slot capacity
+    CHK_POSITION = 5,       // RoPE position outside the table
+    CHK_KV_WRITE = 6,       // KV write slot outside the cache
+    CHK_ATTN_SLOTS = 7,     // attention over slots beyond the capacity
+    CHK_COMPACT = 8,        // accepted ids not increasing from the root within the round
+    CHK_ACCEPT_PARENT = 9,  // acceptance walk met a parent not below its child
+    CHK_COUNT = 10
+};
+#ifdef CAS_DEBUG
+constexpr bool kDeviceChecks = true;
+#else
+constexpr bool kDeviceChecks = false;
+#endif
+// true when ok (always, in release builds); else records code and returns false
+__device__ __forceinline__ bool dcheck(int* word, bool ok, int code) {
+    if constexpr (kDeviceChecks) {
+        if (!ok && word) *word = code;
+        return ok;
+    } else {
+        return true;
+    }
+}
 
 struct GemmArgs {
     const void* W;      // tiled weights, N rows, padded width Kp (element type wtype)
@@ -135,6 +171,7 @@ struct GemmArgs {
     // weights): the caller allows a summation order of its own (drafts; not
     // verify calls, whose rows must not depend on the tree size).  0: off.
     int gv;
+    int* chk;  // device check word (CAS_DEBUG builds; may be nullptr)
 };
 
 // wtype: element type of W and X; atype: activation type written by the
@@ -176,6 +213,7 @@ struct AttnArgs {
     int qmax;
     // partials only: the consumer merges the splits itself (the merge is not launched)
     int no_merge;
+    int* chk;  // device check word (CAS_DEBUG builds; may be nullptr)
 };
 size_t attention_work_bytes(int n_slots, int T, int H, int hd);
 int attention_splits(int n_slots);
@@ -229,20 +267,20 @@ hipError_t launch_tile_act(int atype, const void* src, int T, int K, void* dst, 
 hipError_t launch_untile_act(int atype, const void* src, int T, int K, void* dst, hipStream_t s);
 // Embedding gather for the call's rows plus tree metadata (depth -> position,
 // slot, ancestor masks) from the round's parent array.
-hipError_t launch_embed(int atype, const void* embed, int d, const int* round_tokens, const int* round_parent,
-                        const StepParams* sp, int T, float* h, int* row_pos, int* row_slot,
-                        uint64_t* row_anc, hipStream_t s);
+hipError_t launch_embed(int atype, const void* embed, int d, int vocab, const int* round_tokens,
+                        const int* round_parent, const StepParams* sp, int T, float* h, int* row_pos, int* row_slot,
+                        uint64_t* row_anc, int* chk, hipStream_t s);
 // Greedy acceptance: per-row argmax of logits [T][V], then the tree walk.
 // result: [0] = n_accepted, [1] = bonus token, [2] = NaN flag, [3..] = node ids.
 hipError_t launch_accept(const float* logits, int T, int V, const int* round_tokens, const int* round_parent,
-                         int* argmax_buf, int* result, hipStream_t s);
+                         int* argmax_buf, int* result, int* chk, hipStream_t s);
 // Top-K ids (value descending, lower id on ties; -1 past the finite
 // entries) and softmax probabilities of each of n logits rows [n][V]; K in
 // [1, 16]; flag[row] set to 1 when the row holds a NaN (not cleared here).
 hipError_t launch_topk(const float* logits, int n, int V, int K, int* ids, float* probs, int* flag, hipStream_t s);
 // Move accepted slots Lc+acc[j] -> Lc+j in every layer (K and V caches).
 hipError_t launch_compact(int atype, void* kc, void* vt, int L, int Hkv, int hd, int ctx_cap,
-                          const StepParams* sp, const int* accepted, int n_acc, hipStream_t s);
+                          const StepParams* sp, const int* accepted, int n_acc, int* chk, hipStream_t s);
 hipError_t launch_copy(void* dst, const void* src, size_t bytes, hipStream_t s);
 hipError_t launch_fill_zero(void* dst, size_t bytes, hipStream_t s);
 

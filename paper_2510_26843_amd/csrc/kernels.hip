@@ -247,7 +247,8 @@ struct QkvPre {
         for (int j = 0; j < NT; ++j) {
             const int t = min(16 * j + r, a.T - 1);
             slot[j] = a.row_slot[t];
-            const int pos = a.row_pos[t];
+            int pos = a.row_pos[t];
+            if (!dcheck(a.chk, pos >= 0 && pos < a.ctx_cap, CHK_POSITION)) pos = 0;
 #pragma unroll
             for (int p = 0; p < 2; ++p) {
                 const size_t idx = rot ? (size_t)pos * half + p0 + p : 0;
@@ -330,13 +331,13 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs& a, const typename 
                     AT* o = (AT*)a.out + ((size_t)t * a.H + head) * hd;
                     st2(o, p0, lo[0], lo[1]);
                     st2(o, p0 + half, hi[0], hi[1]);
-                } else {
+                } else if (dcheck(a.chk, slot >= 0 && slot < a.ctx_cap, CHK_KV_WRITE)) {
                     constexpr int ET = sizeof(AT) == 2 ? ET_BF16 : ET_F32;
                     AT* o = (AT*)a.kc + (size_t)head * a.ctx_cap * hd;
                     st2(o, kv_k_off(ET, slot, p0, hd, a.ctx_cap), lo[0], lo[1]);
                     st2(o, kv_k_off(ET, slot, p0 + half, hd, a.ctx_cap), hi[0], hi[1]);
                 }
-            } else {
+            } else if (dcheck(a.chk, slot >= 0 && slot < a.ctx_cap, CHK_KV_WRITE)) {
                 constexpr int ET = sizeof(AT) == 2 ? ET_BF16 : ET_F32;
                 const int rel = nb - qrows - krows;
                 const int head = rel / hd, dd = rel % hd;
@@ -1326,6 +1327,7 @@ __global__ void __launch_bounds__(256) k_attn_bf16(const AttnArgs a, float scale
     const int r = lane & 15, g = lane >> 4;
     const int split = blockIdx.x, kvh = blockIdx.y, rc = blockIdx.z;
     const int Lc = a.sp->Lc, n_tree = a.sp->n_tree, n_slots = Lc + n_tree;
+    if (!dcheck(a.chk, Lc >= 0 && n_slots <= a.sp->cap && a.sp->cap <= a.ctx_cap, CHK_ATTN_SLOTS)) return;
     const int n_tiles = (n_slots + 31) >> 5;
     const AttnWindow win(Lc, n_tree, a.win_sink, a.win_len);
     const int T = a.T, Tp = (T + 15) & ~15, G = a.H / a.Hkv;
@@ -1482,6 +1484,7 @@ __global__ void __launch_bounds__(64 * QT, 2) k_attn_rows(const AttnArgs a, floa
     const int r = lane & 15, g = lane >> 4;
     const int split = blockIdx.x, kvh = blockIdx.y;
     const int Lc = a.sp->Lc, n_tree = a.sp->n_tree, n_slots = Lc + n_tree;
+    if (!dcheck(a.chk, Lc >= 0 && n_slots <= a.sp->cap && a.sp->cap <= a.ctx_cap, CHK_ATTN_SLOTS)) return;
     const int n_tiles = (n_slots + 31) >> 5;
     const AttnWindow win(Lc, n_tree, a.win_sink, a.win_len);
     const int T = a.T, Tp = (T + 15) & ~15, G = a.H / a.Hkv;
@@ -1655,6 +1658,7 @@ __global__ void __launch_bounds__(256) k_attn_f32(const AttnArgs a, float scale)
     const int t = blockIdx.x, h = blockIdx.y, hd = a.hd;
     const int G = a.H / a.Hkv, kvh = h / G;
     const int Lc = a.sp->Lc, n_slots = Lc + a.sp->n_tree;
+    if (!dcheck(a.chk, Lc >= 0 && n_slots <= a.sp->cap && a.sp->cap <= a.ctx_cap, CHK_ATTN_SLOTS)) return;
     const AttnWindow win(Lc, a.sp->n_tree, a.win_sink, a.win_len);
     const uint64_t a0 = a.anc[2 * t], a1 = a.anc[2 * t + 1];
     const float* q = (const float*)a.q + ((size_t)t * a.H + h) * hd;
@@ -2197,14 +2201,23 @@ template <> __device__ __forceinline__ float piece_val<uint16_t>(const i32x4 v, 
 template <> __device__ __forceinline__ float piece_val<float>(const i32x4 v, int e) { return __int_as_float(v[e]); }
 
 template <typename AT>
-__global__ void __launch_bounds__(256) k_embed(const AT* E, int d, const int* rtok, const int* rpar,
+__global__ void __launch_bounds__(256) k_embed(const AT* E, int d, int vocab, const int* rtok, const int* rpar,
                                                const StepParams* sp, float* h, int* row_pos, int* row_slot,
-                                               uint64_t* row_anc) {
+                                               uint64_t* row_anc, int* chk) {
     __shared__ int par[128];
     const int t = blockIdx.x;
     const int node = sp->node_offset + t, Lc = sp->Lc, n_tree = sp->n_tree;
+    if (!dcheck(chk, n_tree <= 128 && sp->node_offset >= 0 && node < n_tree, CHK_TREE_SIZE)) {
+        if (threadIdx.x == 0) {
+            row_pos[t] = 0;
+            row_slot[t] = -1;
+            row_anc[2 * t] = row_anc[2 * t + 1] = 0;
+        }
+        return;
+    }
     if (threadIdx.x < n_tree) par[threadIdx.x] = rpar[threadIdx.x];
-    const int tok = rtok[node];
+    int tok = rtok[node];
+    if (!dcheck(chk, tok >= 0 && tok < vocab, CHK_TOKEN)) tok = 0;
     // the row in 16-byte pieces (d is a multiple of 16), all loads first
     constexpr int EV = 16 / sizeof(AT), MAXP = 4;  // elements per piece; pieces per thread up to d = 8192
     const AT* er = E + (size_t)tok * d;
@@ -2229,26 +2242,31 @@ __global__ void __launch_bounds__(256) k_embed(const AT* E, int d, const int* rt
     if (threadIdx.x == 0) {
         int depth = 0;
         uint64_t a0 = 0, a1 = 0;
-        for (int x = node; x >= 0; x = par[x]) {
+        for (int x = node; x >= 0;) {
             if (x < 64) a0 |= 1ull << x;
             else a1 |= 1ull << (x - 64);
             if (x != node) ++depth;
+            const int p = par[x];
+            if (!dcheck(chk, x == 0 ? p == -1 : p >= 0 && p < x, CHK_PARENT)) break;
+            x = p;
         }
+        const bool slots_ok = dcheck(chk, Lc >= 0 && Lc + n_tree <= sp->cap, CHK_SLOTS);
         row_pos[t] = Lc + depth;
-        row_slot[t] = Lc + node;
+        row_slot[t] = slots_ok ? Lc + node : -1;
         row_anc[2 * t] = a0;
         row_anc[2 * t + 1] = a1;
     }
 }
 
-hipError_t launch_embed(int atype, const void* embed, int d, const int* rtok, const int* rpar, const StepParams* sp,
-                        int T, float* h, int* row_pos, int* row_slot, uint64_t* row_anc, hipStream_t s) {
+hipError_t launch_embed(int atype, const void* embed, int d, int vocab, const int* rtok, const int* rpar,
+                        const StepParams* sp, int T, float* h, int* row_pos, int* row_slot, uint64_t* row_anc,
+                        int* chk, hipStream_t s) {
     if (atype == ET_BF16)
-        hipLaunchKernelGGL(k_embed<uint16_t>, dim3(T), dim3(256), 0, s, (const uint16_t*)embed, d, rtok, rpar, sp, h,
-                           row_pos, row_slot, row_anc);
+        hipLaunchKernelGGL(k_embed<uint16_t>, dim3(T), dim3(256), 0, s, (const uint16_t*)embed, d, vocab, rtok, rpar,
+                           sp, h, row_pos, row_slot, row_anc, chk);
     else
-        hipLaunchKernelGGL(k_embed<float>, dim3(T), dim3(256), 0, s, (const float*)embed, d, rtok, rpar, sp, h,
-                           row_pos, row_slot, row_anc);
+        hipLaunchKernelGGL(k_embed<float>, dim3(T), dim3(256), 0, s, (const float*)embed, d, vocab, rtok, rpar, sp,
+                           h, row_pos, row_slot, row_anc, chk);
     return hipGetLastError();
 }
 
@@ -2412,7 +2430,8 @@ __global__ void __launch_bounds__(256) k_accept_argmax(const float* logits, int 
 // Merge the parts of every row, then walk from the root: next = lowest-id
 // child whose token equals the current node's argmax.
 // result: [0] n_accepted, [1] bonus, [2] NaN, [3..] node ids.
-__global__ void __launch_bounds__(128) k_accept_walk(const int* gbuf, int T, const int* rtok, const int* rpar, int* result) {
+__global__ void __launch_bounds__(128) k_accept_walk(const int* gbuf, int T, const int* rtok, const int* rpar, int* result,
+                                                     int* chk) {
     __shared__ int fmc[128], gs[128];
     __shared__ int nanf;
     const int i = threadIdx.x;
@@ -2434,7 +2453,7 @@ __global__ void __launch_bounds__(128) k_accept_walk(const int* gbuf, int T, con
     __syncthreads();
     if (i > 0 && i < T) {
         const int p = rpar[i];
-        if (rtok[i] == gs[p]) atomicMin(&fmc[p], i);
+        if (dcheck(chk, p >= 0 && p < i, CHK_ACCEPT_PARENT) && rtok[i] == gs[p]) atomicMin(&fmc[p], i);
     }
     __syncthreads();
     if (i == 0) {
@@ -2452,12 +2471,12 @@ __global__ void __launch_bounds__(128) k_accept_walk(const int* gbuf, int T, con
 }
 
 hipError_t launch_accept(const float* logits, int T, int V, const int* rtok, const int* rpar, int* gbuf, int* result,
-                         hipStream_t s) {
+                         int* chk, hipStream_t s) {
     if (T < 1 || T > 128) return hipErrorInvalidValue;
     hipLaunchKernelGGL(k_accept_argmax, dim3(ACC_PARTS, T), dim3(256), 0, s, logits, V, gbuf);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(k_accept_walk, dim3(1), dim3(128), 0, s, gbuf, T, rtok, rpar, result);
+    hipLaunchKernelGGL(k_accept_walk, dim3(1), dim3(128), 0, s, gbuf, T, rtok, rpar, result, chk);
     return hipGetLastError();
 }
 
@@ -2468,11 +2487,17 @@ hipError_t launch_accept(const float* logits, int T, int V, const int* rtok, con
 // any write makes the move safe when a destination is a later node's source.
 template <typename AT>
 __global__ void __launch_bounds__(256) k_compact(AT* kc, AT* vt, int hd, int ctx_cap, const StepParams* sp,
-                                                 const int* acc, int n_acc) {
+                                                 const int* acc, int n_acc, int* chk) {
     constexpr int ET = sizeof(AT) == 2 ? ET_BF16 : ET_F32;
     extern __shared__ unsigned char smem[];
     AT* buf = (AT*)smem;
     const int Lc = sp->Lc;
+    if constexpr (kDeviceChecks) {
+        // every thread checks the whole path, so all of them leave together
+        bool ok = Lc >= 0 && Lc + sp->n_tree <= sp->cap && sp->cap <= ctx_cap && acc[0] == 0;
+        for (int j = 1; j < n_acc; ++j) ok = ok && acc[j] > acc[j - 1] && acc[j] < sp->n_tree;
+        if (!dcheck(chk, ok, CHK_COMPACT)) return;
+    }
     AT* kb = kc + (size_t)blockIdx.x * ctx_cap * hd;
     AT* vb = vt + (size_t)blockIdx.x * ctx_cap * hd;
     const int n = n_acc * hd;
@@ -2486,14 +2511,14 @@ __global__ void __launch_bounds__(256) k_compact(AT* kc, AT* vt, int hd, int ctx
 }
 
 hipError_t launch_compact(int atype, void* kc, void* vt, int L, int Hkv, int hd, int ctx_cap, const StepParams* sp,
-                          const int* accepted, int n_acc, hipStream_t s) {
+                          const int* accepted, int n_acc, int* chk, hipStream_t s) {
     if (n_acc < 1 || n_acc > 129) return hipErrorInvalidValue;
     if (atype == ET_BF16)
         hipLaunchKernelGGL(k_compact<uint16_t>, dim3(L * Hkv), dim3(256), (size_t)n_acc * hd * 2, s, (uint16_t*)kc,
-                           (uint16_t*)vt, hd, ctx_cap, sp, accepted, n_acc);
+                           (uint16_t*)vt, hd, ctx_cap, sp, accepted, n_acc, chk);
     else
         hipLaunchKernelGGL(k_compact<float>, dim3(L * Hkv), dim3(256), (size_t)n_acc * hd * 4, s, (float*)kc,
-                           (float*)vt, hd, ctx_cap, sp, accepted, n_acc);
+                           (float*)vt, hd, ctx_cap, sp, accepted, n_acc, chk);
     return hipGetLastError();
 }
 

@@ -83,6 +83,8 @@ struct cas_ctx {
     int* d_rtok = nullptr;
     int* d_rpar = nullptr;
     StepParams* d_sp = nullptr;
+    int* d_chk = nullptr;  // device check word (CAS_DEBUG builds)
+    int chk_cap = 0;       // slot capacity the device checks allow (0: ctx_cap)
     int* d_row_pos = nullptr;
     int* d_row_slot = nullptr;
     uint64_t* d_row_anc = nullptr;
@@ -140,6 +142,25 @@ cas_status hip_fail(cas_ctx* c, hipError_t e, const char* what) {
         hipError_t _e = (expr);                                \
         if (_e != hipSuccess) return hip_fail((c), _e, #expr); \
     } while (0)
+
+// CAS_DEBUG builds: after a synchronisation, report (and clear) a failed
+// device check as CAS_ERR_DEVICE.  Release builds: nothing to read.
+cas_status poll_checks(cas_ctx* c) {
+    if constexpr (kDeviceChecks) {
+        int code = 0;
+        HIPCHK(c, hipMemcpy(&code, c->d_chk, sizeof code, hipMemcpyDeviceToHost));
+        if (code) {
+            HIPCHK(c, hipMemset(c->d_chk, 0, sizeof code));
+            static const char* const names[CHK_COUNT] = {
+                "none", "tree size", "token id", "parent order", "slot capacity", "RoPE position",
+                "KV write slot", "attention slots", "compaction path", "acceptance parent"};
+            return fail(c, CAS_ERR_DEVICE, std::string("device check failed: ") +
+                                               (code > 0 && code < CHK_COUNT ? names[code] : "unknown") +
+                                               " (code " + std::to_string(code) + ")");
+        }
+    }
+    return CAS_OK;
+}
 
 template <typename T>
 hipError_t dalloc(cas_ctx* c, T** p, size_t bytes) {
@@ -264,13 +285,14 @@ hipError_t enqueue_forward(cas_ctx* c, int T, const uint8_t* skip, int aq) {
         if (e != hipSuccess) return e;                        \
     } while (0)
 
-    RUN(CAS_K_EMBED, launch_embed(et, c->embed, d, c->d_rtok, c->d_rpar, c->d_sp, T, c->d_h, c->d_row_pos,
-                                  c->d_row_slot, c->d_row_anc, s));
+    RUN(CAS_K_EMBED, launch_embed(et, c->embed, d, f.vocab, c->d_rtok, c->d_rpar, c->d_sp, T, c->d_h,
+                                  c->d_row_pos, c->d_row_slot, c->d_row_anc, c->d_chk, s));
     const size_t kv_layer = (size_t)Hkv * c->ctx_cap * hd * c->es;
     AttnArgs at{};
     at.q = c->d_q;
     at.anc = c->d_row_anc;
     at.sp = c->d_sp;
+    at.chk = c->d_chk;
     at.out = c->d_ao;
     at.out_tiled = 1;
     at.T = T;
@@ -348,6 +370,7 @@ hipError_t enqueue_forward(cas_ctx* c, int T, const uint8_t* skip, int aq) {
         g.ws = scopy(w, 0);
         g.out = c->d_q;
         g.gv = gv;
+        g.chk = c->d_chk;
         g.rope_cos = c->rope_cos;
         g.rope_sin = c->rope_sin;
         g.row_pos = c->d_row_pos;
@@ -492,7 +515,7 @@ cas_status do_forward(cas_ctx* c, const int32_t* tokens, const int32_t* parent, 
     hipEvent_t ev = nullptr;
     unsigned char* buf = next_stage(c, &ev);
     if (!buf) return fail(c, CAS_ERR_DEVICE, "staging buffer wait failed");
-    StepParams sp{c->Lc, node_offset, node_offset + n, 0};
+    StepParams sp{c->Lc, node_offset, node_offset + n, c->chk_cap ? c->chk_cap : c->ctx_cap};
     memcpy(buf, &sp, sizeof sp);
     memcpy(buf + 16, tokens, sizeof(int32_t) * n);
     memcpy(buf + 16 + 4 * 128, parent, sizeof(int32_t) * n);
@@ -552,6 +575,7 @@ cas_status do_forward(cas_ctx* c, const int32_t* tokens, const int32_t* parent, 
         HIPCHK(c, hipMemcpyAsync(logits_host, c->d_logits, sizeof(float) * (size_t)n * f.vocab, hipMemcpyDeviceToHost,
                                  c->stream));
         HIPCHK(c, hipStreamSynchronize(c->stream));
+        return poll_checks(c);
     }
     return CAS_OK;
 }
@@ -579,7 +603,7 @@ cas_status do_compact(cas_ctx* c, const int32_t* acc, int n_acc) {
         const cas_config& f = c->cfg;
         hipError_t e = timed(c, CAS_K_COMPACT, [&]() -> hipError_t {
             return launch_compact(c->et, c->kc, c->vt, f.n_layers, f.n_kv_heads, f.head_dim, c->ctx_cap, c->d_sp,
-                                  c->d_acc, n_acc, c->stream);
+                                  c->d_acc, n_acc, c->d_chk, c->stream);
         });
         if (e != hipSuccess) return hip_fail(c, e, "kv compaction");
     }
@@ -732,6 +756,8 @@ cas_status cas_create(const cas_config* cfg, int device, void* stream, cas_ctx**
     ALLOC(c->d_rtok, T * 4);
     ALLOC(c->d_rpar, T * 4);
     ALLOC(c->d_sp, sizeof(StepParams));
+    ALLOC(c->d_chk, 16);
+    if (hipMemset(c->d_chk, 0, 16) != hipSuccess) return cleanup(CAS_ERR_DEVICE, "hipMemset of the check word");
     ALLOC(c->d_row_pos, T * 4);
     ALLOC(c->d_row_slot, T * 4);
     ALLOC(c->d_row_anc, T * 16);
@@ -992,11 +1018,14 @@ cas_status cas_accept_tree(cas_ctx* c, int32_t greedy, int32_t* accepted, int32_
         return fail(c, CAS_ERR_STATE, "cas_accept_tree needs a verify call covering the whole round");
     const int T = c->n_nodes;
     hipError_t e = timed(c, CAS_K_ACCEPT, [&]() -> hipError_t {
-        return launch_accept(c->d_logits, T, c->cfg.vocab, c->d_rtok, c->d_rpar, c->d_gbuf, c->d_result, c->stream);
+        return launch_accept(c->d_logits, T, c->cfg.vocab, c->d_rtok, c->d_rpar, c->d_gbuf, c->d_result, c->d_chk,
+                             c->stream);
     });
     if (e != hipSuccess) return hip_fail(c, e, "acceptance launch");
     HIPCHK(c, hipMemcpyAsync(c->h_result, c->d_result, sizeof(int) * (size_t)(T + 3), hipMemcpyDeviceToHost, c->stream));
     HIPCHK(c, hipStreamSynchronize(c->stream));
+    cas_status cst = poll_checks(c);
+    if (cst != CAS_OK) return cst;
     if (c->h_result[2]) return fail(c, CAS_ERR_DEVICE, "NaN in the verify logits");
     const int na = c->h_result[0];
     if (na < 1 || na > T) return fail(c, CAS_ERR_DEVICE, "acceptance returned an invalid path length");
@@ -1029,6 +1058,8 @@ cas_status cas_topk(cas_ctx* c, int32_t n, int32_t K, int32_t* ids, float* probs
     HIPCHK(c, hipMemcpyAsync(h_p, d_p, sizeof(float) * (size_t)n * K, hipMemcpyDeviceToHost, c->stream));
     HIPCHK(c, hipMemcpyAsync(h_flag, d_flag, sizeof(int) * (size_t)n, hipMemcpyDeviceToHost, c->stream));
     HIPCHK(c, hipStreamSynchronize(c->stream));
+    cas_status cst = poll_checks(c);
+    if (cst != CAS_OK) return cst;
     for (int i = 0; i < n; ++i)
         if (h_flag[i]) return fail(c, CAS_ERR_DEVICE, "NaN in the logits of row " + std::to_string(i));
     memcpy(ids, h_ids, sizeof(int) * (size_t)n * K);
@@ -1081,6 +1112,27 @@ cas_status cas_profile_read(cas_ctx* c, double* ms, int32_t* launches, int32_t r
 cas_status cas_sync(cas_ctx* c) {
     if (!c) return CAS_ERR_ARG;
     HIPCHK(c, hipStreamSynchronize(c->stream));
+    return poll_checks(c);
+}
+
+int32_t cas_debug_build(void) { return kDeviceChecks ? 1 : 0; }
+
+cas_status cas_debug_check(cas_ctx* c, int32_t* code) {
+    if (!c || !code) return CAS_ERR_ARG;
+    HIPCHK(c, hipStreamSynchronize(c->stream));
+    *code = 0;
+    if constexpr (kDeviceChecks) {
+        HIPCHK(c, hipMemcpy(code, c->d_chk, sizeof(int32_t), hipMemcpyDeviceToHost));
+        if (*code) HIPCHK(c, hipMemset(c->d_chk, 0, sizeof(int32_t)));
+    }
+    return CAS_OK;
+}
+
+cas_status cas_debug_limit_slots(cas_ctx* c, int32_t cap) {
+    if (!c) return CAS_ERR_ARG;
+    if (!kDeviceChecks) return fail(c, CAS_ERR_UNSUPPORTED, "device checks are compiled only into CAS_DEBUG builds");
+    if (cap < 0 || cap > c->cfg.max_ctx) return fail(c, CAS_ERR_ARG, "cap must be in [0, max_ctx]");
+    c->chk_cap = cap;
     return CAS_OK;
 }
 
@@ -1192,7 +1244,7 @@ size_t cas_op_attention_work_bytes(int32_t Lc, int32_t n_tree, int32_t T, int32_
 static cas_status attention_op(const void* q, const void* k, const void* v, int32_t ctx_cap, int32_t Lc,
                                int32_t n_tree, int32_t T, int32_t H, int32_t Hkv, int32_t hd, const uint64_t* anc,
                                void* out, void* work, hipStream_t s) {
-    StepParams sp{Lc, 0, n_tree, 0};
+    StepParams sp{Lc, 0, n_tree, ctx_cap};
     char* w = (char*)work;
     StepParams* dsp = (StepParams*)w;
     char* kcache = w + 256;

@@ -21,13 +21,15 @@ def _declared():
     return names
 
 
-def test_library_exports_every_declared_symbol():
-    L = cas.lib()
+@pytest.mark.parametrize("debug", [False, True], ids=["release", "device_checks"])
+def test_library_exports_every_declared_symbol(debug):
+    L = cas.lib(debug)
     declared = _declared()
     assert len(declared) >= 20
     for n in sorted(declared):
         assert hasattr(L, n), n
     assert declared == set(cas.EXPORTS)
+    assert L.cas_debug_build() == (1 if debug else 0)
 
 
 @pytest.mark.parametrize("branching,n", [((3, 2, 1), 15), ((4, 2, 2, 1, 1), 32), ((4, 4, 4, 4), 64),

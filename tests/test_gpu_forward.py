@@ -172,9 +172,11 @@ def test_int4_draft_bf16_tree_with_context(weights, name, skip, window):
     matches the oracle to rounding or has a code that an upstream difference
     of one bf16 step (attention sums in fp32 against fp64) moved across a
     boundary of the 15-level grid, which moves that product by a seventh of
-    the row's range: so at least a third of the rows must match to 1e-5, and
-    no row may move further than the oracle's own largest distance between
-    this draft and the same draft unquantised (the quantisation noise)."""
+    the row's scale.  At least 12 of the 15 rows must match to 1e-5
+    (measured: 14 or 15), and every row must stay within 2e-2 (the fp32
+    decoders' W4A4 bar; measured worst 2.3e-4) and below the oracle's own
+    largest distance between this draft and the same draft unquantised (the
+    quantisation noise, 0.3 to 0.9)."""
     shape = {"gqa_small": GQA, "mha_small": MHA}[name]
     w = weights[name]
     errs, toks, parents = _int4_tree(shape, w, 300, skip, window)
@@ -190,7 +192,8 @@ def test_int4_draft_bf16_tree_with_context(weights, name, skip, window):
     exact = int((errs < 1e-5).sum())
     print(f"[w4a4] {name} skip {skip} window {window}: {exact}/15 rows exact, worst {errs.max():.3e}, "
           f"quantisation noise {noise.min():.3e}..{noise.max():.3e}", flush=True)
-    assert exact >= 5, errs
+    assert exact >= 12, errs
+    assert errs.max() < 2e-2, errs
     assert errs.max() < noise.max(), (errs, noise)
 
 
