@@ -34,6 +34,16 @@ __host__ __device__ inline size_t wt_off(int n, int k, int Kp, int E) {
     const int g = kk / (4 * E), u = (kk / E) & 3, e = kk % E, lane = g * 16 + (n & 15);
     return ((((size_t)(n >> 4) * (Kp / KC) + c) * FRAG_U + u) * 64 + lane) * E + e;
 }
+// The K-major order of a tiled weight matrix: the same 1 KB blocks, block b of
+// tile n at (b * ntiles + n) KB instead of (n * bpt + b) KB (bpt: blocks per
+// tile).  byte: offset in the tile-major order.  The GEMM workgroups walking
+// K then read adjacent blocks at the same time, which streams the gate/up and
+// LM head matrices faster (the runtime's table of block orders gives the
+// measurements); the other matrices stay tile-major.
+__host__ __device__ inline size_t wt_kmajor(size_t byte, int ntiles, int bpt) {
+    const size_t blk = byte >> 10;
+    return ((blk % bpt) * ntiles + blk / bpt) * 1024 + (byte & 1023);
+}
 __host__ __device__ inline size_t xt_off(int t, int k, int NT, int E) {
     const int KC = 16 * E, c = k / KC, kk = k % KC;
     const int g = kk / (4 * E), u = (kk / E) & 3, e = kk % E, lane = g * 16 + (t & 15);
@@ -172,6 +182,7 @@ struct GemmArgs {
     // verify calls, whose rows must not depend on the tree size).  0: off.
     int gv;
     int* chk;  // device check word (CAS_DEBUG builds; may be nullptr)
+    int kmaj;  // W is stored in the K-major block order (wt_kmajor)
 };
 
 // wtype: element type of W and X; atype: activation type written by the
@@ -247,10 +258,13 @@ hipError_t launch_rmsnorm(int atype, float* h, const float* g, int T, int d, flo
 hipError_t launch_quant_rows(int atype, const void* x, int T, int K, int8_t* q, float* qs, int tiled, int qmax,
                              hipStream_t s);
 // Tiled int8 copy of a tiled weight matrix (N rows, width K): per-row scales.
-hipError_t launch_quant_weight(int wtype, const void* w, int N, int K, int8_t* q, float* qs, hipStream_t s);
+// skm / dkm: the source / the copy in the K-major block order.
+hipError_t launch_quant_weight(int wtype, const void* w, int N, int K, int8_t* q, float* qs, hipStream_t s,
+                               int skm = 0, int dkm = 0);
 // Packed int4 copy (wt4_byte layout, width pad_k(K, ET_I8)) of a tiled weight
 // matrix: per-row scales amax / 7.
-hipError_t launch_quant_weight_i4(int wtype, const void* w, int N, int K, uint8_t* q, float* qs, hipStream_t s);
+hipError_t launch_quant_weight_i4(int wtype, const void* w, int N, int K, uint8_t* q, float* qs, hipStream_t s,
+                                  int skm = 0, int dkm = 0);
 hipError_t launch_untile_weight_i4(const uint8_t* src, int N, int K, int8_t* dst, hipStream_t s);
 // Row-major int8 codes in [-7, 7] [N][K] -> packed int4 (for the kernel-level entry point).
 hipError_t launch_pack_weight_i4(const int8_t* src, int N, int K, uint8_t* dst, hipStream_t s);
@@ -258,8 +272,10 @@ hipError_t launch_pack_weight_i4(const int8_t* src, int N, int K, uint8_t* dst, 
 // Source row i lands at tiled row row0 + map(i): mode 0 map(i) = i; mode 1
 // (q/k heads of hd rows) puts rows i and i + hd/2 of a head next to each
 // other; mode 2 map(i) = 2i (interleave with another matrix at 2i + 1).
+// kmaj_tiles > 0: dst is stored in the K-major block order of a matrix of
+// that many 16-row tiles.
 hipError_t launch_tile_weight(int atype, const void* src, int rows, int K, void* dst, int row0, int mode, int hd,
-                              hipStream_t s);
+                              hipStream_t s, int kmaj_tiles = 0);
 hipError_t launch_untile_weight_i8(const int8_t* src, int N, int K, int8_t* dst, hipStream_t s);
 // Row-major X [T][K] -> tiled activations (col_tiles(T) tiles, width pad_k).
 hipError_t launch_tile_act(int atype, const void* src, int T, int K, void* dst, hipStream_t s);

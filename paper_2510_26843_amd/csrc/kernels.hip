@@ -388,7 +388,9 @@ __global__ void __launch_bounds__(64 * WAVES) k_gemm(const GemmArgs a) {
     const int S0 = c0 * (FRAG_U / UC), S1 = c1 * (FRAG_U / UC);  // stages of UC steps
 
     static_assert(WT != ET_I4 || UC % 2 == 0, "int4 stages hold whole blocks");
-    const char* wb = (const char*)a.W + ((size_t)tile * C * wblocks<WT>() * 64 + lane) * 16;
+    // 1 KB weight blocks: tile-major, or K-major (wt_kmajor)
+    const size_t bstride = a.kmaj ? (size_t)(a.N >> 4) * 1024 : 1024;
+    const char* wb = (const char*)a.W + (size_t)lane * 16 + (size_t)tile * (a.kmaj ? 1024 : (size_t)C * wblocks<WT>() * 1024);
     const char* xb = (const char*)a.X + (size_t)lane * 16;
     ACC acc[NT];
 #pragma unroll
@@ -405,7 +407,7 @@ __global__ void __launch_bounds__(64 * WAVES) k_gemm(const GemmArgs a) {
         _Pragma("unroll") for (int u = 0; u < UC; ++u) {                                        \
             if (WT != ET_I4 || (u & 1) == 0)                                                     \
                 A[st][u] = __builtin_nontemporal_load(                                           \
-                    (const i32x4*)(wb + (WT == ET_I4 ? (q + u) / 2 : q + u) * 1024));            \
+                    (const i32x4*)(wb + (WT == ET_I4 ? (q + u) / 2 : q + u) * bstride));         \
             _Pragma("unroll") for (int j = 0; j < NT; ++j) B[st][j][u] =                         \
                 *(const i32x4*)(xb + ((q + u) * NT + j) * 1024);                                 \
         }                                                                                        \
@@ -518,7 +520,7 @@ static constexpr int MX_MAX_T = 2;
 // sums are in a different order than the MFMA's, so verify calls (whose rows
 // must not depend on the tree size) keep the MFMA form.
 template <int WT, int NT, int UC, int D, int WAVES, int TPW, int EPI, typename AT, bool RX, bool QX = false,
-          bool MX = false, bool GV = false>
+          bool MX = false, bool GV = false, bool KM = false>
 __global__ void __launch_bounds__(64 * WAVES) k_gemm_wide(const GemmArgs a) {
     using Tr = WTr<WT>;
     using ACC = typename Tr::acc_t;
@@ -546,8 +548,14 @@ __global__ void __launch_bounds__(64 * WAVES) k_gemm_wide(const GemmArgs a) {
     const int c0 = (int)(((long)blockIdx.y * C) / gridDim.y);
     const int c1 = (int)(((long)(blockIdx.y + 1) * C) / gridDim.y);
     const int s0 = c0 * (FRAG_U / UC), NS = (c1 - c0) * (FRAG_U / UC);
-    const char* wb = (const char*)a.W + ((size_t)tile0 * C * WB * 64 + lane) * 16 + (size_t)s0 * UB * 1024;
-    const size_t tstride = (size_t)C * WB * 1024;  // bytes of one tile
+    // 1 KB weight blocks: tile-major (tiles tstride apart, a tile's blocks
+    // adjacent) or, KM, K-major (wt_kmajor: tiles adjacent, a tile's blocks
+    // N/16 KB apart).  A compile-time choice: a runtime block stride costs
+    // the tile-major loops their immediate load offsets (13B W4A4 draft
+    // 1.63 -> 1.73 ms when both orders shared one kernel).
+    const size_t tstride = KM ? 1024 : (size_t)C * WB * 1024;
+    const size_t bstride = KM ? (size_t)(a.N >> 4) * 1024 : 1024;
+    const char* wb = (const char*)a.W + (size_t)lane * 16 + (size_t)tile0 * tstride + (size_t)s0 * UB * bstride;
     const char* xb = (const char*)a.X + (size_t)lane * 16 + (size_t)s0 * NB * 1024;
     // RX: element k0 of the range, row t, at xr + t * RS + k0 * EB (rows 16 bytes
     // apart in the banks); lane (g, col) of step u in chunk ch reads
@@ -582,7 +590,7 @@ __global__ void __launch_bounds__(64 * WAVES) k_gemm_wide(const GemmArgs a) {
         const size_t q = (size_t)(stage) * UB;                                                   \
         _Pragma("unroll") for (int t = 0; t < TPW; ++t)                                         \
             _Pragma("unroll") for (int u = 0; u < UB; ++u) A[st][t][u] =                        \
-                __builtin_nontemporal_load((const i32x4*)(wb + t * tstride + (q + u) * 1024));   \
+                __builtin_nontemporal_load((const i32x4*)(wb + t * tstride + (q + u) * bstride)); \
         /* a block index past the stage (WAVES not dividing NB) reloads the last block, */  \
         /* so every wave issues the same loads; it is not stored */                         \
         if constexpr (GV)                                                                        \
@@ -803,9 +811,9 @@ static bool rx_use(int wtype, const GemmArgs& a, int ksplit) {
     return wtype == ET_I4 && a.T <= RX_MAX_T && pieces <= 192L * RX_PIECES;
 }
 
-template <int WT, int NT, int EPI, typename AT>
+template <int WT, int NT, int EPI, typename AT, bool KM>
 static hipError_t gemm_go(const GemmArgs& a, hipStream_t s) {
-    if (a.qx || a.mx_o) return hipErrorInvalidValue;  // quantise / merge on load: the split-K form only
+    if (a.qx || a.mx_o || a.kmaj != (int)KM) return hipErrorInvalidValue;  // quantise / merge on load: the split-K form only
     constexpr int UC = stage_uc<WT, NT == 2 ? 4 : (NT == 4 ? 2 : 1)>();
     if (a.N >= 8192 && ((a.N / 16) % 4 == 0 || (a.N / 16) % 3 == 0)) {
         using S1 = WideStageW<WT, NT, 1>;
@@ -826,12 +834,12 @@ static hipError_t gemm_go(const GemmArgs& a, hipStream_t s) {
             // 34.5 us; QKV T = 128 42.9 -> 38.1 us (T = 64 keeps 3x1: 6x1
             // measured 27.6 against 22.3 us).  A row's sums do not change.
             if (tiles % 8 == 0 && tiles / 8 >= 128 && tiles / 8 <= 256) {
-                hipLaunchKernelGGL((k_gemm_wide<WT, NT, 2, 4, 8, 1, EPI, AT, false>), dim3(tiles / 8), dim3(512), 0, s,
+                hipLaunchKernelGGL((k_gemm_wide<WT, NT, 2, 4, 8, 1, EPI, AT, false, false, false, false, KM>), dim3(tiles / 8), dim3(512), 0, s,
                                    a);
                 return hipGetLastError();
             }
             if (NT == 8 && tiles % 6 == 0 && tiles / 6 >= 96 && tiles / 6 <= 256) {
-                hipLaunchKernelGGL((k_gemm_wide<WT, NT, 2, 4, 6, 1, EPI, AT, false>), dim3(tiles / 6), dim3(384), 0, s,
+                hipLaunchKernelGGL((k_gemm_wide<WT, NT, 2, 4, 6, 1, EPI, AT, false, false, false, false, KM>), dim3(tiles / 6), dim3(384), 0, s,
                                    a);
                 return hipGetLastError();
             }
@@ -852,16 +860,16 @@ static hipError_t gemm_go(const GemmArgs& a, hipStream_t s) {
                 // GEMV-style tiles, same workgroup split (stage shapes measured
                 // best alone at one row: 4x2 UC 2 D 4, 3x1 UC 4 D 4)
                 if (bw == 4 && bt == 2)
-                    hipLaunchKernelGGL((k_gemm_wide<WT, 2, 2, 4, 4, 2, EPI, AT, false, false, false, true>), dim3(bg),
+                    hipLaunchKernelGGL((k_gemm_wide<WT, 2, 2, 4, 4, 2, EPI, AT, false, false, false, true, KM>), dim3(bg),
                                        dim3(256), 0, s, a);
                 else if (bw == 3 && bt == 1)
-                    hipLaunchKernelGGL((k_gemm_wide<WT, 2, 4, 4, 3, 1, EPI, AT, false, false, false, true>), dim3(bg),
+                    hipLaunchKernelGGL((k_gemm_wide<WT, 2, 4, 4, 3, 1, EPI, AT, false, false, false, true, KM>), dim3(bg),
                                        dim3(192), 0, s, a);
                 else if (bw == 4 && bt == 1)
-                    hipLaunchKernelGGL((k_gemm_wide<WT, 2, 4, 4, 4, 1, EPI, AT, false, false, false, true>), dim3(bg),
+                    hipLaunchKernelGGL((k_gemm_wide<WT, 2, 4, 4, 4, 1, EPI, AT, false, false, false, true, KM>), dim3(bg),
                                        dim3(256), 0, s, a);
                 else
-                    hipLaunchKernelGGL((k_gemm_wide<WT, 2, 2, 4, 3, 2, EPI, AT, false, false, false, true>), dim3(bg),
+                    hipLaunchKernelGGL((k_gemm_wide<WT, 2, 2, 4, 3, 2, EPI, AT, false, false, false, true, KM>), dim3(bg),
                                        dim3(192), 0, s, a);
                 return hipGetLastError();
             }
@@ -870,28 +878,28 @@ static hipError_t gemm_go(const GemmArgs& a, hipStream_t s) {
             if (rx_use(WT, a, 1)) {
                 const unsigned lb = (unsigned)rx_lds_bytes(WT, a.T, a.Kp, 1);
                 if (bw == 4 && bt == 1)
-                    hipLaunchKernelGGL((k_gemm_wide<WT, 1, S1::UC, S1::D, 4, 1, EPI, AT, true>), dim3(bg), dim3(256),
+                    hipLaunchKernelGGL((k_gemm_wide<WT, 1, S1::UC, S1::D, 4, 1, EPI, AT, true, false, false, false, KM>), dim3(bg), dim3(256),
                                        lb, s, a);
                 else if (bw == 3 && bt == 1)
-                    hipLaunchKernelGGL((k_gemm_wide<WT, 1, S1::UC, S1::D, 3, 1, EPI, AT, true>), dim3(bg), dim3(192),
+                    hipLaunchKernelGGL((k_gemm_wide<WT, 1, S1::UC, S1::D, 3, 1, EPI, AT, true, false, false, false, KM>), dim3(bg), dim3(192),
                                        lb, s, a);
                 else if (bw == 4)
-                    hipLaunchKernelGGL((k_gemm_wide<WT, 1, S2::UC, S2::D, 4, 2, EPI, AT, true>), dim3(bg), dim3(256),
+                    hipLaunchKernelGGL((k_gemm_wide<WT, 1, S2::UC, S2::D, 4, 2, EPI, AT, true, false, false, false, KM>), dim3(bg), dim3(256),
                                        lb, s, a);
                 else
-                    hipLaunchKernelGGL((k_gemm_wide<WT, 1, S2::UC, S2::D, 3, 2, EPI, AT, true>), dim3(bg), dim3(192),
+                    hipLaunchKernelGGL((k_gemm_wide<WT, 1, S2::UC, S2::D, 3, 2, EPI, AT, true, false, false, false, KM>), dim3(bg), dim3(192),
                                        lb, s, a);
                 return hipGetLastError();
             }
         }
         if (bw == 4 && bt == 1)
-            hipLaunchKernelGGL((k_gemm_wide<WT, NT, S1::UC, S1::D, 4, 1, EPI, AT, false>), dim3(bg), dim3(256), 0, s, a);
+            hipLaunchKernelGGL((k_gemm_wide<WT, NT, S1::UC, S1::D, 4, 1, EPI, AT, false, false, false, false, KM>), dim3(bg), dim3(256), 0, s, a);
         else if (bw == 3 && bt == 1)
-            hipLaunchKernelGGL((k_gemm_wide<WT, NT, S1::UC, S1::D, 3, 1, EPI, AT, false>), dim3(bg), dim3(192), 0, s, a);
+            hipLaunchKernelGGL((k_gemm_wide<WT, NT, S1::UC, S1::D, 3, 1, EPI, AT, false, false, false, false, KM>), dim3(bg), dim3(192), 0, s, a);
         else if (bw == 4)
-            hipLaunchKernelGGL((k_gemm_wide<WT, NT, S2::UC, S2::D, 4, 2, EPI, AT, false>), dim3(bg), dim3(256), 0, s, a);
+            hipLaunchKernelGGL((k_gemm_wide<WT, NT, S2::UC, S2::D, 4, 2, EPI, AT, false, false, false, false, KM>), dim3(bg), dim3(256), 0, s, a);
         else
-            hipLaunchKernelGGL((k_gemm_wide<WT, NT, S2::UC, S2::D, 3, 2, EPI, AT, false>), dim3(bg), dim3(192), 0, s, a);
+            hipLaunchKernelGGL((k_gemm_wide<WT, NT, S2::UC, S2::D, 3, 2, EPI, AT, false, false, false, false, KM>), dim3(bg), dim3(192), 0, s, a);
         return hipGetLastError();
     }
     // (int4 at 8 column tiles: two steps per stage, so a shallower ring)
@@ -900,12 +908,12 @@ static hipError_t gemm_go(const GemmArgs& a, hipStream_t s) {
     return hipGetLastError();
 }
 
-template <int WT, int EPI, typename AT>
+template <int WT, int EPI, typename AT, bool KM = false>
 static hipError_t gemm_nt(const GemmArgs& a, hipStream_t s) {
     switch (col_tiles(a.T)) {
-    case 2: return gemm_go<WT, 2, EPI, AT>(a, s);
-    case 4: return gemm_go<WT, 4, EPI, AT>(a, s);
-    default: return gemm_go<WT, 8, EPI, AT>(a, s);
+    case 2: return gemm_go<WT, 2, EPI, AT, KM>(a, s);
+    case 4: return gemm_go<WT, 4, EPI, AT, KM>(a, s);
+    default: return gemm_go<WT, 8, EPI, AT, KM>(a, s);
     }
 }
 
@@ -916,17 +924,20 @@ hipError_t launch_gemm(int wtype, int atype, int epi, const GemmArgs& a, hipStre
     switch (wtype) {
     case ET_F32:
         switch (epi) {
-        case EPI_STORE: return gemm_nt<ET_F32, EPI_STORE, float>(a, s);
+        case EPI_STORE:
+            return a.kmaj ? gemm_nt<ET_F32, EPI_STORE, float, true>(a, s) : gemm_nt<ET_F32, EPI_STORE, float>(a, s);
         case EPI_RESID: return gemm_nt<ET_F32, EPI_RESID, float>(a, s);
-        case EPI_SWIGLU: return gemm_nt<ET_F32, EPI_SWIGLU, float>(a, s);
+        case EPI_SWIGLU: return gemm_nt<ET_F32, EPI_SWIGLU, float, true>(a, s);
         case EPI_QKV: return gemm_nt<ET_F32, EPI_QKV, float>(a, s);
         }
         break;
     case ET_BF16:
         switch (epi) {
-        case EPI_STORE: return gemm_nt<ET_BF16, EPI_STORE, uint16_t>(a, s);
+        case EPI_STORE:
+            return a.kmaj ? gemm_nt<ET_BF16, EPI_STORE, uint16_t, true>(a, s)
+                          : gemm_nt<ET_BF16, EPI_STORE, uint16_t>(a, s);
         case EPI_RESID: return gemm_nt<ET_BF16, EPI_RESID, uint16_t>(a, s);
-        case EPI_SWIGLU: return gemm_nt<ET_BF16, EPI_SWIGLU, uint16_t>(a, s);
+        case EPI_SWIGLU: return gemm_nt<ET_BF16, EPI_SWIGLU, uint16_t, true>(a, s);
         case EPI_QKV: return gemm_nt<ET_BF16, EPI_QKV, uint16_t>(a, s);
         }
         break;
@@ -936,7 +947,7 @@ hipError_t launch_gemm(int wtype, int atype, int epi, const GemmArgs& a, hipStre
         case EPI_RESID: return gemm_nt<ET_I8, EPI_RESID, float>(a, s);
         case EPI_RAW: return gemm_nt<ET_I8, EPI_RAW, float>(a, s);
         case EPI_SWIGLU:
-            return bf ? gemm_nt<ET_I8, EPI_SWIGLU, uint16_t>(a, s) : gemm_nt<ET_I8, EPI_SWIGLU, float>(a, s);
+            return bf ? gemm_nt<ET_I8, EPI_SWIGLU, uint16_t, true>(a, s) : gemm_nt<ET_I8, EPI_SWIGLU, float, true>(a, s);
         case EPI_QKV:
             return bf ? gemm_nt<ET_I8, EPI_QKV, uint16_t>(a, s) : gemm_nt<ET_I8, EPI_QKV, float>(a, s);
         }
@@ -972,6 +983,7 @@ int gemm_parts_count(int wtype, int N, int Kp, int T) {
 template <int WT, typename AT>
 static hipError_t gemm_parts_go(const GemmArgs& a, hipStream_t s) {
     const dim3 grid(a.N / 64, a.ksplit);
+    if (a.kmaj) return hipErrorInvalidValue;  // residual projections stay tile-major
     if (a.mx_o) {
         if constexpr (WT == ET_BF16) {
             hipLaunchKernelGGL((k_gemm_wide<WT, 1, 4, 2, 4, 1, EPI_STORE, AT, true, false, true>), grid, dim3(256),
@@ -1022,7 +1034,7 @@ hipError_t launch_gemm_parts(int wtype, const GemmArgs& a, hipStream_t s) {
 
 // Row-major weights -> tiled: one thread per 16-byte destination fragment.
 template <typename T>
-__global__ void k_tile_weight(const T* src, int rows, int K, int Kp, T* dst, int row0, int mode, int hd) {
+__global__ void k_tile_weight(const T* src, int rows, int K, int Kp, T* dst, int row0, int mode, int hd, int kt) {
     constexpr int E = 16 / sizeof(T);
     const int fpr = Kp / E;
     const size_t total = (size_t)rows * fpr;
@@ -1038,7 +1050,9 @@ __global__ void k_tile_weight(const T* src, int rows, int K, int Kp, T* dst, int
         } else {
             dr = i;
         }
-        T* o = dst + wt_off(row0 + dr, k0, Kp, E);
+        size_t off = wt_off(row0 + dr, k0, Kp, E);
+        if (kt) off = wt_kmajor(off * sizeof(T), kt, Kp * (int)sizeof(T) / 64) / sizeof(T);
+        T* o = dst + off;
 #pragma unroll
         for (int e = 0; e < E; ++e) o[e] = (k0 + e < K) ? src[(size_t)i * K + k0 + e] : (T)0;
     }
@@ -1083,18 +1097,19 @@ static unsigned grid_for(size_t n) {
 }
 
 hipError_t launch_tile_weight(int atype, const void* src, int rows, int K, void* dst, int row0, int mode, int hd,
-                              hipStream_t s) {
+                              hipStream_t s, int kt) {
     const int Kp = pad_k(K, atype);
     const size_t n = (size_t)rows * (Kp / frag_elems(atype));
+    if (kt < 0) return hipErrorInvalidValue;
     if (atype == ET_BF16)
         hipLaunchKernelGGL(k_tile_weight<uint16_t>, dim3(grid_for(n)), dim3(256), 0, s, (const uint16_t*)src, rows, K,
-                           Kp, (uint16_t*)dst, row0, mode, hd);
+                           Kp, (uint16_t*)dst, row0, mode, hd, kt);
     else if (atype == ET_F32)
         hipLaunchKernelGGL(k_tile_weight<float>, dim3(grid_for(n)), dim3(256), 0, s, (const float*)src, rows, K, Kp,
-                           (float*)dst, row0, mode, hd);
+                           (float*)dst, row0, mode, hd, kt);
     else
         hipLaunchKernelGGL(k_tile_weight<int8_t>, dim3(grid_for(n)), dim3(256), 0, s, (const int8_t*)src, rows, K, Kp,
-                           (int8_t*)dst, row0, mode, hd);
+                           (int8_t*)dst, row0, mode, hd, kt);
     return hipGetLastError();
 }
 
@@ -2037,20 +2052,29 @@ hipError_t launch_quant_rows(int atype, const void* x, int T, int K, int8_t* q, 
     return hipGetLastError();
 }
 
+// Element offset of W[n][k] in a tiled matrix of element size es and padded
+// width Kp, tile-major or (kmaj) K-major over ntiles tiles.
+__device__ __forceinline__ size_t wt_off_in(int n, int k, int Kp, int E, int es, int kmaj, int ntiles) {
+    const size_t off = wt_off(n, k, Kp, E);
+    return kmaj ? wt_kmajor(off * es, ntiles, Kp * es / 64) / es : off;
+}
+
 // Tiled weights (act type) -> tiled int8 copy with per-row scales, one
 // workgroup per 16-row tile: row amax over the whole row, then the codes.
+// skm / dkm: the source / the copy in the K-major block order.
 template <typename AT>
-__global__ void __launch_bounds__(256) k_quant_weight(const AT* w, int K, int8_t* q, float* qs) {
+__global__ void __launch_bounds__(256) k_quant_weight(const AT* w, int K, int8_t* q, float* qs, int skm, int dkm) {
     __shared__ unsigned amax_bits[16];
     __shared__ float scale[16];
-    constexpr int EA = 16 / sizeof(AT);
-    const int tile = blockIdx.x, n0 = tile * 16;
+    constexpr int EA = 16 / sizeof(AT), ES = sizeof(AT);
+    const int tile = blockIdx.x, n0 = tile * 16, nt = gridDim.x;
     const int Kpa = (K + 16 * EA - 1) / (16 * EA) * (16 * EA), Kpq = (K + 255) / 256 * 256;
     if (threadIdx.x < 16) amax_bits[threadIdx.x] = 0u;
     __syncthreads();
     const int r = threadIdx.x & 15;
     float m = 0.f;
-    for (int k = threadIdx.x >> 4; k < K; k += 16) m = fmaxf(m, fabsf(Act<AT>::ld(w, wt_off(n0 + r, k, Kpa, EA))));
+    for (int k = threadIdx.x >> 4; k < K; k += 16)
+        m = fmaxf(m, fabsf(Act<AT>::ld(w, wt_off_in(n0 + r, k, Kpa, EA, ES, skm, nt))));
     atomicMax(&amax_bits[r], __float_as_uint(m));  // non-negative floats order like their bits
     __syncthreads();
     if (threadIdx.x < 16) {
@@ -2063,17 +2087,19 @@ __global__ void __launch_bounds__(256) k_quant_weight(const AT* w, int K, int8_t
     for (int k = threadIdx.x >> 4; k < Kpq; k += 16) {
         float rq = 0.f;
         if (k < K && sc != 0.f)
-            rq = fminf(fmaxf(rintf(Act<AT>::ld(w, wt_off(n0 + r, k, Kpa, EA)) / sc), -127.f), 127.f);
-        q[wt_off(n0 + r, k, Kpq, 16)] = (int8_t)rq;
+            rq = fminf(fmaxf(rintf(Act<AT>::ld(w, wt_off_in(n0 + r, k, Kpa, EA, ES, skm, nt)) / sc), -127.f), 127.f);
+        q[wt_off_in(n0 + r, k, Kpq, 16, 1, dkm, nt)] = (int8_t)rq;
     }
 }
 
-hipError_t launch_quant_weight(int wtype, const void* w, int N, int K, int8_t* q, float* qs, hipStream_t s) {
+hipError_t launch_quant_weight(int wtype, const void* w, int N, int K, int8_t* q, float* qs, hipStream_t s, int skm,
+                               int dkm) {
     if (N % 16) return hipErrorInvalidValue;
     if (wtype == ET_BF16)
-        hipLaunchKernelGGL(k_quant_weight<uint16_t>, dim3(N / 16), dim3(256), 0, s, (const uint16_t*)w, K, q, qs);
+        hipLaunchKernelGGL(k_quant_weight<uint16_t>, dim3(N / 16), dim3(256), 0, s, (const uint16_t*)w, K, q, qs, skm,
+                           dkm);
     else
-        hipLaunchKernelGGL(k_quant_weight<float>, dim3(N / 16), dim3(256), 0, s, (const float*)w, K, q, qs);
+        hipLaunchKernelGGL(k_quant_weight<float>, dim3(N / 16), dim3(256), 0, s, (const float*)w, K, q, qs, skm, dkm);
     return hipGetLastError();
 }
 
@@ -2106,18 +2132,19 @@ __device__ __forceinline__ void wt4_inv(int b, int c, int& r, int& k) {
 // one workgroup per 16-row tile: row amax over the whole row, then 4 packed
 // bytes per thread and step.
 template <typename AT>
-__global__ void __launch_bounds__(256) k_quant_weight_i4(const AT* w, int K, uint8_t* q, float* qs) {
+__global__ void __launch_bounds__(256) k_quant_weight_i4(const AT* w, int K, uint8_t* q, float* qs, int skm, int dkm) {
     __shared__ unsigned amax_bits[16];
     __shared__ float scale[16];
-    constexpr int EA = 16 / sizeof(AT);
-    const int tile = blockIdx.x, n0 = tile * 16;
+    constexpr int EA = 16 / sizeof(AT), ES = sizeof(AT);
+    const int tile = blockIdx.x, n0 = tile * 16, nt = gridDim.x;
     const int Kpa = (K + 16 * EA - 1) / (16 * EA) * (16 * EA), C = (K + 255) / 256;
     if (threadIdx.x < 16) amax_bits[threadIdx.x] = 0u;
     __syncthreads();
     {
         const int r = threadIdx.x & 15;
         float m = 0.f;
-        for (int k = threadIdx.x >> 4; k < K; k += 16) m = fmaxf(m, fabsf(Act<AT>::ld(w, wt_off(n0 + r, k, Kpa, EA))));
+        for (int k = threadIdx.x >> 4; k < K; k += 16)
+            m = fmaxf(m, fabsf(Act<AT>::ld(w, wt_off_in(n0 + r, k, Kpa, EA, ES, skm, nt))));
         atomicMax(&amax_bits[r], __float_as_uint(m));  // non-negative floats order like their bits
     }
     __syncthreads();
@@ -2127,7 +2154,7 @@ __global__ void __launch_bounds__(256) k_quant_weight_i4(const AT* w, int K, uin
         qs[n0 + threadIdx.x] = sc;
     }
     __syncthreads();
-    uint8_t* qt = q + (size_t)tile * C * 2048;
+    const size_t qt = (size_t)tile * C * 2048;  // the tile's bytes in the tile-major order
     for (int w4 = threadIdx.x; w4 < C * 512; w4 += 256) {
         const int c = w4 >> 9;
         uint32_t word = 0;
@@ -2136,20 +2163,25 @@ __global__ void __launch_bounds__(256) k_quant_weight_i4(const AT* w, int K, uin
             int r, k;
             wt4_inv((w4 & 511) * 4 + i, c, r, k);
             const float sc = scale[r];
-            const float lo = k < K ? qcode(Act<AT>::ld(w, wt_off(n0 + r, k, Kpa, EA)), sc, 7.f) : 0.f;
-            const float hi = k + 8 < K ? qcode(Act<AT>::ld(w, wt_off(n0 + r, k + 8, Kpa, EA)), sc, 7.f) : 0.f;
+            const float lo = k < K ? qcode(Act<AT>::ld(w, wt_off_in(n0 + r, k, Kpa, EA, ES, skm, nt)), sc, 7.f) : 0.f;
+            const float hi =
+                k + 8 < K ? qcode(Act<AT>::ld(w, wt_off_in(n0 + r, k + 8, Kpa, EA, ES, skm, nt)), sc, 7.f) : 0.f;
             word |= (uint32_t)(((int)lo + 8) | (((int)hi + 8) << 4)) << (8 * i);
         }
-        *(uint32_t*)(qt + (size_t)w4 * 4) = word;
+        const size_t b = qt + (size_t)w4 * 4;
+        *(uint32_t*)(q + (dkm ? wt_kmajor(b, nt, C * 2) : b)) = word;
     }
 }
 
-hipError_t launch_quant_weight_i4(int wtype, const void* w, int N, int K, uint8_t* q, float* qs, hipStream_t s) {
+hipError_t launch_quant_weight_i4(int wtype, const void* w, int N, int K, uint8_t* q, float* qs, hipStream_t s,
+                                  int skm, int dkm) {
     if (N % 16 || K < 1) return hipErrorInvalidValue;
     if (wtype == ET_BF16)
-        hipLaunchKernelGGL(k_quant_weight_i4<uint16_t>, dim3(N / 16), dim3(256), 0, s, (const uint16_t*)w, K, q, qs);
+        hipLaunchKernelGGL(k_quant_weight_i4<uint16_t>, dim3(N / 16), dim3(256), 0, s, (const uint16_t*)w, K, q, qs,
+                           skm, dkm);
     else
-        hipLaunchKernelGGL(k_quant_weight_i4<float>, dim3(N / 16), dim3(256), 0, s, (const float*)w, K, q, qs);
+        hipLaunchKernelGGL(k_quant_weight_i4<float>, dim3(N / 16), dim3(256), 0, s, (const float*)w, K, q, qs, skm,
+                           dkm);
     return hipGetLastError();
 }
 

@@ -22,6 +22,14 @@ namespace {
 
 constexpr int kStages = 8;          // pinned upload buffers in flight
 constexpr size_t kMaxGraphs = 64;   // captured forwards kept at once
+// Block order of each layer's projection (QKV, O, gate/up, down) and of its
+// int8 copy: 1 = K-major (wt_kmajor).  The LM head is K-major too; the packed
+// int4 copies stay tile-major.  Measured with cold weights and in the
+// forwards: K-major gate/up 7B T = 32 34.9 -> 34.0 us, 8B one-row verify
+// 1.40 -> 1.19 ms per forward; LM head 7B 50.3 -> 43.6 us.  The O projection
+// gained on the 7B shape (12.6 -> 11.6 us) but lost on the 13B one (445 ->
+// 482 us per forward), and QKV and down lost 3-4%: they stay tile-major.
+constexpr int kProjKMajor[4] = {0, 0, 1, 0};
 constexpr size_t kStageBytes = 4096;
 
 struct LayerW {
@@ -371,6 +379,7 @@ hipError_t enqueue_forward(cas_ctx* c, int T, const uint8_t* skip, int aq) {
         g.out = c->d_q;
         g.gv = gv;
         g.chk = c->d_chk;
+        g.kmaj = aq == 2 ? 0 : kProjKMajor[0];
         g.rope_cos = c->rope_cos;
         g.rope_sin = c->rope_sin;
         g.row_pos = c->d_row_pos;
@@ -412,6 +421,7 @@ hipError_t enqueue_forward(cas_ctx* c, int T, const uint8_t* skip, int aq) {
         go.ws = scopy(w, 1);
         go.out = c->d_h;
         go.ldo = d;
+        go.kmaj = aq == 2 ? 0 : kProjKMajor[1];
         RUN(CAS_K_GEMM_O, resid_proj(go));
         // --- FFN block
         RUN(CAS_K_RMSNORM, norm(w.ffn_norm, aq ? nullptr : c->d_xn, aq ? c->d_xq : nullptr, c->d_xs));
@@ -427,6 +437,7 @@ hipError_t enqueue_forward(cas_ctx* c, int T, const uint8_t* skip, int aq) {
         gu.ldo = ffn;
         gu.out_k = ffn;
         gu.gv = gv;
+        gu.kmaj = aq == 2 ? 0 : kProjKMajor[2];
         RUN(CAS_K_GEMM_GATEUP, launch_gemm(wq, et, EPI_SWIGLU, gu, s));
         if (aq && !qx_d) RUN(CAS_K_QUANT, launch_quant_rows(et, c->d_sw, T, ffn, c->d_xq, c->d_xs, 1, qmax, s));
         GemmArgs gd{};
@@ -441,6 +452,7 @@ hipError_t enqueue_forward(cas_ctx* c, int T, const uint8_t* skip, int aq) {
         gd.ws = scopy(w, 3);
         gd.out = c->d_h;
         gd.ldo = d;
+        gd.kmaj = aq == 2 ? 0 : kProjKMajor[3];
         RUN(CAS_K_GEMM_DOWN, resid_proj(gd));
     }
     RUN(CAS_K_RMSNORM, norm(c->final_norm, c->d_xn, nullptr, nullptr));
@@ -453,6 +465,7 @@ hipError_t enqueue_forward(cas_ctx* c, int T, const uint8_t* skip, int aq) {
     gh.out = c->d_logits;
     gh.ldo = f.vocab;
     gh.gv = gv;
+    gh.kmaj = 1;
     RUN(CAS_K_GEMM_HEAD, launch_gemm(et, et, EPI_STORE, gh, s));
 #undef RUN
     return hipSuccess;
@@ -844,7 +857,10 @@ cas_status cas_load_tensor(cas_ctx* c, int32_t kind, int32_t layer, const void* 
         case CAS_T_W_UP: dst = w->wgu; rows = f.ffn_dim; row0 = 1; mode = 2; break;
         case CAS_T_W_DOWN: dst = w->wd; rows = d; K = f.ffn_dim; break;
         }
-        e = launch_tile_weight(c->et, c->stage_dev, rows, K, dst, row0, mode, hd, c->stream);
+        // the gate/up and LM head matrices are stored in the K-major block order
+        const int kt = (kind == CAS_T_W_GATE || kind == CAS_T_W_UP) && kProjKMajor[2] ? 2 * f.ffn_dim / 16
+                       : kind == CAS_T_LM_HEAD ? f.vocab / 16 : 0;
+        e = launch_tile_weight(c->et, c->stage_dev, rows, K, dst, row0, mode, hd, c->stream, kt);
         if (e == hipSuccess) e = hipStreamSynchronize(c->stream);
     }
     if (e != hipSuccess) return hip_fail(c, e, "weight upload");
@@ -874,7 +890,8 @@ cas_status cas_build_int4(cas_ctx* c) {
                 if (dalloc(c, &w.q4[i], N[i] * KQ[i] / 2) != hipSuccess || dalloc(c, &w.s4[i], N[i] * 4) != hipSuccess)
                     return fail(c, CAS_ERR_OOM, "hipMalloc of the int4 weight copy");
             }
-            hipError_t e = launch_quant_weight_i4(c->et, src[i], (int)N[i], (int)K[i], w.q4[i], w.s4[i], c->stream);
+            hipError_t e = launch_quant_weight_i4(c->et, src[i], (int)N[i], (int)K[i], w.q4[i], w.s4[i], c->stream,
+                                                  kProjKMajor[i], 0);
             if (e != hipSuccess) return hip_fail(c, e, "int4 weight quantisation");
         }
     }
@@ -899,7 +916,8 @@ cas_status cas_build_int8(cas_ctx* c) {
                 if (dalloc(c, &w.q8[i], N[i] * KQ[i]) != hipSuccess || dalloc(c, &w.s8[i], N[i] * 4) != hipSuccess)
                     return fail(c, CAS_ERR_OOM, "hipMalloc of the int8 weight copy");
             }
-            hipError_t e = launch_quant_weight(c->et, src[i], (int)N[i], (int)K[i], w.q8[i], w.s8[i], c->stream);
+            hipError_t e = launch_quant_weight(c->et, src[i], (int)N[i], (int)K[i], w.q8[i], w.s8[i], c->stream,
+                                               kProjKMajor[i], kProjKMajor[i]);
             if (e != hipSuccess) return hip_fail(c, e, "int8 weight quantisation");
         }
     }
