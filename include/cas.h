@@ -237,6 +237,19 @@ cas_status cas_tree_info(const int32_t* tree_parent, int32_t n, int32_t* depth, 
  * or launch kernel by kernel (0). */
 cas_status cas_set_graphs(cas_ctx* ctx, int32_t enable);
 
+/* Draft calls of one row (a skip mask, quantised activations or an attention
+ * window) with bf16 or int8 weights run their wide GEMMs (QKV, gate/up, LM
+ * head) as GEMV-style tiles (1: VALU dot products per lane, summed across
+ * the k-group lanes) or as the MFMA tiles every other call uses (0,
+ * default).  The GEMV tiles stream a little faster (7B 16-layer one-row
+ * draft 1.50 -> 1.48 ms; 8B no change) but sum in another order than the
+ * MFMA tiles: with bf16 weights a one-row draft's logits then differ from
+ * the verify's by rounding even where the draft computes the same function
+ * (a skipped layer that contributes nothing), and a near-tie can pick
+ * another token.  With 0 such a draft gives the verify's bits.  Takes effect
+ * at the next forward. */
+cas_status cas_set_gemv(cas_ctx* ctx, int32_t enable);
+
 /* Per-kernel timing: when enabled, the forward launches kernel by kernel and
  * brackets every launch with HIP events on the context's stream.
  * cas_profile_read sums, for each kernel class (cas_kclass), the elapsed

@@ -48,7 +48,7 @@ EXPORTS = ("cas_create", "cas_destroy", "cas_last_error", "cas_create_error", "c
            "cas_op_attention_work_bytes", "cas_op_copy", "cas_op_rmsnorm", "cas_op_rmsnorm_work_bytes",
            "cas_op_attn_merge", "cas_op_attn_merge_work_bytes", "cas_op_gemm_qx", "cas_op_gemm_qx_splits",
            "cas_op_gemm_qx_work_bytes", "cas_op_attention_noalloc", "cas_op_attention_noalloc_max_bytes",
-           "cas_debug_build", "cas_debug_check", "cas_debug_limit_slots")
+           "cas_debug_build", "cas_debug_check", "cas_debug_limit_slots", "cas_set_gemv")
 # device check codes (cas_debug_check)
 DEVICE_CHECKS = ["none", "tree size", "token id", "parent order", "slot capacity", "RoPE position",
                  "KV write slot", "attention slots", "compaction path", "acceptance parent"]
@@ -104,6 +104,7 @@ def lib(debug: bool = False):
             "cas_topk": ([P, I, I, P, P], I),
             "cas_tree_info": ([P, I, P, P], I),
             "cas_set_graphs": ([P, I], I),
+            "cas_set_gemv": ([P, I], I),
             "cas_profile": ([P, I], I),
             "cas_profile_read": ([P, P, P, I], I),
             "cas_sync": ([P], I),
@@ -310,6 +311,11 @@ class Model:
 
     def set_graphs(self, on: bool) -> None:
         self._chk(self._L.cas_set_graphs(self.h, 1 if on else 0))
+
+    def set_gemv(self, on: bool) -> None:
+        """GEMV-style tiles for one-row drafts (default off: the MFMA tiles,
+        whose rows carry the verify's bits)."""
+        self._chk(self._L.cas_set_gemv(self.h, 1 if on else 0))
 
     def profile(self, on: bool) -> None:
         self._chk(self._L.cas_profile(self.h, 1 if on else 0))

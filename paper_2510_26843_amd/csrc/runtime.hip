@@ -118,6 +118,7 @@ struct cas_ctx {
     int stage_i = 0;
 
     bool graphs = true;
+    bool gemv = false;  // GEMV-style tiles for one-row drafts (cas_set_gemv)
     std::map<std::string, hipGraphExec_t> gcache;
     int win_sink = 0, win_len = 0;  // attention window of the forward being enqueued (0: none)
 
@@ -328,11 +329,12 @@ hipError_t enqueue_forward(cas_ctx* c, int T, const uint8_t* skip, int aq) {
     // and gate/up inputs keep the codes their RMSNorm writes
     const bool qxs = aq && et == ET_BF16;
     // drafts of one row (a layer skipped, quantised activations or an
-    // attention window) take the GEMV-style tiles in the wide GEMMs; verify
-    // calls keep the MFMA form, whose row sums do not depend on the tree size
+    // attention window) take the GEMV-style tiles in the wide GEMMs when the
+    // caller asks for them (cas_set_gemv); verify calls always keep the MFMA
+    // form, whose row sums do not depend on the tree size
     bool skips = false;
     for (int l = 0; skip && l < f.n_layers; ++l) skips = skips || skip[l];
-    const int gv = T == 1 && (skips || aq || c->win_len > 0) ? 1 : 0;
+    const int gv = c->gemv && T == 1 && (skips || aq || c->win_len > 0) ? 1 : 0;
     const int ks_o = gemm_parts_count(wq, d, c->kq_q, T), ks_d = gemm_parts_count(wq, d, c->kq_f, T);
     const bool qx_o = qxs && gemm_qx_ok(wq, d, c->kq_q, T, ks_o);
     const bool qx_d = qxs && gemm_qx_ok(wq, d, c->kq_f, T, ks_d);
@@ -473,6 +475,7 @@ hipError_t enqueue_forward(cas_ctx* c, int T, const uint8_t* skip, int aq) {
 
 std::string graph_key(const cas_ctx* c, int T, const uint8_t* skip, int aq, int S) {
     std::string k = std::to_string(T) + ":" + std::to_string(aq) + ":" + std::to_string(S) + ":" +
+                    (c->gemv ? "g:" : "m:") +
                     std::to_string(c->win_sink) + ":" + std::to_string(c->win_len) + ":";
     for (int l = 0; l < c->cfg.n_layers; ++l) k.push_back(skip && skip[l] ? '1' : '0');
     return k;
@@ -1093,6 +1096,12 @@ cas_status cas_kv_compact(cas_ctx* c, const int32_t* accepted, int32_t n_accepte
 cas_status cas_set_graphs(cas_ctx* c, int32_t enable) {
     if (!c) return CAS_ERR_ARG;
     c->graphs = enable != 0;
+    return CAS_OK;
+}
+
+cas_status cas_set_gemv(cas_ctx* c, int32_t enable) {
+    if (!c) return CAS_ERR_ARG;
+    c->gemv = enable != 0;
     return CAS_OK;
 }
 

@@ -120,6 +120,7 @@ static void host_checks(void) {
     CHECK(cas_committed_len(NULL, &n) == CAS_ERR_ARG);
     CHECK(cas_sync(NULL) == CAS_ERR_ARG);
     CHECK(cas_debug_check(NULL, &n) == CAS_ERR_ARG);
+    CHECK(cas_set_gemv(NULL, 1) == CAS_ERR_ARG);
     CHECK(cas_last_error(NULL) != NULL);
     cas_destroy(NULL);
     CHECK(cas_debug_build() == 0 || cas_debug_build() == 1);
@@ -369,6 +370,8 @@ static void run_model(const shape_t* s) {
             OK(c, cas_set_graphs(c, 0));
         }
         if (r == 60) OK(c, cas_set_graphs(c, 1));
+        if (r == 20) OK(c, cas_set_gemv(c, 1));
+        if (r == 75) OK(c, cas_set_gemv(c, 0));
     }
     free(skip);
     error_paths(c, s);

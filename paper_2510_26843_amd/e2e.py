@@ -136,6 +136,8 @@ def main(argv=None) -> None:
                     help="after timing, locate every CAS/AR divergence and report AR's logit margin there")
     ap.add_argument("--damp-odd", type=float, default=None,
                     help="scale the odd layers' W_o and W_down by this factor (unset: unchanged)")
+    ap.add_argument("--gemv", type=int, choices=(0, 1), default=None,
+                    help="GEMV-style tiles for one-row drafts (default: the library's)")
     ap.add_argument("--out", default="")
     args = ap.parse_args(argv)
     log = lambda *a: print(*a, file=sys.stderr, flush=True)
@@ -154,6 +156,8 @@ def main(argv=None) -> None:
     m.load_weights(w)
     m.build_int8()
     m.build_int4()
+    if args.gemv is not None:
+        m.set_gemv(bool(args.gemv))
     del w
     log(f"[e2e] {args.shape} loaded with its int8 and int4 copies in {time.perf_counter() - t0:.1f} s")
     prompt = [int(x) for x in synth.gen_prompt(shape.vocab, args.prompt, seed=1)]
@@ -207,7 +211,7 @@ def main(argv=None) -> None:
         "expansions": stats.get("expansions", {}), "alpha_final": {k: round(v, 4) for k, v in est.a.items()},
         "c_hat": {k: round(v, 4) for k, v in cost.items()}, "latency_model_rms_ms": round(cal["rms_residual_ms"], 4),
         "params": vars(params),
-        "damp_odd": args.damp_odd, "prior": prior, "ties": ties,
+        "damp_odd": args.damp_odd, "gemv": args.gemv, "prior": prior, "ties": ties,
         "data": ("synthetic: random N(0,0.02^2) bf16 weights" +
                  (f", odd layers' W_o and W_down scaled by {args.damp_odd}" if args.damp_odd is not None else "") +
                  ", uniform-random prompt"),
