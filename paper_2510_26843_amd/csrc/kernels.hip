@@ -1330,10 +1330,22 @@ __device__ __forceinline__ void attn_merge_o(f32x4& acc, const f32x4 o, float f)
 }
 __device__ __forceinline__ void attn_merge_l(float& L, float l, float f) { L = fmaf(l, f, L); }
 
+// Query rows of a kv head: its G query heads x T tokens, each head's rows
+// padded to Rp and packed into 16-row tiles, row p = 16 tile + r holding
+// token p % Rp of head p / Rp of the group.  Up to 8 tokens Rp is a power of
+// two, so 16 / Rp heads share a tile (a one-node call of a 4-head group fills
+// one tile instead of four, and the group's K/V pass serves every head);
+// above, Rp rounds T up to 16.  A row's arithmetic does not depend on where
+// it sits in its tile.
+__host__ __device__ inline int attn_head_rows(int T) {
+    return T <= 8 ? (T <= 1 ? 1 : T <= 2 ? 2 : T <= 4 ? 4 : 8) : (T + 15) & ~15;
+}
+__host__ __device__ inline int attn_query_tiles(int T, int G) { return (G * attn_head_rows(T) + 15) / 16; }
+
 // Workgroup = (split of KV slots, kv head, JT query tiles of 16 rows); each
 // of the four waves owns one part (two key tiles) of the split.  The query
-// rows of a kv head are its G query heads x T tokens (each head padded to a
-// multiple of 16 rows), so GQA groups share every K/V fragment.  Scores come
+// rows of a kv head are its G query heads x T tokens, packed into tiles as
+// attn_head_rows describes, so GQA groups share every K/V fragment.  Scores come
 // out of the QK^T MFMA with slots along the row index; the cache puts slots
 // 8g..8g+7 of a tile in lane group g, which is exactly the k-order of the P
 // operand of the PV MFMA, so probabilities never leave registers.  Each wave
@@ -1358,26 +1370,23 @@ __global__ void __launch_bounds__(256) k_attn_bf16(const AttnArgs a, float scale
     if (!dcheck(a.chk, Lc >= 0 && n_slots <= a.sp->cap && a.sp->cap <= a.ctx_cap, CHK_ATTN_SLOTS)) return;
     const int n_tiles = (n_slots + 31) >> 5;
     const AttnWindow win(Lc, n_tree, a.win_sink, a.win_len);
-    const int T = a.T, Tp = (T + 15) & ~15, G = a.H / a.Hkv;
-    const int nct = G * Tp / 16;
+    const int T = a.T, G = a.H / a.Hkv, Rp = attn_head_rows(T);
+    const int nct = attn_query_tiles(T, G);
     const uint16_t* q = (const uint16_t*)a.q;
 
-    // query fragments of the two 16-row column tiles (rows past T read row
-    // T-1 and are zeroed below, so every load is unconditional)
-    bool tv[JT];
-    int head[JT], t0[JT];
+    // query fragments of the JT 16-row tiles; lane row r is row 16 ct + r of
+    // the kv head's packed rows (rows past the group's read a valid row and
+    // are zeroed below, so every load is unconditional)
+    bool rv[JT];
     i32x4 Qf[JT][UD];
     uint64_t an0[JT], an1[JT];
 #pragma unroll
     for (int j = 0; j < JT; ++j) {
-        const int ct = JT * rc + j;
-        tv[j] = ct < nct;
-        const int hg = tv[j] ? (ct * 16) / Tp : 0;
-        t0[j] = (ct * 16) % Tp;
-        head[j] = kvh * G + hg;
-        const int t = min(t0[j] + r, T - 1);
+        const int ct = JT * rc + j, p = ct * 16 + r, hg = p / Rp, tr = p % Rp;
+        rv[j] = ct < nct && hg < G && tr < T;
+        const int t = min(tr, T - 1), head = kvh * G + min(hg, G - 1);
 #pragma unroll
-        for (int u = 0; u < UD; ++u) Qf[j][u] = *(const i32x4*)(q + ((size_t)t * a.H + head[j]) * HD + g * DG + u * 8);
+        for (int u = 0; u < UD; ++u) Qf[j][u] = *(const i32x4*)(q + ((size_t)t * a.H + head) * HD + g * DG + u * 8);
         an0[j] = a.anc[2 * t];
         an1[j] = a.anc[2 * t + 1];
     }
@@ -1403,7 +1412,7 @@ __global__ void __launch_bounds__(256) k_attn_bf16(const AttnArgs a, float scale
     const i32x4 zero = {0, 0, 0, 0};
 #pragma unroll
     for (int j = 0; j < JT; ++j) {
-        if (!(tv[j] && t0[j] + r < T)) {
+        if (!rv[j]) {
 #pragma unroll
             for (int u = 0; u < UD; ++u) Qf[j][u] = zero;
             an0[j] = an1[j] = 0ull;
@@ -1468,8 +1477,8 @@ __global__ void __launch_bounds__(256) k_attn_bf16(const AttnArgs a, float scale
     constexpr int D4 = HD / 4;
     for (int idx = threadIdx.x; idx < JT * 16 * D4; idx += 64 * ATT_WAVES) {
         const int j = idx / (16 * D4), rr = (idx / D4) & 15, d4 = (idx % D4) * 4;
-        const int t = t0[JT == 1 ? 0 : j] + rr;
-        if (!tv[JT == 1 ? 0 : j] || t >= T) continue;
+        const int ct = JT * rc + j, p = ct * 16 + rr, hg = p / Rp, t = p % Rp;
+        if (ct >= nct || hg >= G || t >= T) continue;
         float mw[ATT_WAVES], M = -1e30f;
 #pragma unroll
         for (int w = 0; w < ATT_WAVES; ++w) {
@@ -1484,7 +1493,7 @@ __global__ void __launch_bounds__(256) k_attn_bf16(const AttnArgs a, float scale
             attn_merge_o(acc, *(const f32x4*)(&sm_o[w][j][rr][d4]), f);
             attn_merge_l(L, sm_l[w][j][rr], f);
         }
-        const size_t o = ((size_t)split * a.H + head[JT == 1 ? 0 : j]) * T + t;
+        const size_t o = ((size_t)split * a.H + kvh * G + hg) * T + t;
         *(f32x4*)(a.part_o + o * HD + d4) = acc;
         if (d4 == 0) *(float2*)(a.part_ml + o * 2) = make_float2(M, L);
     }
@@ -1762,17 +1771,17 @@ hipError_t launch_attention(int atype, const AttnArgs& a, hipStream_t s) {
     }
     const int S = attention_splits_win(a.Lc_host, a.n_tree_host, a.win_sink, a.win_len);
     const int G = a.H / a.Hkv, Tp = (a.T + 15) & ~15;
-    const int nct = G * Tp / 16;  // 16-row query tiles per kv head
+    const int nct = attn_query_tiles(a.T, G);  // 16-row query tiles per kv head
     if (a.ctx_cap % 32 || S > ATT_MAX_SPLITS) return hipErrorInvalidValue;
     const float scale_log2 = (1.0f / sqrtf((float)a.hd)) * 1.4426950408889634f;
     // Several query tiles per kv head, each head with at least 32 rows:
     // four tiles per workgroup share one pass of the split's K/V through LDS
     // (k_attn_rows; per layer, 8B 64 nodes at 4096: 27.7 -> 23.3 us, 7B 128
     // nodes at 8192: 112 -> 65 us).
-    // A single-token call of a grouped-query model has four tiles of one row
-    // each and keeps the larger grid of k_attn_bf16 (8B one node at 4096:
-    // 3.80 ms per forward against 3.91 with k_attn_rows).  Both kernels give
-    // the same bits for a row.  Otherwise the split's
+    // Calls of up to 8 tokens pack the grouped heads' rows into shared tiles
+    // (attn_head_rows; 8B one node at 4096: attention 9.6 -> 6.8 us per
+    // layer against one tile of one row per head) and take k_attn_bf16.
+    // Both kernels give the same bits for a row.  Otherwise the split's
     // key tiles spread over four waves (k_attn_bf16), one 16-row tile per
     // workgroup unless the grid of (split, kv head, tile) units is large; then
     // two tiles share each K/V load (7B 32 nodes at 8192: fewer, longer
