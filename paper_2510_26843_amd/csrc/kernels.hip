@@ -1332,14 +1332,12 @@ __device__ __forceinline__ void attn_merge_l(float& L, float l, float f) { L = f
 
 // Query rows of a kv head: its G query heads x T tokens, each head's rows
 // padded to Rp and packed into 16-row tiles, row p = 16 tile + r holding
-// token p % Rp of head p / Rp of the group.  Up to 8 tokens Rp is a power of
-// two, so 16 / Rp heads share a tile (a one-node call of a 4-head group fills
-// one tile instead of four, and the group's K/V pass serves every head);
-// above, Rp rounds T up to 16.  A row's arithmetic does not depend on where
-// it sits in its tile.
-__host__ __device__ inline int attn_head_rows(int T) {
-    return T <= 8 ? (T <= 1 ? 1 : T <= 2 ? 2 : T <= 4 ? 4 : 8) : (T + 15) & ~15;
-}
+// token p % Rp of head p / Rp of the group.  Up to 16 tokens Rp = T, so the
+// heads' rows follow each other (a one-node call of a 4-head group fills one
+// tile instead of four, and the group's K/V pass serves every head; a head's
+// rows may straddle two tiles); above, Rp rounds T up to 16.  A row's
+// arithmetic does not depend on where it sits in its tile.
+__host__ __device__ inline int attn_head_rows(int T) { return T <= 16 ? T : (T + 15) & ~15; }
 __host__ __device__ inline int attn_query_tiles(int T, int G) { return (G * attn_head_rows(T) + 15) / 16; }
 
 // Workgroup = (split of KV slots, kv head, JT query tiles of 16 rows); each
@@ -1762,6 +1760,7 @@ hipError_t launch_attn_merge(const AttnArgs& a, int S, hipStream_t s) {
 }
 
 hipError_t launch_attention(int atype, const AttnArgs& a, hipStream_t s) {
+    if (a.T < 1 || a.T > 128 || a.Hkv < 1 || a.H % a.Hkv) return hipErrorInvalidValue;
     const int n_slots = a.Lc_host + a.n_tree_host;
     if (atype == ET_F32) {
         if (a.ctx_cap > 4096) return hipErrorInvalidValue;
@@ -1778,7 +1777,7 @@ hipError_t launch_attention(int atype, const AttnArgs& a, hipStream_t s) {
     // four tiles per workgroup share one pass of the split's K/V through LDS
     // (k_attn_rows; per layer, 8B 64 nodes at 4096: 27.7 -> 23.3 us, 7B 128
     // nodes at 8192: 112 -> 65 us).
-    // Calls of up to 8 tokens pack the grouped heads' rows into shared tiles
+    // Calls of up to 16 tokens pack the grouped heads' rows into shared tiles
     // (attn_head_rows; 8B one node at 4096: attention 9.6 -> 6.8 us per
     // layer against one tile of one row per head) and take k_attn_bf16.
     // Both kernels give the same bits for a row.  Otherwise the split's
