@@ -244,6 +244,13 @@ def _attention_case(H, Hkv, hd, Lc, parents, seed):
     (16, 16, 128, 3000, ((2,) * 7, 128)),
     (16, 16, 128, 7000, ((2,) * 7, 40)),
     (32, 32, 64, 2500, ((2,) * 7, 64)),
+    # grouped heads packed into shared query tiles (calls of up to 16 tokens):
+    # the 8B layout at one and four tokens (one tile per kv head), seven
+    # tokens (two tiles, a head's rows straddling them) and an 8-head group
+    (32, 8, 128, 4000, ((), 1)),
+    (32, 8, 128, 1500, ((3,), 4)),
+    (8, 2, 128, 600, ((2, 2), 7)),
+    (16, 2, 64, 200, ((2, 2), 5)),
 ])
 def test_attention_tree_mask(H, Hkv, hd, Lc, tree):
     parents = synth.tree_from_branching(*tree) if tree[0] else [-1]
