@@ -1504,17 +1504,26 @@ __global__ void __launch_bounds__(256) k_attn_bf16(const AttnArgs a, float scale
 // Each wave computes, for its rows, the same four part states (two key tiles
 // each) as k_attn_bf16's four waves, with the same helpers, and merges them in
 // part order in registers: the partials are the same bits either way, so the
-// choice between the two kernels never changes a row's result.
-template <int HD, int QT>
-__global__ void __launch_bounds__(64 * QT, 2) k_attn_rows(const AttnArgs a, float scale_log2) {
+// choice between the two kernels never changes a row's result.  NH = 1:
+// the split's K and then its V pass through a 64 KB LDS stage, all loads
+// issued up front (two workgroups per CU).  NH = 2: they pass in halves (the
+// K of parts 0-1, then of parts 2-3, then their V the same way), so a
+// workgroup holds half the LDS and staging registers and three fit on a CU;
+// grids of more than one workgroup per CU take it (8B 64 nodes at 4096, 544
+// workgroups: 30.6 -> 26.4 us per layer; 7B 48-128 nodes at 8192 2-5%
+// faster), smaller grids keep the single stage (7B 128 nodes at 512, 192
+// workgroups: 16.4 against 17.4 us).
+template <int HD, int QT, int NH>
+__global__ void __launch_bounds__(64 * QT, NH == 1 ? 2 : 3) k_attn_rows(const AttnArgs a, float scale_log2) {
     constexpr int UD = HD / 32, DG = HD / 4, NDT = HD / 16, TE = 32 * HD;
     constexpr int NP = ATT_WAVES;        // part states per split
     constexpr int NTS = NP * ATT_TPW;    // key tiles per split
+    constexpr int NTH = NTS / NH;        // key tiles per stage
     constexpr int KF = 2 * UD;           // 1 KB fragments per K tile (V: NDT)
-    constexpr int FS = NTS * KF;         // fragments per split, K and V alike
-    constexpr int LPT = FS / QT;         // fragments each wave stages
-    static_assert(KF == NDT && FS % QT == 0, "K and V tiles must stage alike");
-    __shared__ i32x4 kv[FS * 64];        // the split's K, then its V (64 KB for head_dim 128)
+    constexpr int FH = NTH * KF;         // fragments per stage, K and V alike
+    constexpr int LPH = FH / QT;         // fragments each wave stages per stage
+    static_assert(KF == NDT && FH % QT == 0 && NP % NH == 0 && (NH == 1 || NH == 2), "K and V stages must match");
+    __shared__ i32x4 kv[FH * 64];        // one stage of the split's K or V (NH 1: 64 KB for head_dim 128)
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int r = lane & 15, g = lane >> 4;
     const int split = blockIdx.x, kvh = blockIdx.y;
@@ -1542,45 +1551,61 @@ __global__ void __launch_bounds__(64 * QT, 2) k_attn_rows(const AttnArgs a, floa
         live[tt] = split * NTS + tt < win.n_log;
         ptile[tt] = live[tt] ? win.phys(split * NTS + tt) : n_tiles - 1;
     }
-    // stage: every wave loads LPT of the split's K fragments and LPT of its V
-    // fragments (1 KB each, one per lane-wide load); K goes to LDS first
+    // every wave stages LPH of each stage's 1 KB fragments (one lane-wide
+    // load each): fragment f of stage h is fragment h * FH + f of the split
     const uint16_t* kbase = (const uint16_t*)a.kc + (size_t)kvh * a.ctx_cap * HD + lane * 8;
     const uint16_t* vbase = (const uint16_t*)a.vt + (size_t)kvh * a.ctx_cap * HD + lane * 8;
-    i32x4 Ks[LPT], Vs[LPT];
+    // (the physical tile of a fragment computed, not looked up: a run-time
+    // index into ptile would move that array to LDS)
+    auto phys = [&](int tt) { return split * NTS + tt < win.n_log ? win.phys(split * NTS + tt) : n_tiles - 1; };
+    auto kfrag = [&](int h, int i) -> const i32x4* {
+        const int f = h * FH + wave * LPH + i;
+        return (const i32x4*)(kbase + (size_t)phys(f / KF) * TE + (f % KF) * 512);
+    };
+    auto vfrag = [&](int h, int i) -> const i32x4* {
+        const int f = h * FH + wave * LPH + i;
+        return (const i32x4*)(vbase + (size_t)phys(f / NDT) * TE + (f % NDT) * 512);
+    };
+    // NH 2: K halves 0 and 1 (later V halves 0 and 1); NH 1: K and V
+    i32x4 St0[LPH], St1[LPH];
 #pragma unroll
-    for (int i = 0; i < LPT; ++i) {
-        const int f = wave * LPT + i;
-        Ks[i] = *(const i32x4*)(kbase + (size_t)ptile[f / KF] * TE + (f % KF) * 512);
-    }
+    for (int i = 0; i < LPH; ++i) St0[i] = *kfrag(0, i);
 #pragma unroll
-    for (int i = 0; i < LPT; ++i) {
-        const int f = wave * LPT + i;
-        Vs[i] = *(const i32x4*)(vbase + (size_t)ptile[f / NDT] * TE + (f % NDT) * 512);
-    }
+    for (int i = 0; i < LPH; ++i) St1[i] = NH == 2 ? *kfrag(1, i) : *vfrag(0, i);
     uint64_t an0 = a.anc[2 * min(t0 + r, T - 1)], an1 = a.anc[2 * min(t0 + r, T - 1) + 1];
     if (!(tv && t0 + r < T)) {
 #pragma unroll
         for (int u = 0; u < UD; ++u) Qf[u] = i32x4{0, 0, 0, 0};
         an0 = an1 = 0ull;
     }
-#pragma unroll
-    for (int i = 0; i < LPT; ++i) kv[(wave * LPT + i) * 64 + lane] = Ks[i];
-    __syncthreads();
 
+    // scores of the split's tiles, stage by stage
     f32x4 S[NP][ATT_TPW][2];
 #pragma unroll
-    for (int tt = 0; tt < NTS; ++tt)
+    for (int h = 0; h < NH; ++h) {
+        if (h) __syncthreads();  // every wave is done with the first half
 #pragma unroll
-        for (int h2 = 0; h2 < 2; ++h2) {
-            f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+        for (int i = 0; i < LPH; ++i) kv[(wave * LPH + i) * 64 + lane] = h ? St1[i] : St0[i];
+        __syncthreads();
 #pragma unroll
-            for (int u = 0; u < UD; ++u) acc = mfma_step<ET_BF16>(kv[(tt * KF + h2 * UD + u) * 64 + lane], Qf[u], acc);
-            S[tt / ATT_TPW][tt % ATT_TPW][h2] = acc;
+        for (int th = 0; th < NTH; ++th) {
+            const int tt = h * NTH + th;
+#pragma unroll
+            for (int h2 = 0; h2 < 2; ++h2) {
+                f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                for (int u = 0; u < UD; ++u) acc = mfma_step<ET_BF16>(kv[(th * KF + h2 * UD + u) * 64 + lane], Qf[u], acc);
+                S[tt / ATT_TPW][tt % ATT_TPW][h2] = acc;
+            }
+            // one tile's fragments in registers at a time (three waves per SIMD)
+            if constexpr (NH == 2) __builtin_amdgcn_sched_barrier(0);
         }
-    __syncthreads();
+    }
+    if constexpr (NH == 2) {
+        // the first half of V, in flight while the scores are scaled and masked
 #pragma unroll
-    for (int i = 0; i < LPT; ++i) kv[(wave * LPT + i) * 64 + lane] = Vs[i];
-    __syncthreads();
+        for (int i = 0; i < LPH; ++i) St0[i] = *vfrag(0, i);
+    }
 
     // the parts' scaled, masked scores and maxima first (the merge weights
     // need the maximum over parts), then part by part: probabilities, P V,
@@ -1598,22 +1623,36 @@ __global__ void __launch_bounds__(64 * QT, 2) k_attn_rows(const AttnArgs a, floa
 #pragma unroll
     for (int dt = 0; dt < NDT; ++dt) acc[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int p = 0; p < NP; ++p) {
-        i32x4 Pf[ATT_TPW], Pl[ATT_TPW];
-        const float lp = attn_part_probs<ATT_TPW>(x[p], m[p], Pf, Pl);
-        const float f = attn_merge_weight(m[p], M);
+    for (int h = 0; h < NH; ++h) {
+        __syncthreads();  // every wave is done with the LDS stage it read last
 #pragma unroll
-        for (int dt = 0; dt < NDT; ++dt) {
-            f32x4 o = {0.f, 0.f, 0.f, 0.f};
+        for (int i = 0; i < LPH; ++i) kv[(wave * LPH + i) * 64 + lane] = NH == 1 || h ? St1[i] : St0[i];
+        __syncthreads();
+        if (NH == 2 && h == 0) {
+            // the second half of V, in flight during the first half's P V
 #pragma unroll
-            for (int tt = 0; tt < ATT_TPW; ++tt) {
-                const i32x4 v = kv[((p * ATT_TPW + tt) * NDT + dt) * 64 + lane];
-                o = mfma_step<ET_BF16>(v, Pf[tt], o);
-                o = mfma_step<ET_BF16>(v, Pl[tt], o);
-            }
-            attn_merge_o(acc[dt], o, f);
+            for (int i = 0; i < LPH; ++i) St1[i] = *vfrag(1, i);
         }
-        attn_merge_l(L, lp, f);
+#pragma unroll
+        for (int ph = 0; ph < NP / NH; ++ph) {
+            const int p = h * (NP / NH) + ph;
+            i32x4 Pf[ATT_TPW], Pl[ATT_TPW];
+            const float lp = attn_part_probs<ATT_TPW>(x[p], m[p], Pf, Pl);
+            const float f = attn_merge_weight(m[p], M);
+#pragma unroll
+            for (int dt = 0; dt < NDT; ++dt) {
+                f32x4 o = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                for (int tt = 0; tt < ATT_TPW; ++tt) {
+                    const i32x4 v = kv[((ph * ATT_TPW + tt) * NDT + dt) * 64 + lane];
+                    o = mfma_step<ET_BF16>(v, Pf[tt], o);
+                    o = mfma_step<ET_BF16>(v, Pl[tt], o);
+                }
+                attn_merge_o(acc[dt], o, f);
+                if constexpr (NH == 2) __builtin_amdgcn_sched_barrier(0);
+            }
+            attn_merge_l(L, lp, f);
+        }
     }
     const int t = t0 + r;
     if (tv && t < T) {
@@ -1792,15 +1831,19 @@ hipError_t launch_attention(int atype, const AttnArgs& a, hipStream_t s) {
     // without; 7B 64 nodes at 1024: 4.03 and 3.94 ms).
     const bool rows = (nct >= 5 || (nct >= 3 && (long)S * a.Hkv * nct >= 2048)) && Tp >= 32;
     const int JT = (G == 1 && S * a.Hkv * nct >= 1024) ? 2 : 1;
+    const dim3 rg(S, a.Hkv, (nct + 3) / 4);
+    const bool half = (long)S * a.Hkv * ((nct + 3) / 4) > 256;  // k_attn_rows stages in halves
     const int nrc = (nct + JT - 1) / JT;
     if (a.no_merge && a.qout) return hipErrorInvalidValue;
     if (!a.no_merge && !attn_merge_ok(a)) return hipErrorInvalidValue;
     if (a.hd == 128) {
-        if (rows) hipLaunchKernelGGL((k_attn_rows<128, 4>), dim3(S, a.Hkv, (nct + 3) / 4), dim3(256), 0, s, a, scale_log2);
+        if (rows && half) hipLaunchKernelGGL((k_attn_rows<128, 4, 2>), rg, dim3(256), 0, s, a, scale_log2);
+        else if (rows) hipLaunchKernelGGL((k_attn_rows<128, 4, 1>), rg, dim3(256), 0, s, a, scale_log2);
         else if (JT == 2) hipLaunchKernelGGL((k_attn_bf16<128, 2>), dim3(S, a.Hkv, nrc), dim3(256), 0, s, a, scale_log2);
         else hipLaunchKernelGGL((k_attn_bf16<128, 1>), dim3(S, a.Hkv, nrc), dim3(256), 0, s, a, scale_log2);
     } else if (a.hd == 64) {
-        if (rows) hipLaunchKernelGGL((k_attn_rows<64, 4>), dim3(S, a.Hkv, (nct + 3) / 4), dim3(256), 0, s, a, scale_log2);
+        if (rows && half) hipLaunchKernelGGL((k_attn_rows<64, 4, 2>), rg, dim3(256), 0, s, a, scale_log2);
+        else if (rows) hipLaunchKernelGGL((k_attn_rows<64, 4, 1>), rg, dim3(256), 0, s, a, scale_log2);
         else if (JT == 2) hipLaunchKernelGGL((k_attn_bf16<64, 2>), dim3(S, a.Hkv, nrc), dim3(256), 0, s, a, scale_log2);
         else hipLaunchKernelGGL((k_attn_bf16<64, 1>), dim3(S, a.Hkv, nrc), dim3(256), 0, s, a, scale_log2);
     } else {
