@@ -1825,11 +1825,13 @@ hipError_t launch_attention(int atype, const AttnArgs& a, hipStream_t s) {
     // two tiles share each K/V load (7B 32 nodes at 8192: fewer, longer
     // workgroups halve the per-CU key traffic).
     // With three or four tiles per kv head the shared pass pays only when the
-    // per-tile grid is large (7B 48 nodes at 8192: 5.22 -> 4.94 ms, 13B 64
-    // nodes at 4096: 7.13 -> 6.97 ms); below about 2048 tile workgroups the
-    // larger grid wins (13B 64 nodes at 2048: 6.51 ms with k_attn_rows, 6.46
-    // without; 7B 64 nodes at 1024: 4.03 and 3.94 ms).
-    const bool rows = (nct >= 5 || (nct >= 3 && (long)S * a.Hkv * nct >= 2048)) && Tp >= 32;
+    // per-tile grid is large: from about 1024 tile workgroups (13B 64 nodes at
+    // 2048, 1440 of them: 6.33 ms with k_attn_rows, 6.36 without; 7B 64 nodes
+    // at 2048, 1152: 4.10 and 4.13 ms; 7B 48 nodes at 8192: 5.22 -> 4.94 ms
+    // with the single-stage form); below, the larger grid wins (7B 48 nodes at
+    // 2048, 864: 4.00 ms with k_attn_rows, 3.98 without; 7B 64 nodes at 1024,
+    // 640: 3.93 and 3.90 ms; at 512: 3.84 and 3.74 ms).
+    const bool rows = (nct >= 5 || (nct >= 3 && (long)S * a.Hkv * nct >= 1024)) && Tp >= 32;
     const int JT = (G == 1 && S * a.Hkv * nct >= 1024) ? 2 : 1;
     const dim3 rg(S, a.Hkv, (nct + 3) / 4);
     const bool half = (long)S * a.Hkv * ((nct + 3) / 4) > 256;  // k_attn_rows stages in halves
