@@ -1895,6 +1895,7 @@ hipError_t launch_kv_convert(int atype, void* kc, void* vt, const void* k_rows, 
 // One workgroup of 16 waves per row: the loads of a row spread over the
 // whole CU (measured faster than 4 waves once split-K partials are folded in).
 static constexpr int NORM_THREADS = 1024;
+static constexpr int NORM_MAXP = 8;  // split-K partial sums a norm folds in (launch_gemm_parts allows 8)
 static constexpr int NORM_MAXV = 4;  // float4 per thread: rows up to 16384 elements
 
 // RMSNorm of one row of the residual stream, written as tiled activations
@@ -1919,21 +1920,45 @@ __global__ void __launch_bounds__(NORM_THREADS) k_rmsnorm(float* h, const float*
         gv[i] = *(const float4*)(gain + kc);
     }
     if (nparts > 0) {
+        // rows of up to 8192 elements: every split's loads issue before the
+        // first add (a loop over the splits waited for each split's loads in
+        // turn), then the sums run in split order; longer rows keep the loop
+        // (the registers of all splits would not fit)
         float4 ps[NV];
         const float* pr = parts + (size_t)t * d;
 #pragma unroll
         for (int i = 0; i < NV; ++i) ps[i] = *(const float4*)(pr + min((tid + NORM_THREADS * i) * 4, d - 4));
-        for (int p = 1; p < nparts; ++p) {
-            float4 pp[NV];
+        if constexpr (NV <= 2) {
+            float4 pp[NORM_MAXP - 1][NV];
 #pragma unroll
-            for (int i = 0; i < NV; ++i)
-                pp[i] = *(const float4*)(pr + p * pstride + min((tid + NORM_THREADS * i) * 4, d - 4));
+            for (int p = 1; p < NORM_MAXP; ++p)
+                if (p < nparts)
 #pragma unroll
-            for (int i = 0; i < NV; ++i) {
-                ps[i].x += pp[i].x;
-                ps[i].y += pp[i].y;
-                ps[i].z += pp[i].z;
-                ps[i].w += pp[i].w;
+                    for (int i = 0; i < NV; ++i)
+                        pp[p - 1][i] = *(const float4*)(pr + p * pstride + min((tid + NORM_THREADS * i) * 4, d - 4));
+#pragma unroll
+            for (int p = 1; p < NORM_MAXP; ++p)
+                if (p < nparts)
+#pragma unroll
+                    for (int i = 0; i < NV; ++i) {
+                        ps[i].x += pp[p - 1][i].x;
+                        ps[i].y += pp[p - 1][i].y;
+                        ps[i].z += pp[p - 1][i].z;
+                        ps[i].w += pp[p - 1][i].w;
+                    }
+        } else {
+            for (int p = 1; p < nparts; ++p) {
+                float4 pp[NV];
+#pragma unroll
+                for (int i = 0; i < NV; ++i)
+                    pp[i] = *(const float4*)(pr + p * pstride + min((tid + NORM_THREADS * i) * 4, d - 4));
+#pragma unroll
+                for (int i = 0; i < NV; ++i) {
+                    ps[i].x += pp[i].x;
+                    ps[i].y += pp[i].y;
+                    ps[i].z += pp[i].z;
+                    ps[i].w += pp[i].w;
+                }
             }
         }
 #pragma unroll
@@ -2004,8 +2029,8 @@ static hipError_t rmsnorm_go(float* h, const float* g, int T, int d, float eps, 
 
 hipError_t launch_rmsnorm(int atype, float* h, const float* g, int T, int d, float eps, void* out, int8_t* q,
                           float* qs, const float* parts, int nparts, size_t pstride, int qmax, hipStream_t s) {
-    if (d > 4 * NORM_THREADS * NORM_MAXV || d % 16 || nparts < 0 || (nparts > 0 && (!parts || pstride < (size_t)T * d)) ||
-        (q && qmax != 127 && qmax != 7))
+    if (d > 4 * NORM_THREADS * NORM_MAXV || d % 16 || nparts < 0 || nparts > NORM_MAXP ||
+        (nparts > 0 && (!parts || pstride < (size_t)T * d)) || (q && qmax != 127 && qmax != 7))
         return hipErrorInvalidValue;
     const float qm = (float)qmax;
     if (atype == ET_BF16) {
