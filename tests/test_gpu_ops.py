@@ -239,6 +239,10 @@ def _attention_case(H, Hkv, hd, Lc, parents, seed):
     # workgroup of each head group with one), and an MHA 128-node tree
     (32, 8, 128, 2000, ((4, 4, 4, 4), 64)),
     (8, 8, 128, 3000, ((2,) * 7, 128)),
+    # grids of at most 256 such workgroups stage a whole split at once: a
+    # 64-wide head (MHA, 128 nodes, 3 splits) and a 4:1 group (64 nodes, 2 splits)
+    (8, 8, 64, 500, ((2,) * 7, 128)),
+    (8, 2, 128, 400, ((2,) * 6, 64)),
     # two query tiles per workgroup (large grids of MHA heads): an even and an
     # odd tile count (the last workgroup of each head then has one tile)
     (16, 16, 128, 3000, ((2,) * 7, 128)),
