@@ -519,8 +519,12 @@ static constexpr int MX_MAX_T = 2;
 // shapes at one row: gate/up 28.7 -> 27.9 us, LM head 42.8 -> 39.4 us.  The
 // sums are in a different order than the MFMA's, so verify calls (whose rows
 // must not depend on the tree size) keep the MFMA form.
+// EV: one-tile waves, and the grid splits the N/16 tiles as evenly as it can
+// (workgroup i takes tiles floor(i n / G) .. floor((i + 1) n / G), at most
+// WAVES of them); a wave past its workgroup's share repeats the share's last
+// tile (those loads hit the cache) and stores nothing.
 template <int WT, int NT, int UC, int D, int WAVES, int TPW, int EPI, typename AT, bool RX, bool QX = false,
-          bool MX = false, bool GV = false, bool KM = false>
+          bool MX = false, bool GV = false, bool KM = false, bool EV = false>
 __global__ void __launch_bounds__(64 * WAVES) k_gemm_wide(const GemmArgs a) {
     using Tr = WTr<WT>;
     using ACC = typename Tr::acc_t;
@@ -540,7 +544,15 @@ __global__ void __launch_bounds__(64 * WAVES) k_gemm_wide(const GemmArgs a) {
     extern __shared__ __attribute__((aligned(16))) char xr[];  // RX: T rows of the K range
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-    const int tile0 = (blockIdx.x * WAVES + wave) * TPW;
+    static_assert(!EV || (TPW == 1 && !RX && !GV), "even split: one-tile waves of the ringed loop");
+    int tile0 = (blockIdx.x * WAVES + wave) * TPW;
+    bool wact = true;
+    if constexpr (EV) {
+        const unsigned ntl = (unsigned)a.N >> 4;
+        const int wg0 = (int)((blockIdx.x * ntl) / gridDim.x), wg1 = (int)(((blockIdx.x + 1) * ntl) / gridDim.x);
+        wact = wg0 + wave < wg1;
+        tile0 = min(wg0 + wave, wg1 - 1);
+    }
     const int C = a.Kp / (16 * E);
     // stages of this workgroup: the whole K range, or split gridDim.y ways at
     // chunk boundaries, so the K ranges (and every row's summation order) do
@@ -752,6 +764,9 @@ __global__ void __launch_bounds__(64 * WAVES) k_gemm_wide(const GemmArgs a) {
     }
     GemmArgs ae = a;
     if constexpr (QX) ae.xs = qsc;  // the scales this workgroup derived
+    if constexpr (EV) {
+        if (!wact) return;
+    }
     if (gridDim.y == 1) {
 #pragma unroll
         for (int t = 0; t < TPW; ++t) gemm_epilogue<WT, NT, EPI, AT>(ae, acc[t], tile0 + t, a.N / 16 - 1, lane, qp[t]);
@@ -854,6 +869,33 @@ static hipError_t gemm_go(const GemmArgs& a, hipStream_t s) {
             if (tiles % 8 == 0) { bw = 4; bt = 2; bg = tiles / 8; }
             else if (tiles % 4 == 0) { bw = 4; bt = 1; bg = tiles / 4; }
             else { bw = 3; bt = 1; bg = tiles / 3; }
+        }
+        if constexpr (NT == 2 && (WT == ET_BF16 || WT == ET_I8)) {
+            // A tile count with no divisor near the CU count (7B gate/up:
+            // 1376 tiles, 172 equal workgroups of eight) leaves CUs without
+            // a stream: split the tiles as evenly as the grid allows over
+            // workgroups of six one-tile waves (7B gate/up: 230 of 5-6
+            // tiles), else seven (13B gate/up: 247 of 6-7), with fewer
+            // workgroups than CUs.  Interleaved forwards against the equal
+            // split: 7B verify T = 32 3.220 -> 3.130 ms (gate/up 31.1 -> 29.5
+            // us), one-node skip-50% draft 1.509 -> 1.474 ms, W8A8 one node
+            // 1.205 -> 1.160 ms (eight nodes 1.233 -> 1.247); 13B T = 32 5.575
+            // -> 5.514 ms, skip-50% one node 2.657 -> 2.640 ms.  A grid of
+            // exactly one workgroup per CU did worse: the 8B gate/up as 256
+            // workgroups of seven 0.3-1.3% slower per forward (it keeps the
+            // equal split), the 7B one as 256 of 5-6 tiles, alone, 32.5
+            // against 31.5-32.0 us for 230-248.  A row's sums do not change.
+            const int g6 = (tiles + 5) / 6, g7 = (tiles + 6) / 7;
+            if (bg < 240 && !a.gv && g6 < 256) {
+                hipLaunchKernelGGL((k_gemm_wide<WT, NT, S1::UC, S1::D, 6, 1, EPI, AT, false, false, false, false, KM, true>),
+                                   dim3(g6), dim3(384), 0, s, a);
+                return hipGetLastError();
+            }
+            if (bg < 240 && !a.gv && g7 < 256) {
+                hipLaunchKernelGGL((k_gemm_wide<WT, NT, S1::UC, S1::D, 7, 1, EPI, AT, false, false, false, false, KM, true>),
+                                   dim3(g7), dim3(448), 0, s, a);
+                return hipGetLastError();
+            }
         }
         if constexpr (NT == 2 && (WT == ET_BF16 || WT == ET_I8)) {
             if (a.gv && a.T == 1) {
