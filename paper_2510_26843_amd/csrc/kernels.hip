@@ -839,9 +839,53 @@ static hipError_t gemm_go(const GemmArgs& a, hipStream_t s) {
         // tiles (waves x tiles per wave) with the most workgroups up to 256,
         // else 4x2.
         const int tiles = a.N / 16;
+        static const int opt[4][2] = {{4, 1}, {3, 1}, {4, 2}, {3, 2}};
+        int bw = 0, bt = 0, bg = 0;
+        for (const auto& o : opt) {
+            const int per = o[0] * o[1];
+            if (tiles % per == 0 && tiles / per <= 256 && tiles / per > bg) { bw = o[0]; bt = o[1]; bg = tiles / per; }
+        }
+        if (!bg) {
+            if (tiles % 8 == 0) { bw = 4; bt = 2; bg = tiles / 8; }
+            else if (tiles % 4 == 0) { bw = 4; bt = 1; bg = tiles / 4; }
+            else { bw = 3; bt = 1; bg = tiles / 3; }
+        }
+        if constexpr (WT == ET_BF16 || WT == ET_I8) {
+            // A tile count with no divisor near the CU count (7B gate/up:
+            // 1376 tiles, 172 equal workgroups of eight) leaves CUs without
+            // a stream: split the tiles as evenly as the grid allows over
+            // workgroups of six one-tile waves (7B gate/up: 230 of 5-6
+            // tiles), else seven (13B gate/up: 247 of 6-7), with fewer
+            // workgroups than CUs.  Interleaved forwards against the equal
+            // split: 7B verify T = 32 3.220 -> 3.130 ms (gate/up 31.1 -> 29.5
+            // us), one-node skip-50% draft 1.509 -> 1.474 ms, W8A8 one node
+            // 1.205 -> 1.160 ms (eight nodes 1.233 -> 1.247); 13B T = 32 5.575
+            // -> 5.514 ms, skip-50% one node 2.657 -> 2.640 ms.  Above 32 rows
+            // it also beats the two-waves-per-SIMD form below (172 workgroups
+            // of eight): 7B T = 64 3.739 -> 3.591 ms, T = 128 5.249 -> 5.126 ms
+            // (ctx 512), 13B T = 64 6.339 -> 6.272 ms (T = 128 unchanged).  A grid of
+            // exactly one workgroup per CU did worse: the 8B gate/up as 256
+            // workgroups of seven 0.3-1.3% slower per forward (it keeps the
+            // equal split), the 7B one as 256 of 5-6 tiles, alone, 32.5
+            // against 31.5-32.0 us for 230-248.  A row's sums do not change.
+            constexpr int EUC = NT == 8 ? 2 : S1::UC;  // the stage of the two-waves-per-SIMD form at 8 column tiles
+            const int g6 = (tiles + 5) / 6, g7 = (tiles + 6) / 7;
+            const bool gv1 = a.gv && a.T == 1;  // the GEMV-style tiles take one-row calls
+            if (bg < 240 && !gv1 && g6 < 256) {
+                hipLaunchKernelGGL((k_gemm_wide<WT, NT, EUC, S1::D, 6, 1, EPI, AT, false, false, false, false, KM, true>),
+                                   dim3(g6), dim3(384), 0, s, a);
+                return hipGetLastError();
+            }
+            if (bg < 240 && !gv1 && g7 < 256) {
+                hipLaunchKernelGGL((k_gemm_wide<WT, NT, EUC, S1::D, 7, 1, EPI, AT, false, false, false, false, KM, true>),
+                                   dim3(g7), dim3(448), 0, s, a);
+                return hipGetLastError();
+            }
+        }
         if constexpr (WT == ET_BF16 && NT >= 4) {
             // Trees of more than 32 rows do 2-4x the MFMA and LDS work per
-            // weight byte: two waves per SIMD (workgroups of 8 one-tile
+            // weight byte (matrices the even split above does not take):
+            // two waves per SIMD (workgroups of 8 one-tile
             // waves, or 6 for 8 column tiles where 8 does not divide the
             // tile count into at least 128 workgroups) let one wave's MFMA
             // and LDS reads run under the other's loads.  Measured alone on
@@ -856,44 +900,6 @@ static hipError_t gemm_go(const GemmArgs& a, hipStream_t s) {
             if (NT == 8 && tiles % 6 == 0 && tiles / 6 >= 96 && tiles / 6 <= 256) {
                 hipLaunchKernelGGL((k_gemm_wide<WT, NT, 2, 4, 6, 1, EPI, AT, false, false, false, false, KM>), dim3(tiles / 6), dim3(384), 0, s,
                                    a);
-                return hipGetLastError();
-            }
-        }
-        static const int opt[4][2] = {{4, 1}, {3, 1}, {4, 2}, {3, 2}};
-        int bw = 0, bt = 0, bg = 0;
-        for (const auto& o : opt) {
-            const int per = o[0] * o[1];
-            if (tiles % per == 0 && tiles / per <= 256 && tiles / per > bg) { bw = o[0]; bt = o[1]; bg = tiles / per; }
-        }
-        if (!bg) {
-            if (tiles % 8 == 0) { bw = 4; bt = 2; bg = tiles / 8; }
-            else if (tiles % 4 == 0) { bw = 4; bt = 1; bg = tiles / 4; }
-            else { bw = 3; bt = 1; bg = tiles / 3; }
-        }
-        if constexpr (NT == 2 && (WT == ET_BF16 || WT == ET_I8)) {
-            // A tile count with no divisor near the CU count (7B gate/up:
-            // 1376 tiles, 172 equal workgroups of eight) leaves CUs without
-            // a stream: split the tiles as evenly as the grid allows over
-            // workgroups of six one-tile waves (7B gate/up: 230 of 5-6
-            // tiles), else seven (13B gate/up: 247 of 6-7), with fewer
-            // workgroups than CUs.  Interleaved forwards against the equal
-            // split: 7B verify T = 32 3.220 -> 3.130 ms (gate/up 31.1 -> 29.5
-            // us), one-node skip-50% draft 1.509 -> 1.474 ms, W8A8 one node
-            // 1.205 -> 1.160 ms (eight nodes 1.233 -> 1.247); 13B T = 32 5.575
-            // -> 5.514 ms, skip-50% one node 2.657 -> 2.640 ms.  A grid of
-            // exactly one workgroup per CU did worse: the 8B gate/up as 256
-            // workgroups of seven 0.3-1.3% slower per forward (it keeps the
-            // equal split), the 7B one as 256 of 5-6 tiles, alone, 32.5
-            // against 31.5-32.0 us for 230-248.  A row's sums do not change.
-            const int g6 = (tiles + 5) / 6, g7 = (tiles + 6) / 7;
-            if (bg < 240 && !a.gv && g6 < 256) {
-                hipLaunchKernelGGL((k_gemm_wide<WT, NT, S1::UC, S1::D, 6, 1, EPI, AT, false, false, false, false, KM, true>),
-                                   dim3(g6), dim3(384), 0, s, a);
-                return hipGetLastError();
-            }
-            if (bg < 240 && !a.gv && g7 < 256) {
-                hipLaunchKernelGGL((k_gemm_wide<WT, NT, S1::UC, S1::D, 7, 1, EPI, AT, false, false, false, false, KM, true>),
-                                   dim3(g7), dim3(448), 0, s, a);
                 return hipGetLastError();
             }
         }

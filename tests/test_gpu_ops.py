@@ -37,15 +37,16 @@ def _gemm_bound(x64, w64):
 
 # N >= 8192 with N/16 a multiple of 3 or 4 takes the multi-tile workgroup
 # variant: 4 waves x 1 tile (8192, 8256), 3 x 1 (8208, 12288), 4 x 2 (16512),
-# 3 x 2 (24480); 8240 and smaller N split K inside a one-tile workgroup.  Up
-# to 32 rows, a tile count whose equal split leaves CUs idle spreads evenly
+# 3 x 2 (24480); 8240 and smaller N split K inside a one-tile workgroup.  At
+# any row count, a tile count whose equal split leaves CUs idle spreads evenly
 # over fewer than 256 workgroups of six one-tile waves (22016: 230 workgroups
-# of 5-6 tiles) or seven (27648: 247 of 6-7); 28672 keeps the 4 x 2 split
+# of 5-6 tiles) or seven (27648: 247 of 6-7); 28672 keeps the equal split
 @pytest.mark.parametrize("N,K,T", [(64, 4096, 32), (48, 688, 5), (32, 256, 1), (16, 1376, 17), (64, 512, 128),
                                    (80, 11008, 64), (32, 128, 100), (8192, 512, 32), (8256, 256, 5),
                                    (8192, 384, 128), (8208, 256, 9), (8320, 128, 1), (16512, 256, 32),
                                    (16512, 128, 100), (12288, 256, 32), (24480, 128, 20), (8240, 128, 3),
-                                   (22016, 256, 32), (27648, 128, 7), (28672, 128, 20),
+                                   (22016, 256, 32), (27648, 128, 7), (28672, 128, 20), (22016, 256, 64),
+                                   (22016, 128, 100), (27648, 128, 128),
                                    # one row: the GEMV-style tiles (4x1, 3x2, 3x1 and 4x2 workgroups)
                                    (16512, 256, 1), (12288, 512, 1), (22016, 4096, 1)])
 def test_gemm_bf16(N, K, T):
@@ -78,6 +79,7 @@ def test_gemm_f32_and_residual(N, K, T):
 @pytest.mark.parametrize("N,K,T", [(64, 4096, 32), (48, 688, 5), (16, 13824, 3), (32, 256, 100), (16, 5120, 64),
                                    (8192, 512, 32), (8256, 256, 1), (8192, 256, 65), (16512, 256, 17),
                                    (12288, 128, 5), (24480, 128, 33), (22016, 256, 17), (27648, 128, 32),
+                                   (22016, 256, 40),
                                    # one row: the GEMV-style tiles (exact int32 dot4 sums)
                                    (16512, 256, 1), (12288, 512, 1), (22016, 4096, 1)])
 def test_gemm_int8_bit_exact(N, K, T):
