@@ -853,10 +853,12 @@ static hipError_t gemm_go(const GemmArgs& a, hipStream_t s) {
         if constexpr (WT == ET_BF16 || WT == ET_I8) {
             // A tile count with no divisor near the CU count (7B gate/up:
             // 1376 tiles, 172 equal workgroups of eight) leaves CUs without
-            // a stream: split the tiles as evenly as the grid allows over
-            // workgroups of six one-tile waves (7B gate/up: 230 of 5-6
-            // tiles), else seven (13B gate/up: 247 of 6-7), with fewer
-            // workgroups than CUs.  Interleaved forwards against the equal
+            // a stream while the others carry eight tiles: split the tiles
+            // as evenly as the grid allows over fewer workgroups than CUs,
+            // of six one-tile waves (7B gate/up: 230 of 5-6 tiles), else
+            // seven (13B gate/up: 247 of 6-7), where that lowers a CU's
+            // share below the equal split's (a CU's share, not the grid,
+            // sets the time: the 7B QKV's 256 workgroups of three stay).  Interleaved forwards against the equal
             // split: 7B verify T = 32 3.220 -> 3.130 ms (gate/up 31.1 -> 29.5
             // us), one-node skip-50% draft 1.509 -> 1.474 ms, W8A8 one node
             // 1.205 -> 1.160 ms (eight nodes 1.233 -> 1.247); 13B T = 32 5.575
@@ -871,12 +873,13 @@ static hipError_t gemm_go(const GemmArgs& a, hipStream_t s) {
             constexpr int EUC = NT == 8 ? 2 : S1::UC;  // the stage of the two-waves-per-SIMD form at 8 column tiles
             const int g6 = (tiles + 5) / 6, g7 = (tiles + 6) / 7;
             const bool gv1 = a.gv && a.T == 1;  // the GEMV-style tiles take one-row calls
-            if (bg < 240 && !gv1 && g6 < 256) {
+            const int share = bw * bt;  // tiles per workgroup of the equal split
+            if (share > 6 && !gv1 && g6 < 256) {
                 hipLaunchKernelGGL((k_gemm_wide<WT, NT, EUC, S1::D, 6, 1, EPI, AT, false, false, false, false, KM, true>),
                                    dim3(g6), dim3(384), 0, s, a);
                 return hipGetLastError();
             }
-            if (bg < 240 && !gv1 && g7 < 256) {
+            if (share > 7 && !gv1 && g7 < 256) {
                 hipLaunchKernelGGL((k_gemm_wide<WT, NT, EUC, S1::D, 7, 1, EPI, AT, false, false, false, false, KM, true>),
                                    dim3(g7), dim3(448), 0, s, a);
                 return hipGetLastError();

@@ -38,9 +38,10 @@ def _gemm_bound(x64, w64):
 # N >= 8192 with N/16 a multiple of 3 or 4 takes the multi-tile workgroup
 # variant: 4 waves x 1 tile (8192, 8256), 3 x 1 (8208, 12288), 4 x 2 (16512),
 # 3 x 2 (24480); 8240 and smaller N split K inside a one-tile workgroup.  At
-# any row count, a tile count whose equal split leaves CUs idle spreads evenly
-# over fewer than 256 workgroups of six one-tile waves (22016: 230 workgroups
-# of 5-6 tiles) or seven (27648: 247 of 6-7); 28672 keeps the equal split
+# any row count, a tile count whose equal split gives a workgroup more than
+# six (seven) tiles spreads evenly over fewer than 256 workgroups of six
+# (seven) one-tile waves (22016: 230 workgroups of 5-6 tiles; 27648: 247 of
+# 6-7); 28672 keeps the equal split, as do the smaller matrices above
 @pytest.mark.parametrize("N,K,T", [(64, 4096, 32), (48, 688, 5), (32, 256, 1), (16, 1376, 17), (64, 512, 128),
                                    (80, 11008, 64), (32, 128, 100), (8192, 512, 32), (8256, 256, 5),
                                    (8192, 384, 128), (8208, 256, 9), (8320, 128, 1), (16512, 256, 32),
