@@ -857,15 +857,16 @@ static hipError_t gemm_go(const GemmArgs& a, hipStream_t s) {
             // as evenly as the grid allows over fewer workgroups than CUs,
             // of six one-tile waves (7B gate/up: 230 of 5-6 tiles), else
             // seven (13B gate/up: 247 of 6-7), where that lowers a CU's
-            // share below the equal split's (a CU's share, not the grid,
-            // sets the time: the 7B QKV's 256 workgroups of three stay).  Interleaved forwards against the equal
-            // split: 7B verify T = 32 3.220 -> 3.130 ms (gate/up 31.1 -> 29.5
-            // us), one-node skip-50% draft 1.509 -> 1.474 ms, W8A8 one node
-            // 1.205 -> 1.160 ms (eight nodes 1.233 -> 1.247); 13B T = 32 5.575
-            // -> 5.514 ms, skip-50% one node 2.657 -> 2.640 ms.  Above 32 rows
-            // it also beats the two-waves-per-SIMD form below (172 workgroups
-            // of eight): 7B T = 64 3.739 -> 3.591 ms, T = 128 5.249 -> 5.126 ms
-            // (ctx 512), 13B T = 64 6.339 -> 6.272 ms (T = 128 unchanged).  A grid of
+            // share below the equal split's.  A CU's share, not the grid,
+            // sets the time: the 7B QKV's 256 workgroups of three stay.
+            // Interleaved forwards against the equal split: 7B verify T = 32
+            // 3.220 -> 3.130 ms (gate/up 31.1 -> 29.5 us), one-node skip-50%
+            // draft 1.509 -> 1.474 ms, W8A8 one node 1.205 -> 1.160 ms (eight
+            // nodes 1.233 -> 1.247); 13B T = 32 5.575 -> 5.514 ms, skip-50%
+            // one node 2.657 -> 2.640 ms.  Above 32 rows it also beats the
+            // two-waves-per-SIMD form below (172 workgroups of eight): 7B
+            // T = 64 3.739 -> 3.591 ms, T = 128 5.249 -> 5.126 ms (ctx 512),
+            // 13B T = 64 6.339 -> 6.272 ms (T = 128 unchanged).  A grid of
             // exactly one workgroup per CU did worse: the 8B gate/up as 256
             // workgroups of seven 0.3-1.3% slower per forward (it keeps the
             // equal split), the 7B one as 256 of 5-6 tiles, alone, 32.5
@@ -888,8 +889,8 @@ static hipError_t gemm_go(const GemmArgs& a, hipStream_t s) {
         if constexpr (WT == ET_BF16 && NT >= 4) {
             // Trees of more than 32 rows do 2-4x the MFMA and LDS work per
             // weight byte (matrices the even split above does not take):
-            // two waves per SIMD (workgroups of 8 one-tile
-            // waves, or 6 for 8 column tiles where 8 does not divide the
+            // two waves per SIMD (workgroups of 8 one-tile waves, or 6 for 8
+            // column tiles where 8 does not divide the
             // tile count into at least 128 workgroups) let one wave's MFMA
             // and LDS reads run under the other's loads.  Measured alone on
             // the 7B shapes: gate/up T = 128 53.3 -> 43.8 us, T = 64 35.1 ->
